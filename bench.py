@@ -1,0 +1,221 @@
+"""Benchmark of the IF4 quantized-linear hot path on one MI355X.
+
+One step = one forward pass of an IF4 linear layer at the MLP up-projection
+shape: quantize the bf16 activations A [8192, 4096] and weights W
+[14336, 4096] along K (tensor max pass + quantize pass each), then the
+IF4 x IF4 GEMM Y = A_hat W_hat^T with bf16 output.  Inputs are resident in
+HBM before timing starts.  `value` is the step's whole-job throughput,
+2*M*N*K / step time.
+
+Also reported (one JSON line): per-kernel times from HIP events on the
+launch stream, the roofline of the dominant kernel (the GEMM, MFMA-bound) and
+of the quantizer (HBM-bound), the same kernels in NVFP4 mode, and the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "IF4 quantize GB/s (%HBM peak) + IF4 GEMM TFLOP/s (%MFMA peak), 1 MI355X"
+HBM_PEAK_GBS = 8000.0
+FP16_MFMA_PEAK_TFLOPS = 2500.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-rows", type=int, default=512,
+                   help="activation rows of the CPU-oracle sample")
+    p.add_argument("--small", action="store_true", help="1/8-size shapes (quick checks)")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the multi-GPU layout "
+              "is described in DESIGN.md, not run.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2603_28765_amd import ops, workloads
+
+    torch.cuda.set_device(0)
+    div = 8 if args.small else 1
+    M, N, K = 8192 // div, 14336 // div, 4096 // div
+    w = workloads.fwd_mlp(M, N, K)
+    A = w.tensors["A"].cuda()
+    W = w.tensors["W"].cuda()
+    dev = A.device
+
+    def alloc(fmt, rows, cols):
+        return ops.Packed(fmt, torch.empty((rows, cols * ops.BITS[fmt] // 8), dtype=torch.uint8, device=dev),
+                          torch.empty((rows, cols // 16), dtype=torch.uint8, device=dev),
+                          torch.empty(1, dtype=torch.float32, device=dev), rows, cols)
+
+    ws = torch.empty(4096, dtype=torch.uint8, device=dev)
+    Y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+
+    def run(fmt, pa, pw, ev=None):
+        q = ops.if4_quantize if fmt == ops.IF4 else ops.nvfp4_quantize
+        g = ops.if4_gemm if fmt == ops.IF4 else ops.nvfp4_gemm
+        if ev: ev[0].record()
+        q(A, out=pa, workspace=ws)
+        if ev: ev[1].record()
+        q(W, out=pw, workspace=ws)
+        if ev: ev[2].record()
+        g(pa, pw, ops.BF16, Y)
+        if ev: ev[3].record()
+
+    def timed(fmt, steps, warmup):
+        pa, pw = alloc(fmt, M, K), alloc(fmt, N, K)
+        for _ in range(warmup):
+            run(fmt, pa, pw)
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+        t0 = time.perf_counter()
+        for i in range(steps):
+            run(fmt, pa, pw, evs[i])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        qa = np.mean([e[0].elapsed_time(e[1]) for e in evs]) * 1e-3
+        qw = np.mean([e[1].elapsed_time(e[2]) for e in evs]) * 1e-3
+        gm = np.mean([e[2].elapsed_time(e[3]) for e in evs]) * 1e-3
+        step = np.mean([e[0].elapsed_time(e[3]) for e in evs]) * 1e-3
+        return {"wall_s": wall, "step_s": step, "quant_A_s": qa, "quant_W_s": qw, "gemm_s": gm}
+
+    # single-pass quantize kernel alone (alpha supplied): the HBM-bound kernel
+    def timed_scale_in(fmt, x, steps, warmup):
+        p = alloc(fmt, x.shape[0], x.shape[1])
+        q = ops.if4_quantize if fmt == ops.IF4 else ops.nvfp4_quantize
+        q(x, out=p, workspace=ws)
+        ts = p.tensor_scale.clone()
+        flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device=dev)
+        times = []
+        for i in range(warmup + steps):
+            flush.fill_(i & 0xFF)  # evict the 256 MB infinity cache
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            q(x, flags=ops.SCALE_IN, tensor_scale=ts, out=p)
+            e1.record()
+            torch.cuda.synchronize()
+            if i >= warmup:
+                times.append(e0.elapsed_time(e1) * 1e-3)
+        del flush
+        return float(np.mean(times))
+
+    res = timed(ops.IF4, args.steps, args.warmup)
+    res_nv = timed(ops.NVFP4, max(5, args.steps // 2), 2)
+    n_a, n_w = M * K, N * K
+    flops = 2.0 * M * N * K
+    qbytes_2pass = lambda n: n * (2 + 2 + 0.5 + 1 / 16)  # read for max, read + write codes/scales
+    qbytes_1pass = lambda n: n * (2 + 0.5 + 1 / 16)
+    t_w_1p = timed_scale_in(ops.IF4, W, max(5, args.steps // 2), 2)
+    t_w_1p_nv = timed_scale_in(ops.NVFP4, W, max(5, args.steps // 2), 2)
+
+    gemm_tflops = flops / res["gemm_s"] / 1e12
+    out = {
+        "metric": METRIC,
+        "value": round(flops / res["step_s"] / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(res["step_s"] * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp16",
+        "data": "synthetic (seeded; activations t(4) x lognormal channel scales, weights N(0,0.02^2))",
+        "config": {"workload": f"fwd_mlp_up_{M}x{N}x{K}", "format": "IF4", "M": M, "N": N, "K": K,
+                   "quantize": "row-wise along K, round-to-nearest, alpha from tensor max",
+                   "out": "bf16"},
+        "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2),
+                     "peak": FP16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(gemm_tflops / FP16_MFMA_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "gemm_tn<IF4, bf16 out>"},
+        "roofline_quantize": {
+            "bound": "hbm", "kernel": "quantize_rows<IF4> (alpha supplied, single pass, W)",
+            "achieved": round(qbytes_1pass(n_w) / t_w_1p / 1e9, 1), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(qbytes_1pass(n_w) / t_w_1p / 1e9 / HBM_PEAK_GBS, 4),
+            "traffic": None},
+        "components": {
+            "if4": {"quant_A_us": round(res["quant_A_s"] * 1e6, 2),
+                    "quant_A_GBps_2pass": round(qbytes_2pass(n_a) / res["quant_A_s"] / 1e9, 1),
+                    "quant_W_us": round(res["quant_W_s"] * 1e6, 2),
+                    "quant_W_GBps_2pass": round(qbytes_2pass(n_w) / res["quant_W_s"] / 1e9, 1),
+                    "quant_W_1pass_us": round(t_w_1p * 1e6, 2),
+                    "gemm_us": round(res["gemm_s"] * 1e6, 2),
+                    "gemm_TFLOPs": round(gemm_tflops, 2)},
+            "nvfp4": {"quant_A_us": round(res_nv["quant_A_s"] * 1e6, 2),
+                      "quant_W_us": round(res_nv["quant_W_s"] * 1e6, 2),
+                      "quant_W_1pass_us": round(t_w_1p_nv * 1e6, 2),
+                      "quant_W_1pass_GBps": round(qbytes_1pass(n_w) / t_w_1p_nv / 1e9, 1),
+                      "gemm_us": round(res_nv["gemm_s"] * 1e6, 2),
+                      "gemm_TFLOPs": round(flops / res_nv["gemm_s"] / 1e12, 2),
+                      "step_ms": round(res_nv["step_s"] * 1e3, 4)},
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, M, N, K, args.cpu_rows)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, M, N, K, rows):
+    """The CPU oracle on a bounded sample of the same step: quantize `rows`
+    rows of A and rows*N/M rows of W (C oracle, one thread), then the fp64
+    reference product of the sampled A rows with the sampled W rows (numpy
+    BLAS).  Scaled to the full step: the sample is rows/M of the quantize
+    work and (rows/M)^2 of the GEMM work is not representative, so the GEMM
+    sample is rows x N x K (all of W), i.e. rows/M of the GEMM flops."""
+    import numpy as np
+    import torch
+
+    import oracle as O
+    from threadpoolctl import threadpool_info
+
+    def bits(t):
+        return t.contiguous().view(torch.int16).numpy().view(np.uint16)
+
+    a = bits(w.tensors["A"][:rows])
+    wr = max(16, rows * N // M)
+    wt = bits(w.tensors["W"][:wr])
+    t0 = time.perf_counter()
+    ca, sa, aa = O.quantize(a, O.FMT_IF4)
+    cw, sw, aw = O.quantize(wt, O.FMT_IF4)
+    t_q = time.perf_counter() - t0
+    # GEMM reference: the sampled rows of A against all of W's rows (dequantized
+    # from the oracle quantization of the full W, outside the timing)
+    cwf, swf, awf = O.quantize(bits(w.tensors["W"]), O.FMT_IF4)
+    Wd = O.dequantize(cwf, swf, awf, O.FMT_IF4, np.float64)
+    t1 = time.perf_counter()
+    Ad = O.dequantize(ca, sa, aa, O.FMT_IF4, np.float64)
+    _ = Ad @ Wd.T
+    t_g = time.perf_counter() - t1
+    blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    frac = rows / M
+    t_full = t_q / frac + t_g / frac
+    flops = 2.0 * M * N * K
+    return {"value": round(flops / t_full / 1e12, 6), "unit": "TFLOP/s",
+            "cores": int(blas_threads), "kind": "oracle",
+            "sample": f"IF4 quantize of {rows} rows of A and {wr} rows of W (C oracle, 1 thread, "
+                      f"{t_q:.2f} s) + fp64 reference GEMM of {rows} rows of A against all {N} rows "
+                      f"of W (numpy BLAS, {blas_threads} threads, {t_g:.2f} s); scaled by M/{rows}",
+            "seconds": round(t_q + t_g, 2)}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,196 @@
+/*
+ * ifq.h -- C ABI of the IF4 quantized-linear hot path on AMD Instinct
+ * MI355X (gfx950): the adaptive block-scaled quantizer and the block-scaled
+ * GEMM of "Adaptive Block-Scaled Data Types", with NVFP4, IF3 and IF6
+ * variants for comparison.
+ *
+ * Format (Sec. 3).  A tensor X is stored as
+ *   - one FP32 tensor scale  alpha = max|X| / (M_FP * 448)           (Eq. 1)
+ *   - one byte per group of 16 values along the grouped axis K:
+ *       bits 0-6  E4M3 magnitude of the group scale
+ *                 Delta = max|X_g| / (alpha * M_FP) rounded to E4M3  (Eq. 2)
+ *       bit 7     1 = the group holds scaled integers, 0 = FP elements
+ *                 (the otherwise unused sign bit of the scale, Sec. 3)
+ *   - 16 element codes per group, packed as a little-endian bit stream
+ *     (code j at bits [j*b, j*b + b) of the group's 2b bytes).  For IF4 that
+ *     puts element 2i in the low nibble of byte i.  FP codes are sign-
+ *     magnitude ExMy; INT codes are two's complement in [-M_I, M_I].
+ * A value decodes as  q * Delta * alpha  for FP groups and
+ * q * Delta * (M_FP / M_I) * alpha  for INT groups (the 6/7 method, Sec. 3;
+ * factors 4/3, 7.5/31 and 28/31 for IF3 and IF6 per the Sec. 5.1 footnote).
+ *
+ *   format      bits  FP element     M_FP   INT    M_I
+ *   IF4         4     E2M1           6      INT4   7     (Sec. 3, Fig. 3a)
+ *   NVFP4       4     E2M1           6      --     --    (FP only; bit 7 = 0)
+ *   IF3         3     E2M0           4      INT3   3     (Sec. 5.1, Table 6)
+ *   IF6_E2M3    6     E2M3           7.5    INT6   31    (Sec. 5.1, Table 6)
+ *   IF6_E3M2    6     E3M2           28     INT6   31    (Sec. 5.1, Table 6)
+ *
+ * Layouts (row-major, no padding):
+ *   codes   uint8 [R, K * bits / 8]      scales  uint8 [R, K / 16]
+ * where R is the number of logical rows and K (a multiple of 16) is the
+ * grouped axis.
+ *
+ * Conventions for every call:
+ *   - Pointers marked (device) are HIP device pointers; the caller allocates
+ *     and owns all memory; the library keeps no state and allocates nothing.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  All
+ *     work is enqueued asynchronously on it; no call synchronises.
+ *   - Arguments are validated on the host before anything is enqueued; a
+ *     negative return value means nothing was launched.  IFQ_EHIP means a
+ *     launch was rejected by the runtime (outputs are then undefined).
+ *     Faults inside kernels surface at the caller's next synchronisation.
+ *   - Inputs must be finite.
+ *   - Calls are thread-safe; concurrent calls must not share outputs or a
+ *     workspace.
+ */
+#ifndef IFQ_H
+#define IFQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define IFQ_ABI_VERSION 1
+
+typedef enum ifq_status {
+    IFQ_OK = 0,
+    IFQ_EINVAL = -1,        /* null pointer, unknown flag, format or dtype */
+    IFQ_ESHAPE = -2,        /* negative size, K not a multiple of 16, ld too small, too large */
+    IFQ_EALIGN = -3,        /* a pointer or leading dimension breaks the alignment rules */
+    IFQ_EUNSUPPORTED = -4,  /* valid but not implemented combination */
+    IFQ_EHIP = -5,          /* the HIP runtime rejected a launch */
+    IFQ_EWORKSPACE = -6     /* workspace missing or smaller than required */
+} ifq_status;
+
+typedef enum ifq_format {
+    IFQ_FMT_IF4 = 0,
+    IFQ_FMT_NVFP4 = 1,
+    IFQ_FMT_IF3 = 2,
+    IFQ_FMT_IF6_E2M3 = 3,
+    IFQ_FMT_IF6_E3M2 = 4
+} ifq_format;
+
+typedef enum ifq_dtype { IFQ_F32 = 0, IFQ_BF16 = 1 } ifq_dtype;
+
+/* quantizer flags */
+enum {
+    IFQ_RHT = 1u,          /* 16-point random Hadamard transform of each group first */
+    IFQ_SR = 2u,           /* stochastic rounding of both candidates */
+    IFQ_MARGIN_16_17 = 4u, /* scales computed against M_FP * 16/17 (Sec. 4.1) */
+    IFQ_SCALE_IN = 8u,     /* *tensor_scale is an input instead of Eq. 1's output */
+    IFQ_AXIS_STRIDED = 16u /* groups run along rows; output describes X transposed */
+};
+
+/* ------------------------------------------------------------ quantize --
+ * Quantize a bf16 matrix X (rows x cols, row stride ld_x elements).
+ * Follows Eq. 1 and 2 and Fig. 3a of the paper: alpha from the tensor
+ * maximum, Delta per group rounded to E4M3, then for IF formats both an FP
+ * and a scaled-INT candidate with the INT one kept only if its squared
+ * error is strictly smaller (Fig. 3a line 10).
+ *
+ *   x             (device) bf16 [rows, ld_x], ld_x >= cols; row-wise: 16-byte
+ *                 aligned with ld_x % 8 == 0; strided axis: any alignment
+ *   flags         IFQ_* bits above.  IFQ_RHT applies v = (1/4) H16 diag(s) x
+ *                 to every group (Sylvester order H16[i][j] =
+ *                 (-1)^popcount(i&j), s_j = -1 where bit j of rht_signs is
+ *                 set); the tensor scale is then taken over the transformed
+ *                 values.  IFQ_SR draws 16 uniform 16-bit numbers per group
+ *                 from Philox4x32-10 (key = seed, counter = (group index lo,
+ *                 group index hi, block 0/1, 0), group index = position of
+ *                 its scale byte) and shares draw j between the two
+ *                 candidates of element j.
+ *   rht_signs     16-bit sign mask (upper bits must be zero)
+ *   seed          Philox key for IFQ_SR
+ *   codes         (device) uint8 [R, K*bits/8], 16-byte aligned
+ *   scales        (device) uint8 [R, K/16]
+ *                 Row-wise: R = rows, K = cols (cols % 16 == 0).
+ *                 IFQ_AXIS_STRIDED: R = cols, K = rows (rows % 16 == 0): the
+ *                 output is the packed form of X^T, K-major as the GEMM
+ *                 expects (e.g. dY^T and X^T of a weight gradient).
+ *   tensor_scale  (device) one float: written with alpha, or read when
+ *                 IFQ_SCALE_IN is set.  A group whose alpha * Delta is zero or
+ *                 below FLT_MIN (this includes alpha = 0 and an all-zero
+ *                 tensor) is stored as scale 0 and codes 0.
+ *   workspace     (device) at least ifq_quantize_workspace_bytes() bytes,
+ *                 256-byte aligned, no initial contents required; may be
+ *                 NULL when that size is 0.
+ */
+int if4_quantize(const void* x, int64_t rows, int64_t cols, int64_t ld_x, uint32_t flags,
+                 uint32_t rht_signs, uint64_t seed, uint8_t* codes, uint8_t* scales,
+                 float* tensor_scale, void* workspace, size_t workspace_bytes, void* stream);
+
+/* NVFP4 (Fig. 3a lines 1-4 only): same arguments, bit 7 of every scale is 0. */
+int nvfp4_quantize(const void* x, int64_t rows, int64_t cols, int64_t ld_x, uint32_t flags,
+                   uint32_t rht_signs, uint64_t seed, uint8_t* codes, uint8_t* scales,
+                   float* tensor_scale, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Any format (IF3 and IF6 of Sec. 5.1 included); same arguments. */
+int ifx_quantize(int format, const void* x, int64_t rows, int64_t cols, int64_t ld_x,
+                 uint32_t flags, uint32_t rht_signs, uint64_t seed, uint8_t* codes,
+                 uint8_t* scales, float* tensor_scale, void* workspace, size_t workspace_bytes,
+                 void* stream);
+
+/* Bytes of device workspace the quantizer needs (0 with IFQ_SCALE_IN). */
+size_t ifq_quantize_workspace_bytes(int format, int64_t rows, int64_t cols, uint32_t flags);
+
+/* ---------------------------------------------------------- dequantize --
+ * out[r, k] = q * Delta * (M_FP/M_I if INT) * alpha, evaluated as three fp32
+ * multiplies in that order (Fig. 3a lines 5 and 8 with alpha restored); the
+ * bf16 output is the round-to-nearest-even of that fp32 value.
+ *   codes, scales  (device) packed [R, K] as written by the quantizer
+ *   tensor_scale   (device) alpha
+ *   out            (device) [rows, cols] contiguous, fp32 or bf16 (out_dtype),
+ *                  16-byte aligned
+ */
+int if4_dequantize(const uint8_t* codes, const uint8_t* scales, const float* tensor_scale,
+                   int64_t rows, int64_t cols, void* out, int out_dtype, void* stream);
+int nvfp4_dequantize(const uint8_t* codes, const uint8_t* scales, const float* tensor_scale,
+                     int64_t rows, int64_t cols, void* out, int out_dtype, void* stream);
+int ifx_dequantize(int format, const uint8_t* codes, const uint8_t* scales,
+                   const float* tensor_scale, int64_t rows, int64_t cols, void* out,
+                   int out_dtype, void* stream);
+
+/* ---------------------------------------------------------------- GEMM --
+ * C[m, n] = sum_k A[m, k] * B[n, k] over the dequantized values of two
+ * packed operands that share the grouped axis K ("TN": Y = X W^T, or
+ * dW = dY^T X with both operands quantized along the token axis).  This is
+ * the block-scaled dot product of Sec. 5.2: per 16-wide K block the product
+ * of the two group scales, times 1, 6/7 or 36/49 by the two group types,
+ * accumulated in FP32.  Here each element is decoded to an FP16 MFMA operand
+ * that carries its group scale exactly (7 q Delta for FP groups, 6 q Delta
+ * for INT groups), so one FP32 accumulation over all of K applies every
+ * block's scale pair and range alignment; alpha_A * alpha_B / 49 is applied
+ * once at the end.
+ *   a_codes, a_scales  (device) A packed [M, K]; b_* : B packed [N, K]
+ *   a_tensor_scale, b_tensor_scale  (device) alpha of A and of B
+ *   c                  (device) [M, ldc] fp32 or bf16 (out_dtype); ldc >= N
+ *   code pointers 16-byte aligned; K % 16 == 0.
+ * The result is deterministic for a given shape (no split-K atomics).
+ */
+int if4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_tensor_scale,
+             const uint8_t* b_codes, const uint8_t* b_scales, const float* b_tensor_scale,
+             int64_t M, int64_t N, int64_t K, void* c, int64_t ldc, int out_dtype, void* stream);
+int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_tensor_scale,
+               const uint8_t* b_codes, const uint8_t* b_scales, const float* b_tensor_scale,
+               int64_t M, int64_t N, int64_t K, void* c, int64_t ldc, int out_dtype,
+               void* stream);
+int ifx_gemm(int format, const uint8_t* a_codes, const uint8_t* a_scales,
+             const float* a_tensor_scale, const uint8_t* b_codes, const uint8_t* b_scales,
+             const float* b_tensor_scale, int64_t M, int64_t N, int64_t K, void* c,
+             int64_t ldc, int out_dtype, void* stream);
+
+/* ---------------------------------------------------------- host helpers */
+size_t ifq_codes_bytes(int format, int64_t rows, int64_t cols); /* rows * cols * bits / 8 */
+size_t ifq_scales_bytes(int64_t rows, int64_t cols);            /* rows * cols / 16 */
+const char* ifq_status_string(int status);
+int ifq_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IFQ_H */

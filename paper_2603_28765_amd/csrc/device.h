@@ -1,0 +1,347 @@
+// device.h -- gfx950 device helpers for the adaptive block-scaled formats:
+// format traits, E4M3 scale codec, element rounding, Philox4x32-10, the
+// 16-point random Hadamard transform and the per-group quantizer.
+//
+// Every floating-point step is written out explicitly (the library is built
+// with -ffp-contract=off, so no FMA appears unless __builtin_fmaf is
+// called) because the codes must be bit-identical to the format's
+// definition evaluated in binary32.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ifq.h"
+
+namespace ifq {
+
+constexpr int kGroup = 16;
+
+// ------------------------------------------------------------ format traits
+// EB/MB: exponent and mantissa widths of the FP element (ExMy, bias
+// 2^(EB-1)-1, subnormals, no Inf/NaN).  INT elements are two's complement
+// in [-IMAX, IMAX].  c_up = fp32(IMAX / FP_MAX), k_dn =
+// fp32(FP_MAX / IMAX) realise the 6/7 method (Sec. 3) and its IF3/IF6
+// analogues (Sec. 5.1 footnote).
+template <int FMT> struct Fmt;
+template <> struct Fmt<IFQ_FMT_IF4> {
+    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7;
+    static constexpr bool ADAPTIVE = true;
+    static constexpr float FP_MAX = 6.0f;
+};
+template <> struct Fmt<IFQ_FMT_NVFP4> {
+    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7;
+    static constexpr bool ADAPTIVE = false;
+    static constexpr float FP_MAX = 6.0f;
+};
+template <> struct Fmt<IFQ_FMT_IF3> {
+    static constexpr int BITS = 3, EB = 2, MB = 0, IMAX = 3;
+    static constexpr bool ADAPTIVE = true;
+    static constexpr float FP_MAX = 4.0f;
+};
+template <> struct Fmt<IFQ_FMT_IF6_E2M3> {
+    static constexpr int BITS = 6, EB = 2, MB = 3, IMAX = 31;
+    static constexpr bool ADAPTIVE = true;
+    static constexpr float FP_MAX = 7.5f;
+};
+template <> struct Fmt<IFQ_FMT_IF6_E3M2> {
+    static constexpr int BITS = 6, EB = 3, MB = 2, IMAX = 31;
+    static constexpr bool ADAPTIVE = true;
+    static constexpr float FP_MAX = 28.0f;
+};
+
+template <int FMT> struct FmtDerived {
+    using F = Fmt<FMT>;
+    static constexpr int BIAS = (1 << (F::EB - 1)) - 1;
+    static constexpr float C_UP = (float)F::IMAX / F::FP_MAX;
+    static constexpr float K_DN = F::FP_MAX / (float)F::IMAX;
+    static constexpr uint32_t CODE_MASK = (1u << F::BITS) - 1u;
+    static constexpr uint32_t SIGN_BIT = 1u << (F::BITS - 1);
+};
+
+// ------------------------------------------------------------- bit helpers
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// ------------------------------------------------------------ E4M3 scales
+// Nearest E4M3 code to x >= 0, ties to even, saturating at 448 (0x7E).
+__device__ __forceinline__ uint32_t e4m3_encode(float x)
+{
+    if (!(x < 448.0f)) return 0x7Eu;
+    if (x < 0.015625f) {  // below 2^-6: subnormal codes, step 2^-9
+        return (uint32_t)__builtin_rintf(x * 512.0f);  // 0..8; 8 == 2^-6
+    }
+    uint32_t b = __float_as_uint(x);
+    b += 0x7FFFFu + ((b >> 20) & 1u);  // round the mantissa to 3 bits
+    b &= 0xFFF00000u;
+    uint32_t code = ((((b >> 23) & 0xFFu) - 120u) << 3) | ((b >> 20) & 7u);
+    return code < 0x7Eu ? code : 0x7Eu;
+}
+
+// Value of E4M3 code c (bits 0-6; 0x7F never produced).
+__device__ __forceinline__ float e4m3_value(uint32_t c)
+{
+    c &= 0x7Fu;
+    uint32_t e = c >> 3, m = c & 7u;
+    if (e == 0) return (float)m * 0.001953125f;
+    return __uint_as_float(((e + 120u) << 23) | (m << 20));
+}
+
+// --------------------------------------------------------- Philox4x32-10
+// Salmon et al., SC'11.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1)
+{
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+        uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+        c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+    }
+    return c;
+}
+
+// 8 words = 16 draws of 16 bits for group `gi`; draw j = half (j&1) of word j>>1.
+__device__ __forceinline__ void sr_words(uint64_t seed, uint64_t gi, uint32_t (&w)[8])
+{
+    uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    uint4 a = philox4x32_10(make_uint4((uint32_t)gi, (uint32_t)(gi >> 32), 0u, 0u), k0, k1);
+    uint4 b = philox4x32_10(make_uint4((uint32_t)gi, (uint32_t)(gi >> 32), 1u, 0u), k0, k1);
+    w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
+    w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+}
+
+__device__ __forceinline__ float sr_uniform(const uint32_t (&w)[8], int j)
+{
+    uint32_t h = (w[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+    return (float)h * (1.0f / 65536.0f);
+}
+
+// --------------------------------------------------------------- RHT-16
+// v <- (1/4) H16 diag(s) v; Sylvester order, butterfly strides 1, 2, 4, 8.
+__device__ __forceinline__ void rht16(float (&v)[kGroup], uint32_t signs)
+{
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j)
+        v[j] = __uint_as_float(__float_as_uint(v[j]) ^ (((signs >> j) & 1u) << 31));
+#pragma unroll
+    for (int h = 1; h < kGroup; h <<= 1) {
+#pragma unroll
+        for (int i = 0; i < kGroup; ++i) {
+            if (i & h) continue;
+            float a = v[i], b = v[i + h];
+            v[i] = a + b;
+            v[i + h] = a - b;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) v[j] = v[j] * 0.25f;
+}
+
+// ---------------------------------------------------- FP element rounding
+// Magnitude of non-negative FP code `idx`.
+template <int FMT> __device__ __forceinline__ float fp_magnitude(uint32_t idx)
+{
+    using F = Fmt<FMT>;
+    constexpr int BIAS = FmtDerived<FMT>::BIAS;
+    uint32_t E = idx >> F::MB, M = idx & ((1u << F::MB) - 1u);
+    if (E == 0) return (float)M * __uint_as_float((uint32_t)(127 + 1 - BIAS - F::MB) << 23);
+    return __uint_as_float(((E - BIAS + 127u) << 23) | (M << (23 - F::MB)));
+}
+
+// Nearest FP code index to m >= 0 (ties to the even code), saturating.
+template <int FMT> __device__ __forceinline__ uint32_t fp_rtn_index(float m)
+{
+    using F = Fmt<FMT>;
+    if constexpr (F::MB == 1 && F::EB == 2) {
+        // E2M1 midpoints; ">=" where the upper neighbour has the even code
+        return (uint32_t)(m > 0.25f) + (uint32_t)(m >= 0.75f) + (uint32_t)(m > 1.25f) +
+               (uint32_t)(m >= 1.75f) + (uint32_t)(m > 2.5f) + (uint32_t)(m >= 3.5f) +
+               (uint32_t)(m > 5.0f);
+    } else if constexpr (F::MB == 0) {
+        // E2M0 (0, 1, 2, 4): with no mantissa bit the even code decides ties
+        return (uint32_t)(m > 0.5f) + (uint32_t)(m >= 1.5f) + (uint32_t)(m > 3.0f);
+    } else {
+        // ExMy with MB >= 1: round m to a multiple of the local quantum; the
+        // parity of that multiple is the parity of the code.
+        constexpr int BIAS = FmtDerived<FMT>::BIAS;
+        m = fminf(m, F::FP_MAX);
+        int e = (int)((__float_as_uint(m) >> 23) & 0xFFu) - 127;
+        int ee = e > 1 - BIAS ? e : 1 - BIAS;
+        float inv_u = __uint_as_float((uint32_t)(127 - (ee - F::MB)) << 23);
+        float r = __builtin_rintf(m * inv_u);
+        return (uint32_t)(((ee + BIAS) << F::MB) + (int)r - (1 << F::MB));
+    }
+}
+
+// Stochastic rounding of m >= 0 between its grid neighbours lo <= m < hi:
+// up iff u * (hi - lo) < m - lo.
+template <int FMT> __device__ __forceinline__ uint32_t fp_sr_index(float m, float u)
+{
+    using F = Fmt<FMT>;
+    constexpr int BIAS = FmtDerived<FMT>::BIAS;
+    m = fminf(m, F::FP_MAX);
+    int e = (int)((__float_as_uint(m) >> 23) & 0xFFu) - 127;
+    int ee = e > 1 - BIAS ? e : 1 - BIAS;
+    float q = __uint_as_float((uint32_t)(127 + ee - F::MB) << 23);        // grid step
+    float inv_q = __uint_as_float((uint32_t)(127 - (ee - F::MB)) << 23);
+    float lo_r = __builtin_floorf(m * inv_q);
+    float lo = lo_r * q;
+    int r = (int)lo_r + ((u * q < m - lo) ? 1 : 0);
+    return (uint32_t)(((ee + BIAS) << F::MB) + r - (1 << F::MB));
+}
+
+// ---------------------------------------------------- group quantizer
+// One group of 16 (already transformed) values under tensor scale alpha.
+// denom = fp32(alpha * M) with M = M_FP (or M_FP*16/17).  Writes the 16 codes
+// (low bits of each byte) and returns the scale byte.  Fig. 3a: Delta, the FP
+// candidate, the INT candidate scaled by c_up, and INT iff its error is
+// strictly smaller.  Errors are sums of squares in x-bar units, accumulated
+// in element order with fused multiply-adds.
+template <int FMT, bool SR>
+__device__ __forceinline__ uint32_t quantize_group(const float (&v)[kGroup], float alpha,
+                                                   float denom, const uint32_t (&w)[8],
+                                                   uint32_t (&code)[kGroup])
+{
+    using F = Fmt<FMT>;
+    using D = FmtDerived<FMT>;
+    float amax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(v[j]));
+    uint32_t dcode = e4m3_encode(amax / denom);
+    float s = alpha * e4m3_value(dcode);
+    if (!(s >= 1.17549435e-38f)) {
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) code[j] = 0;
+        return 0;
+    }
+    float inv = 1.0f / s;
+
+    float ef = 0.0f, ei = 0.0f;
+    uint32_t cf[kGroup], ci[kGroup];
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+        float xb = v[j] * inv;
+        float m = fabsf(xb);
+        uint32_t neg = __float_as_uint(xb) >> 31;
+        // FP candidate
+        uint32_t idx;
+        if constexpr (SR)
+            idx = fp_sr_index<FMT>(m, sr_uniform(w, j));
+        else
+            idx = fp_rtn_index<FMT>(m);
+        cf[j] = (neg ? D::SIGN_BIT : 0u) | idx;
+        float q = __uint_as_float(__float_as_uint(fp_magnitude<FMT>(idx)) | (neg << 31));
+        float d = q - xb;
+        ef = __builtin_fmaf(d, d, ef);
+        if constexpr (F::ADAPTIVE) {
+            // INT candidate
+            float r;
+            if constexpr (SR) {
+                float y = xb * D::C_UP;
+                float a = fabsf(y);
+                float lo = __builtin_floorf(a);
+                float rr = (sr_uniform(w, j) < a - lo) ? lo + 1.0f : lo;
+                rr = fminf(rr, (float)F::IMAX);
+                r = (y < 0.0f) ? -rr : rr;
+            } else {
+                float xc = __builtin_amdgcn_fmed3f(xb, -F::FP_MAX, F::FP_MAX);
+                float t = __builtin_fmaf(xc, D::C_UP, 12582912.0f);  // rint(xc*c_up) + 1.5*2^23
+                r = t - 12582912.0f;
+            }
+            ci[j] = (uint32_t)(int)r & D::CODE_MASK;
+            float di = __builtin_fmaf(r, D::K_DN, -xb);
+            ei = __builtin_fmaf(di, di, ei);
+        }
+    }
+    bool use_int = F::ADAPTIVE && (ei < ef);
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) code[j] = use_int ? ci[j] : cf[j];
+    return dcode | (use_int ? 0x80u : 0u);
+}
+
+// Dense little-endian bit stream of 16 codes of BITS bits: 2*BITS bytes,
+// written as BITS/2 32-bit words for even BITS and as 3 16-bit halves for 3.
+template <int BITS> struct Packed;
+template <> struct Packed<4> { uint32_t w[2]; };
+template <> struct Packed<6> { uint32_t w[3]; };
+template <> struct Packed<3> { uint32_t w[2]; };  // 48 bits: w[0] full, w[1] low 16
+
+template <int BITS> __device__ __forceinline__ Packed<BITS> pack16(const uint32_t (&c)[kGroup])
+{
+    Packed<BITS> p;
+    uint64_t lo = 0, hi = 0;
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+        int bit = j * BITS;
+        if (bit < 64) {
+            lo |= (uint64_t)c[j] << bit;
+            if (bit + BITS > 64) hi |= (uint64_t)c[j] >> (64 - bit);
+        } else {
+            hi |= (uint64_t)c[j] << (bit - 64);
+        }
+    }
+    if constexpr (BITS == 4) {
+        p.w[0] = (uint32_t)lo; p.w[1] = (uint32_t)(lo >> 32);
+    } else if constexpr (BITS == 6) {
+        p.w[0] = (uint32_t)lo; p.w[1] = (uint32_t)(lo >> 32); p.w[2] = (uint32_t)hi;
+    } else {
+        p.w[0] = (uint32_t)lo; p.w[1] = (uint32_t)(lo >> 32);
+    }
+    return p;
+}
+
+template <int BITS> __device__ __forceinline__ void store_packed(uint8_t* dst, const Packed<BITS>& p)
+{
+    if constexpr (BITS == 4) {
+        *reinterpret_cast<uint2*>(dst) = make_uint2(p.w[0], p.w[1]);
+    } else if constexpr (BITS == 6) {
+        // 12 bytes at a 4-byte aligned address (group pitch 12)
+        uint32_t* d = reinterpret_cast<uint32_t*>(dst);
+        d[0] = p.w[0]; d[1] = p.w[1]; d[2] = p.w[2];
+    } else {
+        // 6 bytes at a 2-byte aligned address (group pitch 6)
+        uint16_t* d = reinterpret_cast<uint16_t*>(dst);
+        d[0] = (uint16_t)p.w[0]; d[1] = (uint16_t)(p.w[0] >> 16); d[2] = (uint16_t)p.w[1];
+    }
+}
+
+template <int BITS> __device__ __forceinline__ void load_unpack16(const uint8_t* src, uint32_t (&c)[kGroup])
+{
+    uint64_t lo, hi = 0;
+    if constexpr (BITS == 4) {
+        uint2 t = *reinterpret_cast<const uint2*>(src);
+        lo = (uint64_t)t.x | ((uint64_t)t.y << 32);
+    } else if constexpr (BITS == 6) {
+        const uint32_t* s = reinterpret_cast<const uint32_t*>(src);
+        lo = (uint64_t)s[0] | ((uint64_t)s[1] << 32);
+        hi = s[2];
+    } else {
+        const uint16_t* s = reinterpret_cast<const uint16_t*>(src);
+        lo = (uint64_t)s[0] | ((uint64_t)s[1] << 16) | ((uint64_t)s[2] << 32);
+    }
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+        int bit = j * BITS;
+        uint64_t val;
+        if (bit + BITS <= 64)
+            val = lo >> bit;
+        else if (bit >= 64)
+            val = hi >> (bit - 64);
+        else
+            val = (lo >> bit) | (hi << (64 - bit));
+        c[j] = (uint32_t)val & ((1u << BITS) - 1u);
+    }
+}
+
+}  // namespace ifq

@@ -1,0 +1,48 @@
+// launch.h -- internal launchers behind the C ABI (host side).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ifq {
+
+// Upper bound on the per-block maxima the tensor-max pass leaves in the
+// workspace (one float each).
+constexpr int kMaxPartials = 256;
+
+struct QuantArgs {
+    int fmt;
+    const uint16_t* x;
+    int64_t rows, cols, ld;
+    uint32_t flags, signs;
+    uint64_t seed;
+    uint8_t* codes;
+    uint8_t* scales;
+    float* tensor_scale;
+    float* partials;  // workspace
+};
+
+hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream);
+
+hipError_t launch_dequantize(int fmt, const uint8_t* codes, const uint8_t* scales,
+                             const float* tensor_scale, int64_t rows, int64_t cols, void* out,
+                             bool out_bf16, hipStream_t stream);
+
+struct GemmArgs {
+    int fmt;
+    const uint8_t* a_codes;
+    const uint8_t* a_scales;
+    const float* a_ts;
+    const uint8_t* b_codes;
+    const uint8_t* b_scales;
+    const float* b_ts;
+    int64_t M, N, K;
+    void* c;
+    int64_t ldc;
+    bool out_bf16;
+};
+
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream);
+
+}  // namespace ifq

@@ -1,0 +1,324 @@
+// quantize.hip -- tensor maximum and block quantizer kernels (gfx950).
+//
+// Pass 1 (tensor_max_*): every block reduces max|v| over its share of the
+// groups (after the RHT when it is on) and writes one float to the
+// workspace.  Pass 2 (quantize_*): every block re-reduces those partials to
+// the same amax, so each computes the same alpha = amax / (M * 448) (Eq. 1);
+// block (0,0) publishes it.  Then one lane quantizes one group of 16 values
+// at a time (Eq. 2 and Fig. 3a) and stores its packed codes and scale byte.
+//
+// Row-wise: a group is 32 contiguous bytes of bf16, read with two 128-bit
+// loads.  Strided axis: a 64x64 tile is staged through LDS so that a lane
+// can gather 16 consecutive rows of one column.
+#include "device.h"
+#include "launch.h"
+
+namespace ifq {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ float wave_max(float m)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+    return m;
+}
+
+// Block-wide max (kThreads threads); result valid in every thread.
+__device__ __forceinline__ float block_max(float m, float* red)
+{
+    m = wave_max(m);
+    const int wid = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) red[wid] = m;
+    __syncthreads();
+    float r = red[0];
+#pragma unroll
+    for (int i = 1; i < kThreads / 64; ++i) r = fmaxf(r, red[i]);
+    __syncthreads();
+    return r;
+}
+
+__device__ __forceinline__ void load_group_rowwise(const uint16_t* p, float (&v)[kGroup])
+{
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4* q = reinterpret_cast<const u32x4*>(p);
+    u32x4 a = __builtin_nontemporal_load(q);
+    u32x4 b = __builtin_nontemporal_load(q + 1);
+    v[0] = bf16lo(a.x);  v[1] = bf16hi(a.x);  v[2] = bf16lo(a.y);  v[3] = bf16hi(a.y);
+    v[4] = bf16lo(a.z);  v[5] = bf16hi(a.z);  v[6] = bf16lo(a.w);  v[7] = bf16hi(a.w);
+    v[8] = bf16lo(b.x);  v[9] = bf16hi(b.x);  v[10] = bf16lo(b.y); v[11] = bf16hi(b.y);
+    v[12] = bf16lo(b.z); v[13] = bf16hi(b.z); v[14] = bf16lo(b.w); v[15] = bf16hi(b.w);
+}
+
+// alpha for this launch: the caller's, or Eq. 1 from the pass-1 partials.
+__device__ __forceinline__ float resolve_alpha(bool scale_in, float* tensor_scale,
+                                               const float* partials, int npartials,
+                                               float denom_alpha, float* red)
+{
+    if (scale_in) return *tensor_scale;
+    float m = 0.0f;
+    for (int i = threadIdx.x; i < npartials; i += kThreads) m = fmaxf(m, partials[i]);
+    m = block_max(m, red);
+    float alpha = m / denom_alpha;
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *tensor_scale = alpha;
+    return alpha;
+}
+
+// --------------------------------------------------------------- row-wise
+
+template <bool RHT>
+__global__ __launch_bounds__(kThreads) void tensor_max_rows(const uint16_t* __restrict__ x,
+                                                            int64_t nrows, int64_t gpr,
+                                                            int64_t ld, uint32_t signs,
+                                                            float* __restrict__ partials)
+{
+    __shared__ float red[kThreads / 64];
+    float m = 0.0f;
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    for (int64_t r = blockIdx.y; r < nrows; r += gridDim.y) {
+        for (int64_t gc = (int64_t)blockIdx.x * kThreads + threadIdx.x; gc < gpr; gc += stride) {
+            float v[kGroup];
+            load_group_rowwise(x + r * ld + gc * kGroup, v);
+            if constexpr (RHT) rht16(v, signs);
+#pragma unroll
+            for (int j = 0; j < kGroup; ++j) m = fmaxf(m, fabsf(v[j]));
+        }
+    }
+    m = block_max(m, red);
+    if (threadIdx.x == 0) partials[blockIdx.y * gridDim.x + blockIdx.x] = m;
+}
+
+template <int FMT, bool RHT, bool SR>
+__global__ __launch_bounds__(kThreads) void quantize_rows(
+    const uint16_t* __restrict__ x, int64_t nrows, int64_t gpr, int64_t ld, uint32_t signs,
+    uint64_t seed, float scale_max, float denom_alpha, int scale_in,
+    const float* __restrict__ partials, int npartials, uint8_t* __restrict__ codes,
+    uint8_t* __restrict__ scales, float* tensor_scale)
+{
+    constexpr int BITS = Fmt<FMT>::BITS;
+    __shared__ float red[kThreads / 64];
+    const float alpha = resolve_alpha(scale_in, tensor_scale, partials, npartials, denom_alpha, red);
+    const float denom = alpha * scale_max;
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    for (int64_t r = blockIdx.y; r < nrows; r += gridDim.y) {
+        for (int64_t gc = (int64_t)blockIdx.x * kThreads + threadIdx.x; gc < gpr; gc += stride) {
+            float v[kGroup];
+            load_group_rowwise(x + r * ld + gc * kGroup, v);
+            if constexpr (RHT) rht16(v, signs);
+            const int64_t gi = r * gpr + gc;
+            uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+            if constexpr (SR) sr_words(seed, (uint64_t)gi, w);
+            uint32_t c[kGroup];
+            uint32_t sb = quantize_group<FMT, SR>(v, alpha, denom, w, c);
+            store_packed<BITS>(codes + gi * (2 * BITS), pack16<BITS>(c));
+            scales[gi] = (uint8_t)sb;
+        }
+    }
+}
+
+// ---------------------------------------------------- strided (token) axis
+// Tile: kTR rows (kTR/16 groups per column) x kTC columns of X, staged as
+// bf16 in LDS.  Thread t handles column t % kTC and group t / kTC.
+constexpr int kTR = 64, kTC = 64;
+
+__device__ __forceinline__ void stage_tile(const uint16_t* __restrict__ x, int64_t rows,
+                                           int64_t cols, int64_t ld, int64_t r0, int64_t c0,
+                                           bool vec, uint16_t (*tile)[kTC + 2])
+{
+    // kTR rows x kTC columns = kTR * kTC / 8 chunks of 8 values
+#pragma unroll
+    for (int i = 0; i < kTR * kTC / 8 / kThreads; ++i) {
+        const int ch = threadIdx.x + i * kThreads;
+        const int rr = ch / (kTC / 8), cc = (ch % (kTC / 8)) * 8;
+        const int64_t gr = r0 + rr, gcol = c0 + cc;
+        uint16_t tmp[8];
+        if (vec && gr < rows && gcol + 8 <= cols) {
+            uint4 q = *reinterpret_cast<const uint4*>(x + gr * ld + gcol);
+            tmp[0] = (uint16_t)q.x; tmp[1] = (uint16_t)(q.x >> 16);
+            tmp[2] = (uint16_t)q.y; tmp[3] = (uint16_t)(q.y >> 16);
+            tmp[4] = (uint16_t)q.z; tmp[5] = (uint16_t)(q.z >> 16);
+            tmp[6] = (uint16_t)q.w; tmp[7] = (uint16_t)(q.w >> 16);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                tmp[e] = (gr < rows && gcol + e < cols) ? x[gr * ld + gcol + e] : (uint16_t)0;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) tile[rr][cc + e] = tmp[e];
+    }
+}
+
+template <bool RHT>
+__global__ __launch_bounds__(kThreads) void tensor_max_strided(const uint16_t* __restrict__ x,
+                                                               int64_t rows, int64_t cols,
+                                                               int64_t ld, int vec, uint32_t signs,
+                                                               float* __restrict__ partials)
+{
+    __shared__ uint16_t tile[kTR][kTC + 2];
+    __shared__ float red[kThreads / 64];
+    float m = 0.0f;
+    const int c = threadIdx.x % kTC, q = threadIdx.x / kTC;
+    for (int64_t c0 = (int64_t)blockIdx.x * kTC; c0 < cols; c0 += (int64_t)gridDim.x * kTC) {
+        for (int64_t r0 = (int64_t)blockIdx.y * kTR; r0 < rows; r0 += (int64_t)gridDim.y * kTR) {
+            stage_tile(x, rows, cols, ld, r0, c0, vec != 0, tile);
+            __syncthreads();
+            float v[kGroup];
+#pragma unroll
+            for (int j = 0; j < kGroup; ++j) v[j] = __uint_as_float((uint32_t)tile[q * kGroup + j][c] << 16);
+            if constexpr (RHT) rht16(v, signs);  // rows beyond the matrix are zero groups
+#pragma unroll
+            for (int j = 0; j < kGroup; ++j) m = fmaxf(m, fabsf(v[j]));
+            __syncthreads();
+        }
+    }
+    m = block_max(m, red);
+    if (threadIdx.x == 0) partials[blockIdx.y * gridDim.x + blockIdx.x] = m;
+}
+
+template <int FMT, bool RHT, bool SR>
+__global__ __launch_bounds__(kThreads) void quantize_strided(
+    const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t ld, int vec,
+    uint32_t signs, uint64_t seed, float scale_max, float denom_alpha, int scale_in,
+    const float* __restrict__ partials, int npartials, uint8_t* __restrict__ codes,
+    uint8_t* __restrict__ scales, float* tensor_scale)
+{
+    constexpr int BITS = Fmt<FMT>::BITS;
+    __shared__ uint16_t tile[kTR][kTC + 2];
+    __shared__ float red[kThreads / 64];
+    const float alpha = resolve_alpha(scale_in, tensor_scale, partials, npartials, denom_alpha, red);
+    const float denom = alpha * scale_max;
+    const int64_t gpr = rows / kGroup;  // groups per output row (= per column of X)
+    const int c = threadIdx.x % kTC, q = threadIdx.x / kTC;
+    for (int64_t c0 = (int64_t)blockIdx.x * kTC; c0 < cols; c0 += (int64_t)gridDim.x * kTC) {
+        for (int64_t r0 = (int64_t)blockIdx.y * kTR; r0 < rows; r0 += (int64_t)gridDim.y * kTR) {
+            stage_tile(x, rows, cols, ld, r0, c0, vec != 0, tile);
+            __syncthreads();
+            const int64_t col = c0 + c, g = r0 / kGroup + q;
+            if (col < cols && g < gpr) {
+                float v[kGroup];
+#pragma unroll
+                for (int j = 0; j < kGroup; ++j)
+                    v[j] = __uint_as_float((uint32_t)tile[q * kGroup + j][c] << 16);
+                if constexpr (RHT) rht16(v, signs);
+                const int64_t gi = col * gpr + g;
+                uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                if constexpr (SR) sr_words(seed, (uint64_t)gi, w);
+                uint32_t cd[kGroup];
+                uint32_t sb = quantize_group<FMT, SR>(v, alpha, denom, w, cd);
+                store_packed<BITS>(codes + gi * (2 * BITS), pack16<BITS>(cd));
+                scales[gi] = (uint8_t)sb;
+            }
+            __syncthreads();
+        }
+    }
+}
+
+__global__ void write_scalar(float* p, float v) { *p = v; }
+
+// ------------------------------------------------------------- launcher
+
+static inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// 128-bit tile loads need 16-byte aligned row starts; otherwise stage by element.
+static inline int strided_vec_ok(const QuantArgs& a)
+{
+    return (reinterpret_cast<uintptr_t>(a.x) % 16 == 0 && a.ld % 8 == 0) ? 1 : 0;
+}
+
+template <int FMT, bool RHT, bool SR>
+static hipError_t launch_q(const QuantArgs& a, hipStream_t s, int npartials, float scale_max,
+                           float denom_alpha)
+{
+    const int scale_in = (a.flags & IFQ_SCALE_IN) ? 1 : 0;
+    if (a.flags & IFQ_AXIS_STRIDED) {
+        dim3 grid((unsigned)cdiv(a.cols, kTC), (unsigned)std::min<int64_t>(cdiv(a.rows, kTR), 65535));
+        hipLaunchKernelGGL((quantize_strided<FMT, RHT, SR>), grid, dim3(kThreads), 0, s, a.x,
+                           a.rows, a.cols, a.ld, strided_vec_ok(a), a.signs, a.seed, scale_max, denom_alpha, scale_in,
+                           a.partials, npartials, a.codes, a.scales, a.tensor_scale);
+    } else {
+        const bool flat = a.ld == a.cols;
+        const int64_t nrows = flat ? 1 : a.rows;
+        const int64_t gpr = flat ? a.rows * a.cols / kGroup : a.cols / kGroup;
+        const int64_t ld = flat ? 0 : a.ld;
+        dim3 grid((unsigned)cdiv(gpr, kThreads), (unsigned)std::min<int64_t>(nrows, 65535));
+        hipLaunchKernelGGL((quantize_rows<FMT, RHT, SR>), grid, dim3(kThreads), 0, s, a.x, nrows,
+                           gpr, ld, a.signs, a.seed, scale_max, denom_alpha, scale_in, a.partials,
+                           npartials, a.codes, a.scales, a.tensor_scale);
+    }
+    return hipGetLastError();
+}
+
+template <bool RHT>
+static hipError_t launch_tensor_max(const QuantArgs& a, hipStream_t s, int* npartials)
+{
+    if (a.flags & IFQ_AXIS_STRIDED) {
+        int64_t tx = cdiv(a.cols, kTC), ty = cdiv(a.rows, kTR);
+        int64_t bx = std::min<int64_t>(tx, kMaxPartials);
+        int64_t by = std::max<int64_t>(1, std::min<int64_t>(ty, kMaxPartials / bx));
+        *npartials = (int)(bx * by);
+        hipLaunchKernelGGL((tensor_max_strided<RHT>), dim3((unsigned)bx, (unsigned)by), dim3(kThreads),
+                           0, s, a.x, a.rows, a.cols, a.ld, strided_vec_ok(a), a.signs, a.partials);
+    } else {
+        const bool flat = a.ld == a.cols;
+        const int64_t nrows = flat ? 1 : a.rows;
+        const int64_t gpr = flat ? a.rows * a.cols / kGroup : a.cols / kGroup;
+        const int64_t ld = flat ? 0 : a.ld;
+        int64_t by = std::min<int64_t>(nrows, kMaxPartials);
+        int64_t bx = std::max<int64_t>(1, std::min<int64_t>(cdiv(gpr, kThreads), kMaxPartials / by));
+        *npartials = (int)(bx * by);
+        hipLaunchKernelGGL((tensor_max_rows<RHT>), dim3((unsigned)bx, (unsigned)by), dim3(kThreads), 0,
+                           s, a.x, nrows, gpr, ld, a.signs, a.partials);
+    }
+    return hipGetLastError();
+}
+
+template <int FMT>
+static hipError_t dispatch_fmt(const QuantArgs& a, hipStream_t s, int npartials, float scale_max,
+                               float denom_alpha)
+{
+    const bool rht = a.flags & IFQ_RHT, sr = a.flags & IFQ_SR;
+    if (rht && sr) return launch_q<FMT, true, true>(a, s, npartials, scale_max, denom_alpha);
+    if (rht) return launch_q<FMT, true, false>(a, s, npartials, scale_max, denom_alpha);
+    if (sr) return launch_q<FMT, false, true>(a, s, npartials, scale_max, denom_alpha);
+    return launch_q<FMT, false, false>(a, s, npartials, scale_max, denom_alpha);
+}
+
+static float fp_max_of(int fmt)
+{
+    switch (fmt) {
+        case IFQ_FMT_IF4: return Fmt<IFQ_FMT_IF4>::FP_MAX;
+        case IFQ_FMT_NVFP4: return Fmt<IFQ_FMT_NVFP4>::FP_MAX;
+        case IFQ_FMT_IF3: return Fmt<IFQ_FMT_IF3>::FP_MAX;
+        case IFQ_FMT_IF6_E2M3: return Fmt<IFQ_FMT_IF6_E2M3>::FP_MAX;
+        default: return Fmt<IFQ_FMT_IF6_E3M2>::FP_MAX;
+    }
+}
+
+hipError_t launch_quantize(const QuantArgs& a, hipStream_t s)
+{
+    // M of Eq. 1-2: M_FP, or M_FP * 16/17 with the gradient margin (Sec. 4.1)
+    float scale_max = fp_max_of(a.fmt);
+    if (a.flags & IFQ_MARGIN_16_17) scale_max = (float)((double)scale_max * 16.0 / 17.0);
+    const float denom_alpha = scale_max * 448.0f;
+    const bool scale_in = a.flags & IFQ_SCALE_IN;
+
+    if (a.rows == 0 || a.cols == 0) {  // empty tensor: alpha = 0, nothing to quantize
+        if (!scale_in) hipLaunchKernelGGL(write_scalar, dim3(1), dim3(1), 0, s, a.tensor_scale, 0.0f);
+        return hipGetLastError();
+    }
+    int npartials = 0;
+    if (!scale_in) {
+        hipError_t e = (a.flags & IFQ_RHT) ? launch_tensor_max<true>(a, s, &npartials)
+                                            : launch_tensor_max<false>(a, s, &npartials);
+        if (e != hipSuccess) return e;
+    }
+    switch (a.fmt) {
+        case IFQ_FMT_IF4: return dispatch_fmt<IFQ_FMT_IF4>(a, s, npartials, scale_max, denom_alpha);
+        case IFQ_FMT_NVFP4: return dispatch_fmt<IFQ_FMT_NVFP4>(a, s, npartials, scale_max, denom_alpha);
+        case IFQ_FMT_IF3: return dispatch_fmt<IFQ_FMT_IF3>(a, s, npartials, scale_max, denom_alpha);
+        case IFQ_FMT_IF6_E2M3: return dispatch_fmt<IFQ_FMT_IF6_E2M3>(a, s, npartials, scale_max, denom_alpha);
+        default: return dispatch_fmt<IFQ_FMT_IF6_E3M2>(a, s, npartials, scale_max, denom_alpha);
+    }
+}
+
+}  // namespace ifq

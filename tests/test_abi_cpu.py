@@ -1,0 +1,129 @@
+"""The C ABI on a machine without a GPU: the library loads, exports every
+entry point include/ifq.h declares, and rejects bad arguments on the host
+before enqueueing anything (no compute call is made here)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ifq.h")
+
+EINVAL, ESHAPE, EALIGN, EUNSUPPORTED, EWORKSPACE = -1, -2, -3, -4, -6
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2603_28765_amd import ops
+    if not os.path.exists(ops.LIB_PATH):
+        pytest.fail("libifq.so not built (run __graft_entry__.build())")
+    return ops.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\**(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for base in ("quantize", "dequantize", "gemm"):
+        for fam in ("if4", "nvfp4", "ifx"):
+            assert f"{fam}_{base}" in names
+    assert len(names) >= 14
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_version_and_strings(L):
+    assert L.ifq_abi_version() == 1
+    assert L.ifq_status_string(0) == b"ok"
+    assert L.ifq_status_string(-2) == b"invalid shape"
+    assert L.ifq_codes_bytes(0, 256, 256) == 256 * 128
+    assert L.ifq_codes_bytes(2, 16, 64) == 16 * 64 * 3 // 8
+    assert L.ifq_codes_bytes(3, 16, 64) == 16 * 64 * 6 // 8
+    assert L.ifq_scales_bytes(256, 4096) == 256 * 256
+    assert L.ifq_quantize_workspace_bytes(0, 8192, 8192, 0) >= 4
+    assert L.ifq_quantize_workspace_bytes(0, 8192, 8192, 8) == 0
+
+
+# fake, never dereferenced device addresses: validation fails first
+P16 = 0x100000
+P_ODD = 0x100001
+
+
+def q(L, fmt=None, x=P16, rows=32, cols=64, ld=64, flags=0, signs=0, codes=P16, scales=P16,
+      ts=P16, ws=P16, wsb=4096):
+    args = (x, rows, cols, ld, flags, signs, 0, codes, scales, ts, ws, wsb, None)
+    if fmt is None:
+        return L.if4_quantize(*args)
+    return L.ifx_quantize(fmt, *args)
+
+
+def test_quantize_validation(L):
+    assert q(L, ts=None) == EINVAL
+    assert q(L, x=None) == EINVAL
+    assert q(L, codes=None) == EINVAL
+    assert q(L, flags=1 << 7) == EINVAL
+    assert q(L, signs=1 << 16) == EINVAL
+    assert q(L, fmt=9) == EINVAL
+    assert q(L, rows=-1) == ESHAPE
+    assert q(L, cols=40, ld=40) == ESHAPE                  # K % 16
+    assert q(L, rows=40, flags=16) == ESHAPE               # strided: rows % 16
+    assert q(L, ld=48) == ESHAPE                           # ld < cols
+    assert q(L, rows=1 << 30, cols=1 << 20, ld=1 << 20) == ESHAPE
+    assert q(L, x=P_ODD) == EALIGN
+    assert q(L, ld=68) == EALIGN                           # row starts not 16-byte aligned
+    assert q(L, codes=P16 + 8) == EALIGN
+    assert q(L, ws=None) == EWORKSPACE
+    assert q(L, wsb=8) == EWORKSPACE
+
+
+def g(L, fmt=None, a=P16, b=P16, M=64, N=64, K=64, c=P16, ldc=64, dtype=0, ts=P16):
+    args = (a, P16, ts, b, P16, ts, M, N, K, c, ldc, dtype, None)
+    if fmt is None:
+        return L.if4_gemm(*args)
+    return L.ifx_gemm(fmt, *args)
+
+
+def test_gemm_validation(L):
+    assert g(L, K=40) == ESHAPE
+    assert g(L, M=-1) == ESHAPE
+    assert g(L, ldc=32) == ESHAPE
+    assert g(L, c=None) == EINVAL
+    assert g(L, ts=None) == EINVAL
+    assert g(L, dtype=5) == EINVAL
+    assert g(L, a=P16 + 4) == EALIGN
+    assert g(L, fmt=3) == EUNSUPPORTED   # IF6 GEMM: not exact in FP16 operands
+    assert g(L, fmt=7) == EINVAL
+
+
+def test_dequantize_validation(L):
+    d = lambda **k: L.if4_dequantize(k.get("codes", P16), P16, k.get("ts", P16),
+                                     k.get("rows", 8), k.get("cols", 64), k.get("out", P16),
+                                     k.get("dtype", 0), None)
+    assert d(cols=40) == ESHAPE
+    assert d(out=None) == EINVAL
+    assert d(dtype=3) == EINVAL
+    assert d(codes=P16 + 2) == EALIGN
+    assert d(rows=0) == 0     # empty: nothing to do
+
+
+def test_empty_gemm_is_noop(L):
+    assert g(L, M=0) == 0
+    assert g(L, N=0) == 0
+
+
+def test_oracle_not_linked(L):
+    """The product library must not depend on the oracle."""
+    import subprocess
+    from paper_2603_28765_amd import ops
+    out = subprocess.run(["ldd", ops.LIB_PATH], capture_output=True, text=True).stdout
+    assert "oracle" not in out
+    syms = subprocess.run(["nm", "-D", ops.LIB_PATH], capture_output=True, text=True).stdout
+    assert "oracle_" not in syms

@@ -1,0 +1,114 @@
+"""GPU parity of the block-scaled GEMM against an fp64 reference of the
+oracle-dequantized operands: relative Frobenius error <= 1e-3 (fp32 out;
+bf16 out is compared with the bf16 rounding of the fp64 reference)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2603_28765_amd import ops, workloads
+from tests.gpu_common import (GEMM_FORMATS, assert_quant_equal, bf16_round, rel_fro,
+                              require_gpu)
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _quantized_pair(fmt, a_cpu, b_cpu, flags=0, signs=0, seeds=(0, 0)):
+    pa, oa = assert_quant_equal(fmt, a_cpu, flags, signs, seeds[0], tag="A")
+    pb, ob = assert_quant_equal(fmt, b_cpu, flags, signs, seeds[1], tag="B")
+    return pa, oa, pb, ob
+
+
+def _check(fmt, pa, oa, pb, ob, dtype=ops.F32, tag=""):
+    c = ops.ifx_gemm(pa, pb, dtype).float().cpu().numpy()
+    ref = O.gemm_ref(oa[0], oa[1], oa[2], ob[0], ob[1], ob[2], fmt)
+    target = ref if dtype == ops.F32 else bf16_round(ref)
+    err = rel_fro(c, target) if np.linalg.norm(ref) > 0 else np.abs(c).max()
+    assert err <= TOL, (tag, err)
+    return err
+
+
+def test_tiny_config():
+    """256^3, N(0,1) seed 0, IF4 RTN, fp32 out."""
+    w = workloads.tiny()
+    pa, oa, pb, ob = _quantized_pair(ops.IF4, w.tensors["A"], w.tensors["B"])
+    err = _check(ops.IF4, pa, oa, pb, ob, tag="tiny")
+    assert err < 1e-5
+
+
+@pytest.mark.parametrize("fmt", GEMM_FORMATS)
+@pytest.mark.parametrize("dtype", [ops.F32, ops.BF16])
+def test_shapes(fmt, dtype):
+    rng = np.random.default_rng(40 + fmt)
+    for (M, N, K) in [(100, 70, 48), (1, 1, 16), (129, 257, 320), (256, 128, 16), (33, 300, 1024)]:
+        a = workloads.to_bf16(rng.standard_t(3, (M, K)))
+        b = workloads.to_bf16(rng.standard_normal((N, K)) * 0.02)
+        pa, oa, pb, ob = _quantized_pair(fmt, a, b)
+        _check(fmt, pa, oa, pb, ob, dtype, tag=f"{fmt} {M}x{N}x{K}")
+
+
+def test_k_zero_gives_zeros():
+    a = torch.zeros((5, 0), dtype=torch.bfloat16).cuda()
+    pa = ops.if4_quantize(a)
+    pb = ops.if4_quantize(torch.zeros((7, 0), dtype=torch.bfloat16).cuda())
+    c = ops.if4_gemm(pa, pb).cpu()
+    assert c.shape == (5, 7) and not c.any()
+
+
+def test_ldc_padding_and_bf16_out():
+    rng = np.random.default_rng(50)
+    a = workloads.to_bf16(rng.standard_normal((64, 256)))
+    b = workloads.to_bf16(rng.standard_normal((48, 256)))
+    pa, oa, pb, ob = _quantized_pair(ops.IF4, a, b)
+    big = torch.full((64, 80), 7.0, dtype=torch.float32, device="cuda")
+    out = big[:, :48]
+    ops.if4_gemm(pa, pb, ops.F32, out)
+    got = big.cpu().numpy()
+    assert np.all(got[:, 48:] == 7.0)
+    ref = O.gemm_ref(oa[0], oa[1], oa[2], ob[0], ob[1], ob[2])
+    assert rel_fro(got[:, :48], ref) <= TOL
+
+
+def test_wgrad_rht_pair_small():
+    """dW = dY^T X with both operands quantized along the token axis with a
+    shared RHT mask, SR and the 16/17 margin (workload at 1/16 size)."""
+    w = workloads.small_like("wgrad")
+    fl = ops.AXIS_STRIDED | ops.RHT | ops.SR | ops.MARGIN_16_17
+    pa, oa = assert_quant_equal(ops.IF4, w.tensors["dY"], fl, w.info["rht_signs"], w.info["sr_seed_dY"])
+    pb, ob = assert_quant_equal(ops.IF4, w.tensors["X"], fl, w.info["rht_signs"], w.info["sr_seed_X"])
+    _check(ops.IF4, pa, oa, pb, ob, ops.F32, tag="wgrad small")
+
+
+def test_determinism():
+    rng = np.random.default_rng(60)
+    a = workloads.to_bf16(rng.standard_normal((300, 512)))
+    b = workloads.to_bf16(rng.standard_normal((200, 512)))
+    pa = ops.if4_quantize(a.cuda())
+    pb = ops.if4_quantize(b.cuda())
+    c1 = ops.if4_gemm(pa, pb).cpu()
+    c2 = ops.if4_gemm(pa, pb).cpu()
+    assert torch.equal(c1, c2)
+
+
+def test_full_size_fwd_mlp_sampled():
+    """M=8192, N=14336, K=4096 with bf16 out, as timed by the benchmark;
+    operands bit-exact in full, the product checked on 256 sampled rows x
+    512 sampled columns against fp64."""
+    w = workloads.fwd_mlp()
+    pa, oa = assert_quant_equal(ops.IF4, w.tensors["A"], tag="A full")
+    pb, ob = assert_quant_equal(ops.IF4, w.tensors["W"], tag="W full")
+    c = ops.if4_gemm(pa, pb, ops.BF16)
+    rng = np.random.default_rng(70)
+    rows = np.sort(rng.choice(8192, 256, replace=False))
+    cols = np.sort(rng.choice(14336, 512, replace=False))
+    got = c.float().cpu().numpy()[np.ix_(rows, cols)]
+    A = O.dequantize(oa[0][rows], oa[1][rows], oa[2], ops.IF4, np.float64)
+    B = O.dequantize(ob[0][cols], ob[1][cols], ob[2], ops.IF4, np.float64)
+    ref = A @ B.T
+    assert rel_fro(got, bf16_round(ref)) <= TOL

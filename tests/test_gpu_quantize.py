@@ -1,0 +1,159 @@
+"""GPU parity of the quantizer and the dequantizer: codes, scale bytes,
+alpha and dequantized values bit-identical to the CPU oracle, for every
+format and flag combination, ragged and degenerate shapes, adversarial ties,
+and the distributions of the measured workloads."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2603_28765_amd import ops, workloads
+from tests.gpu_common import (FORMATS, assert_quant_equal, bits, gpu_quantize, require_gpu)
+
+pytestmark = pytest.mark.gpu
+
+FLAG_SETS = [0, ops.RHT, ops.SR, ops.MARGIN_16_17, ops.RHT | ops.SR | ops.MARGIN_16_17]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def rand_bf16(shape, seed, kind="normal"):
+    rng = np.random.default_rng(seed)
+    if kind == "normal":
+        x = rng.standard_normal(shape)
+    elif kind == "outliers":
+        x = rng.standard_t(3, shape) * 0.5
+        x[..., :: max(1, shape[-1] // 5)] *= 50
+    elif kind == "wide":
+        x = rng.standard_normal(shape) * np.exp2(rng.uniform(-30, 30, shape))
+    return workloads.to_bf16(x)
+
+
+def test_tiny_config_if4_rtn():
+    """The 256x256 N(0,1) case (seed 0), both operands, IF4 round-to-nearest."""
+    w = workloads.tiny()
+    for name in ("A", "B"):
+        assert_quant_equal(ops.IF4, w.tensors[name], tag=f"tiny {name}")
+
+
+@pytest.mark.parametrize("fmt", FORMATS)
+@pytest.mark.parametrize("flags", FLAG_SETS)
+def test_rowwise_all_formats_and_flags(fmt, flags):
+    for shape, kind, seed in [((37, 48), "normal", 1), ((130, 4096), "outliers", 2),
+                              ((1, 16), "normal", 3), ((64, 272), "wide", 4)]:
+        x = rand_bf16(shape, seed + 10 * fmt, kind)
+        assert_quant_equal(fmt, x, flags, signs=0xA5C3, seed=12345,
+                           tag=f"fmt {fmt} flags {flags} {shape} {kind}")
+
+
+@pytest.mark.parametrize("fmt", FORMATS)
+@pytest.mark.parametrize("flags", FLAG_SETS)
+def test_strided_axis(fmt, flags):
+    for shape, kind, seed in [((48, 37), "normal", 5), ((256, 100), "outliers", 6),
+                              ((16, 1), "normal", 7), ((128, 64), "wide", 8)]:
+        x = rand_bf16(shape, seed + 10 * fmt, kind)
+        assert_quant_equal(fmt, x, flags | ops.AXIS_STRIDED, signs=0x3C5A, seed=777,
+                           tag=f"strided fmt {fmt} flags {flags} {shape}")
+
+
+@pytest.mark.parametrize("fmt", FORMATS)
+def test_scale_in(fmt):
+    x = rand_bf16((96, 512), 9, "outliers")
+    for alpha in (1.0, 2.0 ** -7, 0.013, 1e-3):
+        assert_quant_equal(fmt, x, ops.SCALE_IN, alpha=alpha, tag=f"scale_in {alpha}")
+    # alpha = 0 stores every group as zero
+    assert_quant_equal(fmt, x, ops.SCALE_IN, alpha=0.0, tag="scale_in 0")
+
+
+def test_non_contiguous_rows():
+    x = rand_bf16((50, 320), 11, "outliers")
+    for fmt in (ops.IF4, ops.IF3, ops.IF6_E2M3):
+        assert_quant_equal(fmt, x, 0, ld_pad=24, tag="ld padded")
+        assert_quant_equal(fmt, x, ops.RHT | ops.SR, signs=0x1234, seed=5, ld_pad=8, tag="ld padded rht sr")
+
+
+def test_ties_and_signed_zero():
+    """alpha = 1 and a group maximum of 6 make x-bar equal to the input, so
+    the values below sit exactly on FP4 and INT rounding boundaries."""
+    fp_mid = [0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0]
+    rows = []
+    for sgn in (1, -1):
+        vals = [6.0] + [sgn * m for m in fp_mid] + [sgn * 0.1, -0.0, 0.0, sgn * 1e-3,
+                                                    sgn * 5.999, sgn * 4.5, sgn * 0.2, sgn * 3.0]
+        rows.append(vals)
+    # values whose INT candidate x*7/6 sits at a half-integer in fp32
+    int_ties = [(k + 0.5) * 6 / 7 for k in range(7)]
+    rows.append([6.0] + int_ties + [-t for t in int_ties] + [0.0])
+    # all-zero group, outlier group, tiny group
+    rows.append([0.0] * 16)
+    rows.append([6.0] + [1e-4] * 15)
+    rows.append([1e-30] * 16)
+    x = workloads.to_bf16(np.array(rows))
+    for fmt in FORMATS:
+        assert_quant_equal(fmt, x, ops.SCALE_IN, alpha=1.0, tag=f"ties fmt {fmt}")
+        assert_quant_equal(fmt, x, 0, tag=f"ties auto fmt {fmt}")
+
+
+def test_zero_and_empty():
+    z = torch.zeros((32, 64), dtype=torch.bfloat16)
+    for fmt in FORMATS:
+        assert_quant_equal(fmt, z, 0, tag="zero")
+    p, c, s, a = gpu_quantize(ops.IF4, torch.zeros((0, 64), dtype=torch.bfloat16))
+    assert a == 0.0 and c.size == 0 and s.size == 0
+
+
+@pytest.mark.parametrize("kind", ["quant_sweep", "fwd_mlp", "wgrad", "bitwidth"])
+def test_workload_distributions_small(kind):
+    """The measured workloads' distributions at 1/16 of each dimension."""
+    w = workloads.small_like(kind)
+    if kind == "quant_sweep":
+        x = w.tensors["X"]
+        for fmt in (ops.IF4, ops.NVFP4):
+            assert_quant_equal(fmt, x, 0, tag="sweep")
+            assert_quant_equal(fmt, x, ops.RHT, signs=w.info["rht_signs"], tag="sweep rht")
+    elif kind == "fwd_mlp":
+        assert_quant_equal(ops.IF4, w.tensors["A"], tag="acts")
+        assert_quant_equal(ops.IF4, w.tensors["W"], tag="weights")
+    elif kind == "wgrad":
+        fl = ops.AXIS_STRIDED | ops.RHT | ops.SR | ops.MARGIN_16_17
+        assert_quant_equal(ops.IF4, w.tensors["dY"], fl, w.info["rht_signs"], w.info["sr_seed_dY"], tag="dY")
+        assert_quant_equal(ops.IF4, w.tensors["X"], fl, w.info["rht_signs"], w.info["sr_seed_X"], tag="X")
+    else:
+        for fmt in FORMATS:
+            assert_quant_equal(fmt, w.tensors["A"], tag=f"bitwidth {fmt}")
+
+
+@pytest.mark.parametrize("fmt", FORMATS)
+@pytest.mark.parametrize("dtype", [ops.F32, ops.BF16])
+def test_dequantize_bit_exact(fmt, dtype):
+    x = rand_bf16((70, 640), 21 + fmt, "outliers")
+    for flags in (0, ops.RHT | ops.SR):
+        p, (oc, osc, oa) = assert_quant_equal(fmt, x, flags, signs=0x0F0F, seed=3, tag="dq src")
+        out = ops.ifx_dequantize(p, dtype).cpu()
+        ref = O.dequantize(oc, osc, oa, fmt)
+        if dtype == ops.F32:
+            got = out.numpy()
+            np.testing.assert_array_equal(got.view(np.uint32), ref.view(np.uint32))
+        else:
+            got = out.view(torch.int16).numpy().view(np.uint16)
+            np.testing.assert_array_equal(got, O.bf16_bits(ref))
+
+
+def test_full_size_quant_sweep():
+    """8192x8192 t(3) with outlier columns: IF4 and NVFP4, with and without
+    the RHT, bit-exact over the whole tensor."""
+    w = workloads.quant_sweep()
+    x = w.tensors["X"]
+    for fmt in (ops.IF4, ops.NVFP4):
+        assert_quant_equal(fmt, x, 0, tag="full sweep")
+        assert_quant_equal(fmt, x, ops.RHT, signs=w.info["rht_signs"], tag="full sweep rht")
+
+
+def test_determinism_repeat():
+    x = rand_bf16((512, 1024), 31, "outliers")
+    p1, c1, s1, a1 = gpu_quantize(ops.IF4, x, ops.RHT | ops.SR, 0x5555, 9)
+    p2, c2, s2, a2 = gpu_quantize(ops.IF4, x, ops.RHT | ops.SR, 0x5555, 9)
+    assert a1 == a2 and np.array_equal(c1, c2) and np.array_equal(s1, s2)
