@@ -270,6 +270,94 @@ __device__ __forceinline__ uint32_t quantize_group(const float (&v)[kGroup], flo
     return dcode | (use_int ? 0x80u : 0u);
 }
 
+// ------------------------------------------- fast E2M1 group quantizer
+// IF4 / NVFP4 with round-to-nearest.  Same arithmetic as quantize_group, but
+// the FP candidate uses the gfx950 converter v_cvt_scalef32_pk_fp4_f32 (scale
+// 1.0): round to nearest even onto E2M1, saturating at 6, sign kept (a
+// negative value that rounds to zero gives code 0x8) -- identical to the
+// nearest-even rule over every fp32 input -- and v_cvt_scalef32_pk_f32_fp4 to
+// read the candidate back.  The codes come out packed (element 2i in the low
+// nibble of byte i).
+template <bool ADAPTIVE>
+__device__ __forceinline__ uint32_t quantize_group_e2m1(const float (&v)[kGroup], float alpha,
+                                                        float denom, uint2& packed)
+{
+    constexpr float C_UP = 7.0f / 6.0f, K_DN = 6.0f / 7.0f;
+    float amax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(v[j]));
+    const uint32_t dcode = e4m3_encode(amax / denom);
+    const float s = alpha * e4m3_value(dcode);
+    if (!(s >= 1.17549435e-38f)) {
+        packed = make_uint2(0, 0);
+        return 0;
+    }
+    const float inv = 1.0f / s;
+    float xb[kGroup];
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) xb[j] = v[j] * inv;
+
+    uint32_t f0 = 0, f1 = 0;
+    f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, xb[0], xb[1], 1.0f, 0);
+    f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, xb[2], xb[3], 1.0f, 1);
+    f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, xb[4], xb[5], 1.0f, 2);
+    f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, xb[6], xb[7], 1.0f, 3);
+    f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, xb[8], xb[9], 1.0f, 0);
+    f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, xb[10], xb[11], 1.0f, 1);
+    f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, xb[12], xb[13], 1.0f, 2);
+    f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, xb[14], xb[15], 1.0f, 3);
+    float q[kGroup];
+    {
+        typedef float f2 __attribute__((ext_vector_type(2)));
+        f2 t;
+        t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(f0, 1.0f, 0); q[0] = t[0]; q[1] = t[1];
+        t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(f0, 1.0f, 1); q[2] = t[0]; q[3] = t[1];
+        t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(f0, 1.0f, 2); q[4] = t[0]; q[5] = t[1];
+        t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(f0, 1.0f, 3); q[6] = t[0]; q[7] = t[1];
+        t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(f1, 1.0f, 0); q[8] = t[0]; q[9] = t[1];
+        t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(f1, 1.0f, 1); q[10] = t[0]; q[11] = t[1];
+        t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(f1, 1.0f, 2); q[12] = t[0]; q[13] = t[1];
+        t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(f1, 1.0f, 3); q[14] = t[0]; q[15] = t[1];
+    }
+    float ef = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+        const float d = q[j] - xb[j];
+        ef = __builtin_fmaf(d, d, ef);
+    }
+    if constexpr (!ADAPTIVE) {
+        packed = make_uint2(f0, f1);
+        return dcode;
+    }
+    // INT candidate: rint(clamp(x, -6, 6) * 7/6) in one rounding (1.5 * 2^23
+    // bias); the low nibble of the biased float is the two's-complement code.
+    float ei = 0.0f;
+    uint32_t tb[kGroup];
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+        const float xc = __builtin_amdgcn_fmed3f(xb[j], -6.0f, 6.0f);
+        const float t = __builtin_fmaf(xc, C_UP, 12582912.0f);
+        tb[j] = __float_as_uint(t);
+        const float r = t - 12582912.0f;
+        const float d = __builtin_fmaf(r, K_DN, -xb[j]);
+        ei = __builtin_fmaf(d, d, ei);
+    }
+    // gather the low bytes: even elements -> e*, odd -> o*, then nibble-merge
+    const uint32_t e0 = __builtin_amdgcn_perm(tb[2], tb[0], 0x0C0C0400u) |
+                        __builtin_amdgcn_perm(tb[6], tb[4], 0x04000C0Cu);
+    const uint32_t o0 = __builtin_amdgcn_perm(tb[3], tb[1], 0x0C0C0400u) |
+                        __builtin_amdgcn_perm(tb[7], tb[5], 0x04000C0Cu);
+    const uint32_t e1 = __builtin_amdgcn_perm(tb[10], tb[8], 0x0C0C0400u) |
+                        __builtin_amdgcn_perm(tb[14], tb[12], 0x04000C0Cu);
+    const uint32_t o1 = __builtin_amdgcn_perm(tb[11], tb[9], 0x0C0C0400u) |
+                        __builtin_amdgcn_perm(tb[15], tb[13], 0x04000C0Cu);
+    const uint32_t i0 = (e0 & 0x0F0F0F0Fu) | ((o0 << 4) & 0xF0F0F0F0u);
+    const uint32_t i1 = (e1 & 0x0F0F0F0Fu) | ((o1 << 4) & 0xF0F0F0F0u);
+    const bool use_int = ei < ef;
+    packed = use_int ? make_uint2(i0, i1) : make_uint2(f0, f1);
+    return dcode | (use_int ? 0x80u : 0u);
+}
+
 // Dense little-endian bit stream of 16 codes of BITS bits: 2*BITS bytes,
 // written as BITS/2 32-bit words for even BITS and as 3 16-bit halves for 3.
 template <int BITS> struct Packed;

@@ -64,6 +64,28 @@ __device__ __forceinline__ float resolve_alpha(bool scale_in, float* tensor_scal
     return alpha;
 }
 
+// Quantize one (transformed) group and store its codes and scale byte.
+template <int FMT, bool SR>
+__device__ __forceinline__ void quantize_store(const float (&v)[kGroup], float alpha, float denom,
+                                               uint64_t seed, int64_t gi, uint8_t* __restrict__ codes,
+                                               uint8_t* __restrict__ scales)
+{
+    constexpr int BITS = Fmt<FMT>::BITS;
+    if constexpr (BITS == 4 && !SR) {
+        uint2 pk;
+        const uint32_t sb = quantize_group_e2m1<Fmt<FMT>::ADAPTIVE>(v, alpha, denom, pk);
+        *reinterpret_cast<uint2*>(codes + gi * 8) = pk;
+        scales[gi] = (uint8_t)sb;
+    } else {
+        uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        if constexpr (SR) sr_words(seed, (uint64_t)gi, w);
+        uint32_t c[kGroup];
+        const uint32_t sb = quantize_group<FMT, SR>(v, alpha, denom, w, c);
+        store_packed<BITS>(codes + gi * (2 * BITS), pack16<BITS>(c));
+        scales[gi] = (uint8_t)sb;
+    }
+}
+
 // --------------------------------------------------------------- row-wise
 
 template <bool RHT>
@@ -106,12 +128,7 @@ __global__ __launch_bounds__(kThreads) void quantize_rows(
             load_group_rowwise(x + r * ld + gc * kGroup, v);
             if constexpr (RHT) rht16(v, signs);
             const int64_t gi = r * gpr + gc;
-            uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-            if constexpr (SR) sr_words(seed, (uint64_t)gi, w);
-            uint32_t c[kGroup];
-            uint32_t sb = quantize_group<FMT, SR>(v, alpha, denom, w, c);
-            store_packed<BITS>(codes + gi * (2 * BITS), pack16<BITS>(c));
-            scales[gi] = (uint8_t)sb;
+            quantize_store<FMT, SR>(v, alpha, denom, seed, gi, codes, scales);
         }
     }
 }
@@ -201,12 +218,7 @@ __global__ __launch_bounds__(kThreads) void quantize_strided(
                     v[j] = __uint_as_float((uint32_t)tile[q * kGroup + j][c] << 16);
                 if constexpr (RHT) rht16(v, signs);
                 const int64_t gi = col * gpr + g;
-                uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                if constexpr (SR) sr_words(seed, (uint64_t)gi, w);
-                uint32_t cd[kGroup];
-                uint32_t sb = quantize_group<FMT, SR>(v, alpha, denom, w, cd);
-                store_packed<BITS>(codes + gi * (2 * BITS), pack16<BITS>(cd));
-                scales[gi] = (uint8_t)sb;
+                quantize_store<FMT, SR>(v, alpha, denom, seed, gi, codes, scales);
             }
             __syncthreads();
         }
