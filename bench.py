@@ -38,6 +38,9 @@ def parse():
     p.add_argument("--cpu-rows", type=int, default=512,
                    help="activation rows of the CPU-oracle sample")
     p.add_argument("--small", action="store_true", help="1/8-size shapes (quick checks)")
+    p.add_argument("--mode", choices=["full", "step", "copy"], default="full",
+                   help="step: only the timed IF4 step (for counter runs); copy: a plain 1 GiB "
+                        "device copy, the reference for scaling the HBM byte counters")
     return p.parse_args()
 
 
@@ -54,6 +57,15 @@ def main():
     from paper_2603_28765_amd import ops, workloads
 
     torch.cuda.set_device(0)
+    if args.mode == "copy":
+        n = 1 << 30
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"mode": "copy", "bytes_read_per_launch": n, "bytes_written_per_launch": n}))
+        return
     div = 8 if args.small else 1
     M, N, K = 8192 // div, 14336 // div, 4096 // div
     w = workloads.fwd_mlp(M, N, K)
@@ -118,6 +130,9 @@ def main():
         return float(np.mean(times))
 
     res = timed(ops.IF4, args.steps, args.warmup)
+    if args.mode == "step":
+        print(json.dumps({"mode": "step", "ms_per_step": res["step_s"] * 1e3}))
+        return
     res_nv = timed(ops.NVFP4, max(5, args.steps // 2), 2)
     n_a, n_w = M * K, N * K
     flops = 2.0 * M * N * K
