@@ -35,8 +35,11 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-rows", type=int, default=512,
-                   help="activation rows of the CPU-oracle sample")
+    p.add_argument("--cpu-rows", type=int, default=1024,
+                   help="activation rows in the CPU oracle's GEMM sample")
+    p.add_argument("--traffic-from", metavar="DIR",
+                   help="read rocprofv3 FETCH_SIZE/WRITE_SIZE counter CSVs of a --mode step run "
+                        "(DIR/pmc_FETCH_SIZE, DIR/pmc_WRITE_SIZE) and write profiles/hbm_traffic.json")
     p.add_argument("--small", action="store_true", help="1/8-size shapes (quick checks)")
     p.add_argument("--mode", choices=["full", "step", "copy"], default="full",
                    help="step: only the timed IF4 step (for counter runs); copy: a plain 1 GiB "
@@ -46,6 +49,9 @@ def parse():
 
 def main():
     args = parse()
+    if args.traffic_from:
+        record_traffic(args.traffic_from)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the multi-GPU layout "
               "is described in DESIGN.md, not run.", file=sys.stderr)
@@ -160,8 +166,9 @@ def main():
                    "out": "bf16"},
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2),
                      "peak": FP16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(gemm_tflops / FP16_MFMA_PEAK_TFLOPS, 4), "traffic": None,
-                     "kernel": "gemm_tn<IF4, bf16 out>"},
+                     "frac": round(gemm_tflops / FP16_MFMA_PEAK_TFLOPS, 4),
+                     "traffic": gemm_traffic(M, N, K), "traffic_unit": "HBM bytes per launch",
+                     "kernel": "gemm_tn_interior<IF4, bf16 out>"},
         "roofline_quantize": {
             "bound": "hbm", "kernel": "quantize_rows<IF4> (alpha supplied, single pass, W)",
             "achieved": round(qbytes_1pass(n_w) / t_w_1p / 1e9, 1), "peak": HBM_PEAK_GBS,
@@ -189,13 +196,68 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+GEMM_SOURCES = ("paper_2603_28765_amd/csrc/gemm.hip", "paper_2603_28765_amd/csrc/device.h")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+GEMM_KERNEL = "ifq::gemm_tn_interior<0, true>"
+# Per-dispatch calibration of the byte counters against a plain 1 GiB device
+# copy (bench.py --mode copy): FETCH_SIZE reads back half the bytes read,
+# WRITE_SIZE the bytes written.
+FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
+
+
+def _sources_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def gemm_traffic(M, N, K):
+    """Counter-measured HBM bytes per GEMM launch, or None when the record is
+    missing, was taken at another shape, or the GEMM sources changed since."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            rec = json.load(fh)["gemm"]
+    except (OSError, KeyError, ValueError):
+        return None
+    if rec.get("sha256") != _sources_digest() or rec.get("shape") != [M, N, K]:
+        return None
+    return int(rec["fetch_bytes"] + rec["write_bytes"])
+
+
+def record_traffic(d):
+    import csv
+
+    def per_dispatch(sub):
+        vals = []
+        for root, _, files in os.walk(os.path.join(d, sub)):
+            for f in files:
+                if f.endswith("counter_collection.csv"):
+                    with open(os.path.join(root, f)) as fh:
+                        vals += [float(r["Counter_Value"]) for r in csv.DictReader(fh)
+                                 if r["Kernel_Name"].replace("void ", "").startswith(GEMM_KERNEL)]
+        if not vals:
+            raise SystemExit(f"no {GEMM_KERNEL} dispatches under {os.path.join(d, sub)}")
+        return sum(vals) / len(vals) * 1024.0
+    fetch = per_dispatch("pmc_FETCH_SIZE") * FETCH_SCALE
+    write = per_dispatch("pmc_WRITE_SIZE") * WRITE_SCALE
+    rec = {"gemm": {"kernel": GEMM_KERNEL, "shape": [8192, 14336, 4096], "sources": list(GEMM_SOURCES),
+                    "sha256": _sources_digest(), "fetch_bytes": round(fetch), "write_bytes": round(write),
+                    "calibration": {"FETCH_SIZE": FETCH_SCALE, "WRITE_SIZE": WRITE_SCALE}}}
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(rec))
+
+
 def cpu_baseline(w, M, N, K, rows):
-    """The CPU oracle on a bounded sample of the same step: quantize `rows`
-    rows of A and rows*N/M rows of W (C oracle, one thread), then the fp64
-    reference product of the sampled A rows with the sampled W rows (numpy
-    BLAS).  Scaled to the full step: the sample is rows/M of the quantize
-    work and (rows/M)^2 of the GEMM work is not representative, so the GEMM
-    sample is rows x N x K (all of W), i.e. rows/M of the GEMM flops."""
+    """The CPU oracle on a bounded sample of the same step: the C oracle
+    quantizes all of A and W (one thread; the step's whole quantize work),
+    then its reference GEMM (dequantize to fp64, numpy BLAS product) runs for
+    `rows` rows of A against all of W.  The product's time is scaled by
+    M/rows; the quantize time and W's dequantize are taken as measured."""
     import numpy as np
     import torch
 
@@ -205,31 +267,28 @@ def cpu_baseline(w, M, N, K, rows):
     def bits(t):
         return t.contiguous().view(torch.int16).numpy().view(np.uint16)
 
-    a = bits(w.tensors["A"][:rows])
-    wr = max(16, rows * N // M)
-    wt = bits(w.tensors["W"][:wr])
+    a, wt = bits(w.tensors["A"]), bits(w.tensors["W"])
     t0 = time.perf_counter()
     ca, sa, aa = O.quantize(a, O.FMT_IF4)
     cw, sw, aw = O.quantize(wt, O.FMT_IF4)
     t_q = time.perf_counter() - t0
-    # GEMM reference: the sampled rows of A against all of W's rows (dequantized
-    # from the oracle quantization of the full W, outside the timing)
-    cwf, swf, awf = O.quantize(bits(w.tensors["W"]), O.FMT_IF4)
-    Wd = O.dequantize(cwf, swf, awf, O.FMT_IF4, np.float64)
     t1 = time.perf_counter()
-    Ad = O.dequantize(ca, sa, aa, O.FMT_IF4, np.float64)
+    Wd = O.dequantize(cw, sw, aw, O.FMT_IF4, np.float64)
+    t_dw = time.perf_counter() - t1
+    t2 = time.perf_counter()
+    Ad = O.dequantize(ca[:rows], sa[:rows], aa, O.FMT_IF4, np.float64)
     _ = Ad @ Wd.T
-    t_g = time.perf_counter() - t1
+    t_g = time.perf_counter() - t2
     blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    frac = rows / M
-    t_full = t_q / frac + t_g / frac
+    t_full = t_q + t_dw + t_g * M / rows
     flops = 2.0 * M * N * K
     return {"value": round(flops / t_full / 1e12, 6), "unit": "TFLOP/s",
             "cores": int(blas_threads), "kind": "oracle",
-            "sample": f"IF4 quantize of {rows} rows of A and {wr} rows of W (C oracle, 1 thread, "
-                      f"{t_q:.2f} s) + fp64 reference GEMM of {rows} rows of A against all {N} rows "
-                      f"of W (numpy BLAS, {blas_threads} threads, {t_g:.2f} s); scaled by M/{rows}",
-            "seconds": round(t_q + t_g, 2)}
+            "sample": f"IF4 quantize of all of A and W (C oracle, 1 thread, {t_q:.2f} s), "
+                      f"fp64 dequantize of W ({t_dw:.2f} s), reference GEMM of {rows} of {M} rows of A "
+                      f"against all {N} rows of W (numpy BLAS, {blas_threads} threads, {t_g:.2f} s, "
+                      f"scaled by M/{rows})",
+            "seconds": round(t_q + t_dw + t_g, 2)}
 
 
 if __name__ == "__main__":
