@@ -40,6 +40,8 @@ def parse():
     p.add_argument("--traffic-from", metavar="DIR",
                    help="read rocprofv3 FETCH_SIZE/WRITE_SIZE counter CSVs of a --mode step run "
                         "(DIR/pmc_FETCH_SIZE, DIR/pmc_WRITE_SIZE) and write profiles/hbm_traffic.json")
+    p.add_argument("--format", choices=["if4", "nvfp4"], default="if4",
+                   help="format of the --mode step run")
     p.add_argument("--small", action="store_true", help="1/8-size shapes (quick checks)")
     p.add_argument("--mode", choices=["full", "step", "copy"], default="full",
                    help="step: only the timed IF4 step (for counter runs); copy: a plain 1 GiB "
@@ -135,10 +137,13 @@ def main():
         del flush
         return float(np.mean(times))
 
-    res = timed(ops.IF4, args.steps, args.warmup)
     if args.mode == "step":
-        print(json.dumps({"mode": "step", "ms_per_step": res["step_s"] * 1e3}))
+        fmt = ops.IF4 if args.format == "if4" else ops.NVFP4
+        r = timed(fmt, args.steps, args.warmup)
+        print(json.dumps({"mode": "step", "format": args.format, "ms_per_step": r["step_s"] * 1e3,
+                          "gemm_us": r["gemm_s"] * 1e6}))
         return
+    res = timed(ops.IF4, args.steps, args.warmup)
     res_nv = timed(ops.NVFP4, max(5, args.steps // 2), 2)
     n_a, n_w = M * K, N * K
     flops = 2.0 * M * N * K

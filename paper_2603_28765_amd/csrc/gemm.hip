@@ -284,60 +284,75 @@ __device__ __forceinline__ void read_bfrags(const _Float16* Bs, int kk, int lane
         bf[j] = *reinterpret_cast<const half8*>(Bs + (j * 32 + (lane & 31)) * kPitch + kofs);
 }
 
+// Register state carried across K steps.  Slots alternate with the step
+// parity P (the loop is unrolled by two so that no slot is ever copied): raw
+// A chunks of steps s (slot P) and s + 1 (slot P ^ 1); raw B of step s + 2
+// (slot P, decoded during step s) and s + 3 (slot P ^ 1, loading).
 template <int FMT, bool EDGE> struct TileState {
-    RawA<FMT> a_cur[2], a_nxt[2];  // [row block i]: this step, next step
-    RawB<FMT> b_nxt, b_fill;       // next step (decoded now), step + 2 (loading)
-    half8 af[2][2][2];             // [group gg][row block i][slice parity]
+    RawA<FMT> a[2][2];     // [slot][row block i]
+    RawB<FMT> b[2];        // [slot]
+    half8 af[2][2][2];     // [group gg][row block i][slice parity]
+    half8 bf[2][8];        // B fragments, double buffered over slices
 };
 
-// One 64-wide K step.  Slice kk multiplies B fragments read from LDS stage
-// `cur` with A fragments in registers while: the B fragments of slice kk + 1
-// are read, one B group of the next step is decoded into stage cur ^ 1, and
-// one A decode unit is produced -- this step's second group (slices 2, 3) at
-// kk = 0, 1 and the next step's first group (slices 0, 1) at kk = 2, 3.
-// Loads of step s + 2 are clamped to the last step (harmless extra work that
-// keeps the loop free of branches).
-template <int FMT, bool EDGE>
+// Wait for this wavefront's LDS writes, then meet the other wavefronts.
+// (A full __syncthreads() would also wait for every outstanding global load.)
+__device__ __forceinline__ void lds_barrier()
+{
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// One 64-wide K step s.  B is staged in a ring of three LDS buffers: step s
+// reads stage s % 3, decodes B of step s + 2 into stage (s + 2) % 3 and, in
+// its last slice, prefetches the first B fragments of step s + 1 from stage
+// (s + 1) % 3, which the barrier closing step s - 1 made visible; so no
+// slice waits on a fresh LDS read after the barrier.  Slice kk multiplies
+// the B fragments of the slice with A fragments in registers while one B
+// group and one A decode unit are produced -- this step's second A group
+// (slices 2, 3) at kk = 0, 1 and the next step's first group (slices 0, 1) at
+// kk = 2, 3.  Loads beyond the last step are clamped to it (harmless extra
+// work that keeps the loop free of branches).
+template <int FMT, bool EDGE, int P>
 __device__ __forceinline__ void gemm_step(int s, int nsteps, const uint8_t* __restrict__ a_codes,
                                           const uint8_t* __restrict__ a_scales,
                                           const uint8_t* __restrict__ b_codes,
                                           const uint8_t* __restrict__ b_scales, int64_t M,
                                           int64_t N, int64_t gpr, int64_t arow0, int64_t n0,
-                                          TileState<FMT, EDGE>& st, _Float16 (*lds)[kStageHalves],
-                                          int cur, floatx16 (&acc)[2][8])
+                                          TileState<FMT, EDGE>& st, const _Float16* Bs,
+                                          const _Float16* Bn, _Float16* Bd, floatx16 (&acc)[2][8])
 {
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int h = lane >> 5;
-    const _Float16* Bs = lds[cur];
-    _Float16* Bd = lds[cur ^ 1];
-    half8 bf[2][8];
-    read_bfrags(Bs, 0, lane, bf[0]);
+    const int64_t g3 = (int64_t)min(s + 3, nsteps - 1) * kGroupsPerStep;
     const int64_t g2 = (int64_t)min(s + 2, nsteps - 1) * kGroupsPerStep;
-    load_b<FMT, EDGE>(b_codes, b_scales, n0 + t, N, gpr, g2, st.b_fill);
+    load_b<FMT, EDGE>(b_codes, b_scales, n0 + t, N, gpr, g3, st.b[P ^ 1]);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
         const int f = kk & 1;
-        if (kk < 3) read_bfrags(Bs, kk + 1, lane, bf[f ^ 1]);
-        decode_b<FMT>(st.b_nxt, Bd, t, kk);
+        if (kk < 3)
+            read_bfrags(Bs, kk + 1, lane, st.bf[f ^ 1]);
+        else
+            read_bfrags(Bn, 0, lane, st.bf[f ^ 1]);
+        decode_b<FMT>(st.b[P], Bd, t, kk);
         if (kk < 2) {
-            decode_a<FMT>(st.a_cur[kk], 1, st.af[1][kk][0], st.af[1][kk][1]);
+            decode_a<FMT>(st.a[P][kk], 1, st.af[1][kk][0], st.af[1][kk][1]);
         } else {
             if (kk == 2) {
                 // this step's A chunks are fully decoded: refill them with step s + 2
 #pragma unroll
                 for (int i = 0; i < 2; ++i)
-                    load_a<FMT, EDGE>(a_codes, a_scales, arow0 + 32 * i, M, gpr, g2 + 2 * h, st.a_cur[i]);
+                    load_a<FMT, EDGE>(a_codes, a_scales, arow0 + 32 * i, M, gpr, g2 + 2 * h, st.a[P][i]);
             }
-            decode_a<FMT>(st.a_nxt[kk - 2], 0, st.af[0][kk - 2][0], st.af[0][kk - 2][1]);
+            decode_a<FMT>(st.a[P ^ 1][kk - 2], 0, st.af[0][kk - 2][0], st.af[0][kk - 2][1]);
         }
         const int gg = kk >> 1, par = kk & 1;
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(st.af[gg][i][par], bf[f][j], acc[i][j], 0, 0, 0);
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(st.af[gg][i][par], st.bf[f][j], acc[i][j], 0, 0, 0);
 #pragma unroll
         for (int m = 0; m < 16; ++m) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -347,65 +362,20 @@ __device__ __forceinline__ void gemm_step(int s, int nsteps, const uint8_t* __re
         }
         __builtin_amdgcn_sched_barrier(0);
     }
-    __syncthreads();
+    lds_barrier();
 }
 
+// Scale the accumulators by alpha_A alpha_B / (lambda fold_FP)^2 and store
+// the 256 x 256 tile (lane layout of v_mfma_f32_32x32x16_f16: column
+// lane % 32, rows 8 (e / 4) + 4 (lane / 32) + e % 4 of each 32 x 32 block).
 template <int FMT, bool OUT_BF16, bool EDGE>
-__device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ a_codes,
-                                          const uint8_t* __restrict__ a_scales,
-                                          const float* __restrict__ a_ts,
-                                          const uint8_t* __restrict__ b_codes,
-                                          const uint8_t* __restrict__ b_scales,
-                                          const float* __restrict__ b_ts, int64_t M, int64_t N,
-                                          int64_t K, void* __restrict__ C, int64_t ldc,
-                                          int64_t m0, int64_t n0, _Float16 (*lds)[kStageHalves])
+__device__ __forceinline__ void store_tile(const floatx16 (&acc)[2][8], const float* __restrict__ a_ts,
+                                           const float* __restrict__ b_ts, int64_t M, int64_t N,
+                                           void* __restrict__ C, int64_t ldc, int64_t m0, int64_t n0)
 {
-    const int64_t gpr = K / kGroup;
-    const int nsteps = (int)((gpr + kGroupsPerStep - 1) / kGroupsPerStep);
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     const int h = lane >> 5;
-    const int64_t arow0 = m0 + 64 * wave + (lane & 31);  // row of block i is arow0 + 32 i
-
-    floatx16 acc[2][8];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-
-    if (nsteps > 0) {
-        TileState<FMT, EDGE> st;
-        const int64_t g1 = (int64_t)min(1, nsteps - 1) * kGroupsPerStep;
-        RawB<FMT> b0;
-        load_b<FMT, EDGE>(b_codes, b_scales, n0 + t, N, gpr, 0, b0);
-        load_b<FMT, EDGE>(b_codes, b_scales, n0 + t, N, gpr, g1, st.b_nxt);
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            load_a<FMT, EDGE>(a_codes, a_scales, arow0 + 32 * i, M, gpr, 2 * h, st.a_cur[i]);
-            load_a<FMT, EDGE>(a_codes, a_scales, arow0 + 32 * i, M, gpr, g1 + 2 * h, st.a_nxt[i]);
-        }
-#pragma unroll
-        for (int g = 0; g < kGroupsPerStep; ++g) decode_b<FMT>(b0, lds[0], t, g);
-#pragma unroll
-        for (int i = 0; i < 2; ++i) decode_a<FMT>(st.a_cur[i], 0, st.af[0][i][0], st.af[0][i][1]);
-        __syncthreads();
-        for (int s = 0; s < nsteps; ++s) {
-            gemm_step<FMT, EDGE>(s, nsteps, a_codes, a_scales, b_codes, b_scales, M, N, gpr, arow0,
-                                 n0, st, lds, s & 1, acc);
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const RawA<FMT> ta = st.a_cur[i];
-                st.a_cur[i] = st.a_nxt[i];
-                st.a_nxt[i] = ta;
-            }
-            const RawB<FMT> tb = st.b_nxt;
-            st.b_nxt = st.b_fill;
-            st.b_fill = tb;
-        }
-    }
-
     const float sc = (*a_ts * *b_ts) * Fold<FMT>::EPI;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -427,21 +397,80 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ a_codes,
     }
 }
 
-// Interior tiles: every row, column and K group in range (K % 64 == 0,
-// 4-byte aligned scale rows).  Workgroup ids are dealt round robin to the 8
-// XCDs; they are remapped so that each XCD walks a contiguous range of tile
+template <int FMT, bool OUT_BF16, bool EDGE>
+__device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ a_codes,
+                                          const uint8_t* __restrict__ a_scales,
+                                          const float* __restrict__ a_ts,
+                                          const uint8_t* __restrict__ b_codes,
+                                          const uint8_t* __restrict__ b_scales,
+                                          const float* __restrict__ b_ts, int64_t M, int64_t N,
+                                          int64_t K, void* __restrict__ C, int64_t ldc,
+                                          int64_t m0, int64_t n0, _Float16 (*lds)[kStageHalves])
+{
+    const int64_t gpr = K / kGroup;
+    // steps run in pairs; a padding step (EDGE tiles only: interior tiles have
+    // K % 128 == 0) loads guarded, zero-filled groups and adds nothing
+    const int nsteps = 2 * (int)((gpr + 2 * kGroupsPerStep - 1) / (2 * kGroupsPerStep));
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int h = lane >> 5;
+    const int64_t arow0 = m0 + 64 * wave + (lane & 31);  // row of block i is arow0 + 32 i
+
+    floatx16 acc[2][8];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+    if (nsteps > 0) {
+        TileState<FMT, EDGE> st;
+        const int64_t g1 = (int64_t)min(1, nsteps - 1) * kGroupsPerStep;
+        const int64_t g2 = (int64_t)min(2, nsteps - 1) * kGroupsPerStep;
+        RawB<FMT> b0;
+        load_b<FMT, EDGE>(b_codes, b_scales, n0 + t, N, gpr, 0, b0);
+        load_b<FMT, EDGE>(b_codes, b_scales, n0 + t, N, gpr, g1, st.b[1]);
+        load_b<FMT, EDGE>(b_codes, b_scales, n0 + t, N, gpr, g2, st.b[0]);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            load_a<FMT, EDGE>(a_codes, a_scales, arow0 + 32 * i, M, gpr, 2 * h, st.a[0][i]);
+            load_a<FMT, EDGE>(a_codes, a_scales, arow0 + 32 * i, M, gpr, g1 + 2 * h, st.a[1][i]);
+        }
+#pragma unroll
+        for (int g = 0; g < kGroupsPerStep; ++g) {
+            decode_b<FMT>(b0, lds[0], t, g);
+            decode_b<FMT>(st.b[1], lds[1], t, g);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) decode_a<FMT>(st.a[0][i], 0, st.af[0][i][0], st.af[0][i][1]);
+        lds_barrier();
+        read_bfrags(lds[0], 0, lane, st.bf[0]);
+        // stage indices of steps s, s + 1, s + 2
+        int r0 = 0, r1 = 1, r2 = 2;
+        for (int s = 0; s < nsteps; s += 2) {
+            gemm_step<FMT, EDGE, 0>(s, nsteps, a_codes, a_scales, b_codes, b_scales, M, N, gpr, arow0,
+                                    n0, st, lds[r0], lds[r1], lds[r2], acc);
+            gemm_step<FMT, EDGE, 1>(s + 1, nsteps, a_codes, a_scales, b_codes, b_scales, M, N, gpr,
+                                    arow0, n0, st, lds[r1], lds[r2], lds[r0], acc);
+            // advance the ring by two steps
+            const int n0r = r2, n1r = r0, n2r = r1;
+            r0 = n0r;
+            r1 = n1r;
+            r2 = n2r;
+        }
+    }
+
+    store_tile<FMT, OUT_BF16, EDGE>(acc, a_ts, b_ts, M, N, C, ldc, m0, n0);
+}
+
+// Tile of workgroup blockIdx.x.  Workgroup ids are dealt round robin to the
+// 8 XCDs; they are remapped so that each XCD walks a contiguous range of tile
 // ids, and tile ids are ordered in bands of 4 tile rows (column-major inside
 // a band), so the 32 workgroups resident on one XCD form a 4 x 8 block of
 // tiles that share A and B rows in its L2.
-template <int FMT, bool OUT_BF16>
-__global__ __launch_bounds__(kGemmThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void gemm_tn_interior(const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
-                      const float* __restrict__ a_ts, const uint8_t* __restrict__ b_codes,
-                      const uint8_t* __restrict__ b_scales, const float* __restrict__ b_ts,
-                      int64_t M, int64_t N, int64_t K, void* __restrict__ C, int64_t ldc,
-                      int tiles_m, int tiles_n)
+__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn)
 {
-    __shared__ __attribute__((aligned(16))) _Float16 lds[2][kStageHalves];
     const int nwg = gridDim.x;
     const int bid = blockIdx.x;
     const int tile = (nwg % 8 == 0) ? (bid % 8) * (nwg / 8) + bid / 8 : bid;
@@ -450,7 +479,489 @@ void gemm_tn_interior(const uint8_t* __restrict__ a_codes, const uint8_t* __rest
     const int first_m = band * GM;
     const int gm = min(tiles_m - first_m, GM);
     const int in_band = tile - band * GM * tiles_n;
-    const int tm = first_m + in_band % gm, tn = in_band / gm;
+    tm = first_m + in_band % gm;
+    tn = in_band / gm;
+}
+
+// ------------------------------------------------------- fast interior path
+// Interior tiles of 4-bit formats with K % 512 == 0 and 16-byte aligned
+// operands.  Same tiling and operand values as above; what changes is how
+// the packed operands reach the kernel.  Row-major codes give each row only
+// 32 bytes per K step, so per-lane row loads touch a different cache line in
+// every lane and every step (and scale bytes far more so).  Here operands
+// arrive in line-sized, coalesced pieces:
+//   B codes: two K steps (64 bytes per row) per chunk, copied straight into
+//            LDS by global_load_lds (four lanes per row), two chunk slots;
+//   scales : eight K steps (32 bytes per row, A and B) per chunk, the same
+//            way, two slots;
+//   A codes: 32 bytes per lane and chunk (both 16-byte halves of one row's
+//            64 bytes are read by the lane pair that owns the row), straight
+//            into registers, two slots.
+// K order.  Within a 2-step chunk (8 groups), lane half h of every MFMA
+// holds groups 4h .. 4h + 3; step j of the chunk uses groups 4h + 2j and
+// 4h + 2j + 1 (slices 0, 1 and 2, 3).  The B stage of step j therefore holds,
+// per row, groups 2j, 2j + 1 (half 0) and 4 + 2j, 5 + 2j (half 1).
+// Loads are issued from inline assembly and waited for with explicit
+// vmcnt counts (the compiler's own tracking would wait for every copy into
+// LDS before any LDS access); the counts below follow the fixed issue order
+// of the four-step loop body:
+//   odd step,  slice 0: 4 copies of B codes (+ 2 copies of scales at step 1)
+//   odd step,  slice 2: 4 loads of A codes
+// Decoded B stages are 128-byte rows whose 16-byte pieces are XOR-swizzled
+// by swz8(row) = (row % 8) ^ ((row / 8) % 2), raw B rows (64 bytes) by
+// swz4(row) = ((row / 2) % 4) ^ ((row / 8) % 2): both keep the row-wise
+// accesses (consecutive lanes on consecutive rows) free of bank conflicts
+// whether a 128-bit access is served 8 lanes over 32 banks or 16 lanes over
+// 64 banks at a time.
+namespace fast {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kStageBytes = kBN * kBK * 2;       // decoded B stage, 32 KiB
+constexpr int kRawBytes = kBN * 64;              // B codes of one chunk, 16 KiB
+constexpr int kSclBytes = (kBM + kBN) * 32;      // scales of one 8-step chunk, 16 KiB
+constexpr int kSclB = kBM * 32;                  // offset of the B rows in a scale chunk
+
+__device__ __forceinline__ int swz8(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+__device__ __forceinline__ int swz4(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
+
+__device__ __forceinline__ uint32_t lds_off(const void* p)
+{
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// 16 bytes per lane from global memory into LDS at lds + 16 * lane (lds is
+// wave-uniform).
+__device__ __forceinline__ void copy16(const void* g, uint32_t lds)
+{
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds)
+                 : "memory", "m0");
+}
+
+__device__ __forceinline__ u32x4 load16(const void* g)
+{
+    u32x4 v;
+    asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(g) : "memory");
+    return v;
+}
+
+template <int N> __device__ __forceinline__ void vm_wait()
+{
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Wait as above and mark the four registers of an A chunk as produced here.
+template <int N> __device__ __forceinline__ void vm_wait(u32x4& a, u32x4& b, u32x4& c, u32x4& d)
+{
+    asm volatile("s_waitcnt vmcnt(%4)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : "n"(N) : "memory");
+}
+
+// Fold constants of the two groups whose scale bytes are the low and high
+// byte of sw, one half each: the operand is K x + C, x the converted code.
+//   IF4 FP group : K = 7 Delta / 32, C = 0
+//   IF4 INT group: K = 96 Delta, C = -1.5 Delta (x = (q + 8) 2^-9)
+//   NVFP4        : K = Delta, C = 0
+// For IF4 the E4M3 conversion keeps the indicator bit as the sign (d = -Delta
+// for INT groups), so max(7 d / 32, -96 d) and min(1.5 d, 0) select the
+// constants without masks; C != 0 marks an INT group (an INT group with
+// Delta = 0 decodes to zeros either way).
+struct KC {
+    half2v K, C;
+};
+
+template <int FMT>
+__device__ __forceinline__ KC pair_kc(uint32_t sw)
+{
+    KC r;
+    if constexpr (Fmt<FMT>::ADAPTIVE) {
+        const half2v d = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw, 1.0f, false);
+        const half2v f = {(_Float16)Fold<FMT>::FP, (_Float16)Fold<FMT>::FP};
+        const half2v fi = {(_Float16)-96.0f, (_Float16)-96.0f};
+        const half2v c = {(_Float16)1.5f, (_Float16)1.5f};
+        const half2v z = {(_Float16)0.0f, (_Float16)0.0f};
+        r.K = __builtin_elementwise_max(d * f, d * fi);
+        r.C = __builtin_elementwise_min(d * c, z);
+    } else {
+        const half2v f = {(_Float16)Fold<FMT>::FP, (_Float16)Fold<FMT>::FP};
+        r.K = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw & 0x7F7Fu, 1.0f, false) * f;
+        r.C = half2v{(_Float16)0.0f, (_Float16)0.0f};
+    }
+    return r;
+}
+
+// Four operand pairs from one dword of 4-bit codes (elements 2i, 2i + 1 in
+// byte i).  INT codes: u = n ^ 8 per nibble, spread to bytes (u0 u1 u2 u3),
+// (u4 u5 u6 u7), and converted as E4M3 (exact u 2^-9).
+template <int FMT>
+__device__ __forceinline__ void decode_word_kc(uint32_t w, bool is_int, half2v K2, half2v C2,
+                                               uint32_t (&out)[4])
+{
+    uint32_t x[4];
+    x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 0));
+    x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 1));
+    x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 2));
+    x[3] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 3));
+    if constexpr (Fmt<FMT>::ADAPTIVE) {
+        const uint32_t w4 = w >> 4;
+        const uint32_t d0 = (__builtin_amdgcn_perm(w4, w, 0x05010400u) & 0x0F0F0F0Fu) ^ 0x08080808u;
+        const uint32_t d1 = (__builtin_amdgcn_perm(w4, w, 0x07030602u) & 0x0F0F0F0Fu) ^ 0x08080808u;
+        const uint32_t y0 = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d0, 1.0f, false));
+        const uint32_t y1 = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d0, 1.0f, true));
+        const uint32_t y2 = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d1, 1.0f, false));
+        const uint32_t y3 = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d1, 1.0f, true));
+        x[0] = is_int ? y0 : x[0];
+        x[1] = is_int ? y1 : x[1];
+        x[2] = is_int ? y2 : x[2];
+        x[3] = is_int ? y3 : x[3];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[i] = h2_as_u32(__builtin_elementwise_fma(u32_as_h2(x[i]), K2, C2));
+}
+
+// One group (two dwords w[0], w[1]) with the constants of half HS of kc.
+template <int FMT, int HS>
+__device__ __forceinline__ void decode_group_kc(const uint32_t* w, const KC& kc, uint32_t (&out)[8])
+{
+    const half2v K2 = {kc.K[HS], kc.K[HS]};
+    const half2v C2 = {kc.C[HS], kc.C[HS]};
+    const uint32_t cb = h2_as_u32(kc.C);
+    const bool is_int = Fmt<FMT>::ADAPTIVE && (HS ? (cb > 0xFFFFu) : ((cb & 0xFFFFu) != 0u));
+    uint32_t o0[4], o1[4];
+    decode_word_kc<FMT>(w[0], is_int, K2, C2, o0);
+    decode_word_kc<FMT>(w[1], is_int, K2, C2, o1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        out[i] = o0[i];
+        out[4 + i] = o1[i];
+    }
+}
+
+struct Ctx {
+    const uint8_t* a_codes;
+    const uint8_t* a_scales;
+    const uint8_t* b_codes;
+    const uint8_t* b_scales;
+    int64_t rowb;    // bytes per code row (K / 2)
+    int64_t gpr;     // groups (scale bytes) per row
+    int nch;         // 2-step chunks
+    int nsc;         // 8-step scale chunks
+    int64_t m0, n0;
+    uint8_t* dec;    // 3 decoded stages
+    uint8_t* raw;    // 2 raw B slots
+    uint8_t* scl;    // 2 scale slots
+};
+
+struct State {
+    u32x4 a[2][2][2];   // A codes [chunk slot][row block][16-byte half]
+    uint32_t as[2][2];  // A scale bytes [chunk slot][row block] (4 groups)
+    uint32_t bw[8];     // B codes of the next decode (4 groups, decode order)
+    uint32_t bs;        // their scale bytes
+    KC akc[2];          // A fold constants of the pair in use [row block]
+    half8 af[2][2][2];  // A fragments [group gg][row block][slice parity]
+    half8 bf[2][8];     // B fragments, double buffered over slices
+};
+
+// B codes of chunk cc (rows n0 .. n0 + 255, 64 bytes each) into raw slot:
+// instruction q of wave w covers rows 16 (4 q + w) .. + 15, four lanes per
+// row; piece p of a row is stored at position p ^ swz4(row).
+__device__ __forceinline__ void copy_b_chunk(const Ctx& x, int cc, uint8_t* slot)
+{
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int r0 = (4 * q + wave) * 16;
+        const int r = r0 + (lane >> 2);
+        const int p = (lane & 3) ^ swz4(r);
+        copy16(x.b_codes + (x.n0 + r) * x.rowb + (int64_t)cc * 64 + 16 * p,
+               __builtin_amdgcn_readfirstlane(lds_off(slot + r0 * 64)));
+    }
+}
+
+// Half `hf` of scale chunk e (hf 0: the A rows, 1: the B rows): 8
+// instructions of 32 rows x 32 bytes, two per wave.
+__device__ __forceinline__ void copy_scales(const Ctx& x, int e, int hf, uint8_t* slot)
+{
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const uint8_t* src = hf ? x.b_scales : x.a_scales;
+    const int64_t row0 = hf ? x.n0 : x.m0;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int r0 = (2 * wave + q) * 32;
+        const int r = r0 + (lane >> 1);
+        copy16(src + (row0 + r) * x.gpr + (int64_t)e * 32 + 16 * (lane & 1),
+               __builtin_amdgcn_readfirstlane(lds_off(slot + hf * kSclB + r0 * 32)));
+    }
+}
+
+// A codes of chunk cc for this lane: rows arow0 + 32 i, bytes 32 h .. 32 h + 31.
+__device__ __forceinline__ void load_a_chunk(const Ctx& x, int64_t arow0, int h, int cc, u32x4 (&a)[2][2])
+{
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const uint8_t* p = x.a_codes + (arow0 + 32 * i) * x.rowb + (int64_t)cc * 64 + 32 * h;
+        a[i][0] = load16(p);
+        a[i][1] = load16(p + 16);
+    }
+}
+
+// Scale bytes of A chunk c for this lane (4 groups per row block).
+__device__ __forceinline__ void read_a_scales(const Ctx& x, int c, int arow_local, int h, uint32_t (&as)[2])
+{
+    const uint8_t* sl = x.scl + ((c >> 2) & 1) * kSclBytes;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+        as[i] = *reinterpret_cast<const uint32_t*>(sl + (arow_local + 32 * i) * 32 + 8 * (c & 3) + 4 * h);
+}
+
+// B codes and scale bytes that step s decodes (B of step s + 2) -- chunk
+// (s + 2) / 2, step j = s % 2 of it -- for row t.
+__device__ __forceinline__ void read_b_raw(const Ctx& x, int sd, State& st)
+{
+    const int t = threadIdx.x;
+    const int c = sd >> 1, j = sd & 1;
+    const uint8_t* rs = x.raw + (c & 1) * kRawBytes + t * 64;
+    const int sw = swz4(t);
+    const u32x4 lo = *reinterpret_cast<const u32x4*>(rs + 16 * (j ^ sw));
+    const u32x4 hi = *reinterpret_cast<const u32x4*>(rs + 16 * ((2 + j) ^ sw));
+    st.bw[0] = lo.x; st.bw[1] = lo.y; st.bw[2] = lo.z; st.bw[3] = lo.w;
+    st.bw[4] = hi.x; st.bw[5] = hi.y; st.bw[6] = hi.z; st.bw[7] = hi.w;
+    const uint2 v = *reinterpret_cast<const uint2*>(x.scl + ((c >> 2) & 1) * kSclBytes + kSclB + t * 32 + 8 * (c & 3));
+    st.bs = __builtin_amdgcn_perm(v.y, v.x, j ? 0x07060302u : 0x05040100u);
+}
+
+// Decode B group G (0..3, decode order) of row t into stage `stg`: halves
+// 16 G .. 16 G + 15, i.e. pieces 2 G and 2 G + 1 (swizzled); kc holds the
+// constants of groups 2 (G / 2) and 2 (G / 2) + 1.
+template <int FMT, int G>
+__device__ __forceinline__ void decode_b_fast(const State& st, const KC& kc, uint8_t* stg)
+{
+    const int t = threadIdx.x;
+    uint32_t v[8];
+    decode_group_kc<FMT, G & 1>(st.bw + 2 * G, kc, v);
+    const int sw = swz8(t);
+    uint8_t* row = stg + t * 128;
+    *reinterpret_cast<u32x4*>(row + 16 * ((2 * G) ^ sw)) = u32x4{v[0], v[1], v[2], v[3]};
+    *reinterpret_cast<u32x4*>(row + 16 * ((2 * G + 1) ^ sw)) = u32x4{v[4], v[5], v[6], v[7]};
+}
+
+template <int FMT>
+__device__ __forceinline__ void decode_b_all(const State& st, uint8_t* stg)
+{
+    const KC k0 = pair_kc<FMT>(st.bs & 0xFFFFu), k1 = pair_kc<FMT>(st.bs >> 16);
+    decode_b_fast<FMT, 0>(st, k0, stg);
+    decode_b_fast<FMT, 1>(st, k0, stg);
+    decode_b_fast<FMT, 2>(st, k1, stg);
+    decode_b_fast<FMT, 3>(st, k1, stg);
+}
+
+// Decode local group G (0..3) of the lane's A chunk (one row block) with the
+// constants kc of its pair.
+template <int FMT, int G>
+__device__ __forceinline__ void decode_a_fast(const u32x4 (&a)[2], const KC& kc, half8& f0, half8& f1)
+{
+    const uint32_t w[2] = {G < 2 ? a[0][2 * (G & 1)] : a[1][2 * (G & 1)],
+                           G < 2 ? a[0][2 * (G & 1) + 1] : a[1][2 * (G & 1) + 1]};
+    uint32_t v[8];
+    decode_group_kc<FMT, G & 1>(w, kc, v);
+    f0 = __builtin_bit_cast(half8, u32x4{v[0], v[1], v[2], v[3]});
+    f1 = __builtin_bit_cast(half8, u32x4{v[4], v[5], v[6], v[7]});
+}
+
+__device__ __forceinline__ void read_bfrags_fast(const uint8_t* stg, int kk, int lane, half8 (&bf)[8])
+{
+    const int h = lane >> 5;
+    const uint8_t* base = stg + (lane & 31) * 128 + 16 * ((4 * h + kk) ^ swz8(lane & 31));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) bf[j] = *reinterpret_cast<const half8*>(base + j * 32 * 128);
+}
+
+// One K step s = 4 u + Q of the four-step loop body.  c = s / 2 is the A
+// chunk of this step (slot CS = Q / 2), j = Q % 2 the step within it.
+template <int FMT, int Q>
+__device__ __forceinline__ void step(const Ctx& x, State& st, int s, int64_t arow0, int arow_local,
+                                     uint8_t* Bs, uint8_t* Bn, uint8_t* Bd, floatx16 (&acc)[2][8])
+{
+    constexpr int j = Q & 1, CS = Q >> 1;
+    const int lane = threadIdx.x & 63;
+    const int h = lane >> 5;
+    const int c = s >> 1;
+    if constexpr (j == 1) {
+        copy_b_chunk(x, min(c + 3, x.nch - 1), x.raw + (CS ^ 1) * kRawBytes);
+        if constexpr (Q == 1) {
+            // scale chunk e = (u + 3) / 2, half (u + 1) % 2, for u = s / 4
+            const int u = s >> 2;
+            const int e = (u + 3) >> 1;
+            copy_scales(x, min(e, x.nsc - 1), (u + 1) & 1, x.scl + (e & 1) * kSclBytes);
+        }
+    } else {
+        read_a_scales(x, min(c + 1, x.nch - 1), arow_local, h, st.as[CS ^ 1]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    KC bkc;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+        const int f = kk & 1;
+        if (kk < 3)
+            read_bfrags_fast(Bs, kk + 1, lane, st.bf[f ^ 1]);
+        else
+            read_bfrags_fast(Bn, 0, lane, st.bf[f ^ 1]);
+        if (kk == 0) bkc = pair_kc<FMT>(st.bs & 0xFFFFu);
+        if (kk == 2) bkc = pair_kc<FMT>(st.bs >> 16);
+        if (kk == 0) decode_b_fast<FMT, 0>(st, bkc, Bd);
+        if (kk == 1) decode_b_fast<FMT, 1>(st, bkc, Bd);
+        if (kk == 2) decode_b_fast<FMT, 2>(st, bkc, Bd);
+        if (kk == 3) decode_b_fast<FMT, 3>(st, bkc, Bd);
+        if (kk == 3) read_b_raw(x, s + 3, st);
+        if (kk < 2) {
+            // group 1 of this step: local group 2 j + 1 of chunk c, whose pair
+            // constants were computed with group 2 j
+            decode_a_fast<FMT, 2 * j + 1>(st.a[CS][kk], st.akc[kk], st.af[1][kk][0], st.af[1][kk][1]);
+        } else {
+            if constexpr (j == 1) {
+                if (kk == 2) {
+                    // chunk c + 1 (loaded two steps ago) must have landed; then
+                    // refill slot CS, whose last group was decoded above
+                    vm_wait<Q == 1 ? 6 : 4>(st.a[CS ^ 1][0][0], st.a[CS ^ 1][0][1], st.a[CS ^ 1][1][0],
+                                            st.a[CS ^ 1][1][1]);
+                    load_a_chunk(x, arow0, h, min(c + 2, x.nch - 1), st.a[CS]);
+                }
+                // group 0 of the next step: local group 0 of chunk c + 1
+                st.akc[kk - 2] = pair_kc<FMT>(st.as[CS ^ 1][kk - 2] & 0xFFFFu);
+                decode_a_fast<FMT, 0>(st.a[CS ^ 1][kk - 2], st.akc[kk - 2], st.af[0][kk - 2][0],
+                                      st.af[0][kk - 2][1]);
+            } else {
+                // group 0 of the next step: local group 2 of chunk c
+                st.akc[kk - 2] = pair_kc<FMT>(st.as[CS][kk - 2] >> 16);
+                decode_a_fast<FMT, 2>(st.a[CS][kk - 2], st.akc[kk - 2], st.af[0][kk - 2][0],
+                                      st.af[0][kk - 2][1]);
+            }
+        }
+        const int gg = kk >> 1, par = kk & 1;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int jb = 0; jb < 8; ++jb)
+                acc[i][jb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(st.af[gg][i][par], st.bf[f][jb], acc[i][jb], 0, 0, 0);
+#pragma unroll
+        for (int m = 0; m < 16; ++m) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+            if (m < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            if (m == 3 || m == 7) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // even steps: the copies of the last odd step (B codes, scales) must have
+    // landed before the barrier makes them visible
+    if constexpr (j == 0) vm_wait<4>();
+    lds_barrier();
+}
+
+template <int FMT, bool OUT_BF16>
+__device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
+                                     const float* __restrict__ a_ts, const uint8_t* __restrict__ b_codes,
+                                     const uint8_t* __restrict__ b_scales, const float* __restrict__ b_ts,
+                                     int64_t M, int64_t N, int64_t K, void* __restrict__ C, int64_t ldc,
+                                     int64_t m0, int64_t n0, uint8_t* dec, uint8_t* raw, uint8_t* scl)
+{
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int h = lane >> 5;
+    const int arow_local = 64 * wave + (lane & 31);
+    const int64_t arow0 = m0 + arow_local;
+    Ctx x{a_codes, a_scales, b_codes, b_scales, K / 2, K / kGroup, (int)(K / 128), (int)(K / 512),
+          m0, n0, dec, raw, scl};
+    const int nsteps = (int)(K / kBK);
+
+    floatx16 acc[2][8];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int jb = 0; jb < 8; ++jb)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][jb][e] = 0.0f;
+
+    State st;
+    // prologue: B codes of chunks 0, 1; scale chunk 0 and the A half of
+    // chunk 1; A codes of chunk 0
+    copy_b_chunk(x, 0, raw);
+    copy_b_chunk(x, min(1, x.nch - 1), raw + kRawBytes);
+    copy_scales(x, 0, 0, scl);
+    copy_scales(x, 0, 1, scl);
+    copy_scales(x, min(1, x.nsc - 1), 0, scl + kSclBytes);
+    load_a_chunk(x, arow0, h, 0, st.a[0]);
+    vm_wait<0>(st.a[0][0][0], st.a[0][0][1], st.a[0][1][0], st.a[0][1][1]);
+    lds_barrier();
+    int r0 = 0, r1 = 1, r2 = 2;
+    read_b_raw(x, 0, st);
+    decode_b_all<FMT>(st, dec + r0 * kStageBytes);
+    read_b_raw(x, 1, st);
+    decode_b_all<FMT>(st, dec + r1 * kStageBytes);
+    read_b_raw(x, 2, st);
+    read_a_scales(x, 0, arow_local, h, st.as[0]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        st.akc[i] = pair_kc<FMT>(st.as[0][i] & 0xFFFFu);
+        decode_a_fast<FMT, 0>(st.a[0][i], st.akc[i], st.af[0][i][0], st.af[0][i][1]);
+    }
+    lds_barrier();
+    // the odd step before step 0: B codes of chunk 2 into slot 0, A codes of chunk 1
+    copy_b_chunk(x, min(2, x.nch - 1), raw);
+    load_a_chunk(x, arow0, h, min(1, x.nch - 1), st.a[1]);
+    read_bfrags_fast(dec + r0 * kStageBytes, 0, lane, st.bf[0]);
+
+    for (int s = 0; s < nsteps; s += 4) {
+        step<FMT, 0>(x, st, s, arow0, arow_local, dec + r0 * kStageBytes, dec + r1 * kStageBytes,
+                     dec + r2 * kStageBytes, acc);
+        step<FMT, 1>(x, st, s + 1, arow0, arow_local, dec + r1 * kStageBytes, dec + r2 * kStageBytes,
+                     dec + r0 * kStageBytes, acc);
+        step<FMT, 2>(x, st, s + 2, arow0, arow_local, dec + r2 * kStageBytes, dec + r0 * kStageBytes,
+                     dec + r1 * kStageBytes, acc);
+        step<FMT, 3>(x, st, s + 3, arow0, arow_local, dec + r0 * kStageBytes, dec + r1 * kStageBytes,
+                     dec + r2 * kStageBytes, acc);
+        // advance the ring by four steps (one position)
+        const int t0 = r1;
+        r1 = r2;
+        r2 = r0;
+        r0 = t0;
+    }
+    vm_wait<0>();
+    store_tile<FMT, OUT_BF16, false>(acc, a_ts, b_ts, M, N, C, ldc, m0, n0);
+}
+
+}  // namespace fast
+
+// Interior tiles on the fast path (4-bit formats, K % 512 == 0, 16-byte
+// aligned operands), with the same XCD-aware tile order as below.
+template <int FMT, bool OUT_BF16>
+__global__ __launch_bounds__(kGemmThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gemm_tn_fast(const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
+                  const float* __restrict__ a_ts, const uint8_t* __restrict__ b_codes,
+                  const uint8_t* __restrict__ b_scales, const float* __restrict__ b_ts,
+                  int64_t M, int64_t N, int64_t K, void* __restrict__ C, int64_t ldc,
+                  int tiles_m, int tiles_n)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t dec[3 * fast::kStageBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t raw[2 * fast::kRawBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t scl[2 * fast::kSclBytes];
+    int tm, tn;
+    tile_coords(tiles_m, tiles_n, tm, tn);
+    fast::tile<FMT, OUT_BF16>(a_codes, a_scales, a_ts, b_codes, b_scales, b_ts, M, N, K, C, ldc,
+                              (int64_t)tm * kBM, (int64_t)tn * kBN, dec, raw, scl);
+}
+
+// Interior tiles: every row, column and K group in range (K % 128 == 0,
+// 4-byte aligned scale rows).
+template <int FMT, bool OUT_BF16>
+__global__ __launch_bounds__(kGemmThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gemm_tn_interior(const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
+                      const float* __restrict__ a_ts, const uint8_t* __restrict__ b_codes,
+                      const uint8_t* __restrict__ b_scales, const float* __restrict__ b_ts,
+                      int64_t M, int64_t N, int64_t K, void* __restrict__ C, int64_t ldc,
+                      int tiles_m, int tiles_n)
+{
+    __shared__ __attribute__((aligned(16))) _Float16 lds[3][kStageHalves];
+    int tm, tn;
+    tile_coords(tiles_m, tiles_n, tm, tn);
     gemm_tile<FMT, OUT_BF16, false>(a_codes, a_scales, a_ts, b_codes, b_scales, b_ts, M, N, K, C,
                                     ldc, (int64_t)tm * kBM, (int64_t)tn * kBN, lds);
 }
@@ -467,7 +978,7 @@ void gemm_tn_edge(const uint8_t* __restrict__ a_codes, const uint8_t* __restrict
                   int64_t N, int64_t K, void* __restrict__ C, int64_t ldc, int full_m,
                   int n_start_tile, int ext_n, int tiles_n)
 {
-    __shared__ __attribute__((aligned(16))) _Float16 lds[2][kStageHalves];
+    __shared__ __attribute__((aligned(16))) _Float16 lds[3][kStageHalves];
     const int bid = blockIdx.x;
     int tm, tn;
     if (bid < full_m * ext_n) {
@@ -487,20 +998,27 @@ static hipError_t launch_g(const GemmArgs& a, hipStream_t s)
     const int64_t tiles_m = (a.M + kBM - 1) / kBM, tiles_n = (a.N + kBN - 1) / kBN;
     if (tiles_m == 0 || tiles_n == 0) return hipSuccess;
     if (tiles_m * tiles_n > (int64_t)1 << 30) return hipErrorInvalidValue;
-    const bool interior_ok = (a.K % kBK) == 0 && ((uintptr_t)a.a_scales % 4) == 0 &&
+    const bool interior_ok = (a.K % (2 * kBK)) == 0 && ((uintptr_t)a.a_scales % 4) == 0 &&
                              ((uintptr_t)a.b_scales % 4) == 0 && Fmt<FMT>::BITS == 4;
     const int64_t full_m = interior_ok ? a.M / kBM : 0;
     const int64_t full_n = interior_ok ? a.N / kBN : 0;
     if constexpr (Fmt<FMT>::BITS == 4) {
       if (full_m * full_n > 0) {
-        if (a.out_bf16)
-            hipLaunchKernelGGL((gemm_tn_interior<FMT, true>), dim3((unsigned)(full_m * full_n)),
-                               dim3(kGemmThreads), 0, s, a.a_codes, a.a_scales, a.a_ts, a.b_codes,
-                               a.b_scales, a.b_ts, a.M, a.N, a.K, a.c, a.ldc, (int)full_m, (int)full_n);
+        const bool fast_ok = (a.K % 512) == 0 && ((uintptr_t)a.a_codes % 16) == 0 &&
+                             ((uintptr_t)a.b_codes % 16) == 0 && ((uintptr_t)a.a_scales % 16) == 0 &&
+                             ((uintptr_t)a.b_scales % 16) == 0;
+        const dim3 grid((unsigned)(full_m * full_n)), block(kGemmThreads);
+#define IFQ_GEMM_ARGS a.a_codes, a.a_scales, a.a_ts, a.b_codes, a.b_scales, a.b_ts, a.M, a.N, a.K, a.c, a.ldc, \
+                      (int)full_m, (int)full_n
+        if (fast_ok && a.out_bf16)
+            hipLaunchKernelGGL((gemm_tn_fast<FMT, true>), grid, block, 0, s, IFQ_GEMM_ARGS);
+        else if (fast_ok)
+            hipLaunchKernelGGL((gemm_tn_fast<FMT, false>), grid, block, 0, s, IFQ_GEMM_ARGS);
+        else if (a.out_bf16)
+            hipLaunchKernelGGL((gemm_tn_interior<FMT, true>), grid, block, 0, s, IFQ_GEMM_ARGS);
         else
-            hipLaunchKernelGGL((gemm_tn_interior<FMT, false>), dim3((unsigned)(full_m * full_n)),
-                               dim3(kGemmThreads), 0, s, a.a_codes, a.a_scales, a.a_ts, a.b_codes,
-                               a.b_scales, a.b_ts, a.M, a.N, a.K, a.c, a.ldc, (int)full_m, (int)full_n);
+            hipLaunchKernelGGL((gemm_tn_interior<FMT, false>), grid, block, 0, s, IFQ_GEMM_ARGS);
+#undef IFQ_GEMM_ARGS
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
       }

@@ -53,6 +53,41 @@ def test_shapes(fmt, dtype):
         _check(fmt, pa, oa, pb, ob, dtype, tag=f"{fmt} {M}x{N}x{K}")
 
 
+@pytest.mark.parametrize("fmt", GEMM_FORMATS)
+@pytest.mark.parametrize("dtype", [ops.F32, ops.BF16])
+def test_shapes_k_multiple_of_512(fmt, dtype):
+    """Shapes whose full 256 x 256 tiles take the interior kernel with
+    line-sized operand copies (4-bit formats, K % 512 == 0), alone and next
+    to boundary tiles."""
+    rng = np.random.default_rng(60 + fmt)
+    for (M, N, K) in [(256, 256, 512), (512, 768, 1024), (600, 520, 1536), (1024, 256, 4096)]:
+        a = workloads.to_bf16(rng.standard_t(3, (M, K)))
+        b = workloads.to_bf16(rng.standard_normal((N, K)) * 0.02)
+        pa, oa, pb, ob = _quantized_pair(fmt, a, b)
+        _check(fmt, pa, oa, pb, ob, dtype, tag=f"{fmt} {M}x{N}x{K}")
+
+
+def test_unaligned_scales_take_the_general_path():
+    """Scale buffers that start 4 bytes past a 16-byte boundary cannot use the
+    line-sized operand copies (codes must be 16-byte aligned by contract);
+    the product must not change."""
+    rng = np.random.default_rng(70)
+    M, N, K = 512, 512, 1024
+    a = workloads.to_bf16(rng.standard_t(3, (M, K)))
+    b = workloads.to_bf16(rng.standard_normal((N, K)) * 0.02)
+    pa, oa, pb, ob = _quantized_pair(ops.IF4, a, b)
+    ref = O.gemm_ref(oa[0], oa[1], oa[2], ob[0], ob[1], ob[2])
+
+    def shifted(p):
+        sb = torch.empty(p.scales.numel() + 4, dtype=torch.uint8, device="cuda")
+        scales = sb[4:].view(p.scales.shape)
+        scales.copy_(p.scales)
+        return ops.Packed(p.fmt, p.codes, scales, p.tensor_scale, p.rows, p.cols)
+
+    c = ops.if4_gemm(shifted(pa), shifted(pb), ops.F32).cpu().numpy()
+    assert rel_fro(c, ref) <= TOL
+
+
 def test_k_zero_gives_zeros():
     a = torch.zeros((5, 0), dtype=torch.bfloat16).cuda()
     pa = ops.if4_quantize(a)
