@@ -35,8 +35,8 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-rows", type=int, default=1024,
-                   help="activation rows in the CPU oracle's GEMM sample")
+    p.add_argument("--cpu-rows", type=int, default=0,
+                   help="activation rows in the CPU oracle's GEMM sample (0: all)")
     p.add_argument("--traffic-from", metavar="DIR",
                    help="read rocprofv3 FETCH_SIZE/WRITE_SIZE counter CSVs of a --mode step run "
                         "(DIR/pmc_FETCH_SIZE, DIR/pmc_WRITE_SIZE) and write profiles/hbm_traffic.json")
@@ -172,13 +172,13 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2),
                      "peak": FP16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(gemm_tflops / FP16_MFMA_PEAK_TFLOPS, 4),
-                     "traffic": gemm_traffic(M, N, K), "traffic_unit": "HBM bytes per launch",
-                     "kernel": "gemm_tn_interior<IF4, bf16 out>"},
+                     "traffic": recorded_traffic("gemm", (M, N, K)),
+                     "traffic_unit": "HBM bytes per launch", "kernel": "gemm_tn_fast<IF4, bf16 out>"},
         "roofline_quantize": {
             "bound": "hbm", "kernel": "quantize_rows<IF4> (alpha supplied, single pass, W)",
             "achieved": round(qbytes_1pass(n_w) / t_w_1p / 1e9, 1), "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": round(qbytes_1pass(n_w) / t_w_1p / 1e9 / HBM_PEAK_GBS, 4),
-            "traffic": None},
+            "traffic": recorded_traffic("quantize_W", (N, K)), "traffic_unit": "HBM bytes per launch"},
         "components": {
             "if4": {"quant_A_us": round(res["quant_A_s"] * 1e6, 2),
                     "quant_A_GBps_2pass": round(qbytes_2pass(n_a) / res["quant_A_s"] / 1e9, 1),
@@ -197,37 +197,44 @@ def main():
         },
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, M, N, K, args.cpu_rows)
+        out["cpu_baseline"] = cpu_baseline(w, M, N, K, args.cpu_rows or M)
     print(json.dumps(out), flush=True)
 
 
-GEMM_SOURCES = ("paper_2603_28765_amd/csrc/gemm.hip", "paper_2603_28765_amd/csrc/device.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
-GEMM_KERNEL = "ifq::gemm_tn_interior<0, true>"
+# Kernels whose HBM traffic bench.py reports: record key -> (kernel name in
+# the profiler, which of its dispatches per step, sources it is built from).
+TRAFFIC_KERNELS = {
+    "gemm": ("ifq::gemm_tn_fast<0, true>", None,
+             ("paper_2603_28765_amd/csrc/gemm.hip", "paper_2603_28765_amd/csrc/device.h")),
+    "quantize_W": ("ifq::quantize_rows<0, false, false>", 1,
+                   ("paper_2603_28765_amd/csrc/quantize.hip", "paper_2603_28765_amd/csrc/device.h")),
+}
 # Per-dispatch calibration of the byte counters against a plain 1 GiB device
 # copy (bench.py --mode copy): FETCH_SIZE reads back half the bytes read,
 # WRITE_SIZE the bytes written.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 
 
-def _sources_digest():
+def _sources_digest(files):
     import hashlib
     h = hashlib.sha256()
-    for f in GEMM_SOURCES:
+    for f in files:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
 
-def gemm_traffic(M, N, K):
-    """Counter-measured HBM bytes per GEMM launch, or None when the record is
-    missing, was taken at another shape, or the GEMM sources changed since."""
+def recorded_traffic(key, shape):
+    """Counter-measured HBM bytes per launch of kernel `key`, or None when the
+    record is missing, was taken at another shape, or the kernel's sources
+    changed since."""
     try:
         with open(TRAFFIC_FILE) as fh:
-            rec = json.load(fh)["gemm"]
+            rec = json.load(fh)[key]
     except (OSError, KeyError, ValueError):
         return None
-    if rec.get("sha256") != _sources_digest() or rec.get("shape") != [M, N, K]:
+    if rec.get("sha256") != _sources_digest(TRAFFIC_KERNELS[key][2]) or rec.get("shape") != list(shape):
         return None
     return int(rec["fetch_bytes"] + rec["write_bytes"])
 
@@ -235,22 +242,28 @@ def gemm_traffic(M, N, K):
 def record_traffic(d):
     import csv
 
-    def per_dispatch(sub):
+    def per_dispatch(sub, kernel, which):
         vals = []
         for root, _, files in os.walk(os.path.join(d, sub)):
-            for f in files:
+            for f in sorted(files):
                 if f.endswith("counter_collection.csv"):
                     with open(os.path.join(root, f)) as fh:
                         vals += [float(r["Counter_Value"]) for r in csv.DictReader(fh)
-                                 if r["Kernel_Name"].replace("void ", "").startswith(GEMM_KERNEL)]
+                                 if r["Kernel_Name"].replace("void ", "").startswith(kernel)]
+        if which is not None:  # every second dispatch: the W operand of each step
+            vals = vals[which::2]
         if not vals:
-            raise SystemExit(f"no {GEMM_KERNEL} dispatches under {os.path.join(d, sub)}")
+            raise SystemExit(f"no {kernel} dispatches under {os.path.join(d, sub)}")
         return sum(vals) / len(vals) * 1024.0
-    fetch = per_dispatch("pmc_FETCH_SIZE") * FETCH_SCALE
-    write = per_dispatch("pmc_WRITE_SIZE") * WRITE_SCALE
-    rec = {"gemm": {"kernel": GEMM_KERNEL, "shape": [8192, 14336, 4096], "sources": list(GEMM_SOURCES),
-                    "sha256": _sources_digest(), "fetch_bytes": round(fetch), "write_bytes": round(write),
-                    "calibration": {"FETCH_SIZE": FETCH_SCALE, "WRITE_SIZE": WRITE_SCALE}}}
+
+    shapes = {"gemm": [8192, 14336, 4096], "quantize_W": [14336, 4096]}
+    rec = {}
+    for key, (kernel, which, sources) in TRAFFIC_KERNELS.items():
+        rec[key] = {"kernel": kernel, "shape": shapes[key], "sources": list(sources),
+                    "sha256": _sources_digest(sources),
+                    "fetch_bytes": round(per_dispatch("pmc_FETCH_SIZE", kernel, which) * FETCH_SCALE),
+                    "write_bytes": round(per_dispatch("pmc_WRITE_SIZE", kernel, which) * WRITE_SCALE),
+                    "calibration": {"FETCH_SIZE": FETCH_SCALE, "WRITE_SIZE": WRITE_SCALE}}
     with open(TRAFFIC_FILE, "w") as fh:
         json.dump(rec, fh, indent=1)
         fh.write("\n")
