@@ -98,7 +98,21 @@ __global__ __launch_bounds__(kThreads) void tensor_max_rows(const uint16_t* __re
     float m = 0.0f;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     for (int64_t r = blockIdx.y; r < nrows; r += gridDim.y) {
-        for (int64_t gc = (int64_t)blockIdx.x * kThreads + threadIdx.x; gc < gpr; gc += stride) {
+        int64_t gc = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+        // four groups' loads in flight per lane: the grid is small (at most
+        // kMaxPartials blocks), so bytes in flight come from unrolling
+        for (; gc + 3 * stride < gpr; gc += 4 * stride) {
+            float v[4][kGroup];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) load_group_rowwise(x + r * ld + (gc + u * stride) * kGroup, v[u]);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if constexpr (RHT) rht16(v[u], signs);
+#pragma unroll
+                for (int j = 0; j < kGroup; ++j) m = fmaxf(m, fabsf(v[u][j]));
+            }
+        }
+        for (; gc < gpr; gc += stride) {
             float v[kGroup];
             load_group_rowwise(x + r * ld + gc * kGroup, v);
             if constexpr (RHT) rht16(v, signs);
@@ -225,6 +239,151 @@ __global__ __launch_bounds__(kThreads) void quantize_strided(
     }
 }
 
+// ------------------------------------------- strided axis, register path
+// When rows are 16-byte aligned (x and ld) and cols % 8 == 0, a lane loads
+// the same 16 bytes (8 columns) from 16 consecutive rows: one wave
+// instruction reads 1 KiB of one row, fully coalesced.  The lane then holds
+// 8 complete column groups in 16 registers and quantizes them one after
+// another -- no LDS and no barriers.  A block covers 512 columns (4
+// wavefronts x 64 lanes x 8 columns); wavefront w of a block takes row
+// groups w, w + 4, ... of the block's row range.
+constexpr int kColsPerBlock = 64 * 8;          // 512: every wave spans the block's 512 columns
+
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void load_col_block(const uint16_t* __restrict__ p, int64_t ld, u32x4v (&r)[kGroup])
+{
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) r[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(p + j * ld));
+}
+
+// Column c (0..7) of the 16 x 8 bf16 block as 16 floats.
+__device__ __forceinline__ void column_of(const u32x4v (&r)[kGroup], int c, float (&v)[kGroup])
+{
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+        const uint32_t w = r[j][c >> 1];
+        v[j] = (c & 1) ? bf16hi(w) : bf16lo(w);
+    }
+}
+
+template <bool RHT>
+__global__ __launch_bounds__(kThreads) void tensor_max_cols(const uint16_t* __restrict__ x,
+                                                            int64_t rows, int64_t cols, int64_t ld,
+                                                            uint32_t signs, float* __restrict__ partials)
+{
+    __shared__ float red[kThreads / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t ngroups = rows / kGroup;
+    float m = 0.0f;
+    for (int64_t cb = blockIdx.x; cb * kColsPerBlock < cols; cb += gridDim.x) {
+        const int64_t col = cb * kColsPerBlock + 8 * lane;
+        if (col >= cols) continue;
+        for (int64_t g = (int64_t)blockIdx.y * 4 + wave; g < ngroups; g += (int64_t)gridDim.y * 4) {
+            u32x4v r[kGroup];
+            load_col_block(x + g * kGroup * ld + col, ld, r);
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                float v[kGroup];
+                column_of(r, c, v);
+                if constexpr (RHT) rht16(v, signs);
+#pragma unroll
+                for (int j = 0; j < kGroup; ++j) m = fmaxf(m, fabsf(v[j]));
+            }
+        }
+    }
+    m = block_max(m, red);
+    if (threadIdx.x == 0) partials[blockIdx.y * gridDim.x + blockIdx.x] = m;
+}
+
+// Pass 2 of the register path.  A block owns a tile of 64 columns x 2048
+// rows (128 groups per output row) and stages its output in LDS so that
+// every output row segment -- 1 KiB of codes and 128 bytes of scales -- is
+// written as whole cache lines.  Lane l of wavefront w handles column chunk
+// l / 8 (8 columns) and group l % 8 of the wavefront's 8 groups per round;
+// one load instruction reads 16 B from each of 8 rows' 128-byte column
+// segments.  LDS rows are XOR-swizzled by 8 (col / 8) slots, which keeps the
+// 8-byte code writes of a 32-lane pass on distinct banks.
+constexpr int kColTile = 64;          // columns (output rows) per block
+constexpr int kGrpTile = 128;         // groups per output row per block
+constexpr int kCodeRowBytes = kGrpTile * 8;
+
+template <int FMT, bool RHT, bool SR>
+__global__ __launch_bounds__(kThreads) void quantize_cols(
+    const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t ld, uint32_t signs,
+    uint64_t seed, float scale_max, float denom_alpha, int scale_in,
+    const float* __restrict__ partials, int npartials, uint8_t* __restrict__ codes,
+    uint8_t* __restrict__ scales, float* tensor_scale)
+{
+    static_assert(Fmt<FMT>::BITS == 4, "register path stores 8-byte code groups");
+    __shared__ __attribute__((aligned(16))) uint8_t lcodes[kColTile * kCodeRowBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t lscales[kColTile * kGrpTile];
+    __shared__ float red[kThreads / 64];
+    const float alpha = resolve_alpha(scale_in, tensor_scale, partials, npartials, denom_alpha, red);
+    const float denom = alpha * scale_max;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int64_t ngroups = rows / kGroup;  // groups per output row (= per column of X)
+    const int64_t c0 = (int64_t)blockIdx.x * kColTile, g0 = (int64_t)blockIdx.y * kGrpTile;
+    const int ntg = (int)min<int64_t>(kGrpTile, ngroups - g0);
+    const int ncol = (int)min<int64_t>(kColTile, cols - c0);
+    const int cc = lane >> 3, q = lane & 7;
+    const int sw = 8 * cc;  // swizzle of the LDS rows 8 cc .. 8 cc + 7
+    for (int rg = 0; rg < ntg; rg += 32) {
+        const int gl = rg + 8 * wave + q;
+        if (gl < ntg && 8 * cc < ncol) {
+            u32x4v r[kGroup];
+            load_col_block(x + (g0 + gl) * kGroup * ld + c0 + 8 * cc, ld, r);
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                float v[kGroup];
+                column_of(r, c, v);
+                if constexpr (RHT) rht16(v, signs);
+                const int64_t gi = (c0 + 8 * cc + c) * ngroups + g0 + gl;  // SR counter: global group index
+                uint2 pk;
+                uint32_t sb;
+                if constexpr (!SR) {
+                    sb = quantize_group_e2m1<Fmt<FMT>::ADAPTIVE>(v, alpha, denom, pk);
+                } else {
+                    uint32_t w[8];
+                    sr_words(seed, (uint64_t)gi, w);
+                    uint32_t cq[kGroup];
+                    sb = quantize_group<FMT, true>(v, alpha, denom, w, cq);
+                    const Packed<4> pp = pack16<4>(cq);
+                    pk = make_uint2(pp.w[0], pp.w[1]);
+                }
+                const int row = 8 * cc + c;
+                *reinterpret_cast<uint2*>(lcodes + row * kCodeRowBytes + (gl ^ sw) * 8) = pk;
+                lscales[row * kGrpTile + (gl ^ sw)] = (uint8_t)sb;
+            }
+        }
+    }
+    __syncthreads();
+    // codes: ncol rows x ntg * 8 bytes, 16-byte pieces (groups 2p, 2p + 1)
+    const int ppr = ntg / 2;
+    for (int idx = t; idx < ncol * ppr; idx += kThreads) {
+        const int row = idx / ppr, pc = idx % ppr;
+        const int s = 8 * (row >> 3);
+        const uint4 v = *reinterpret_cast<const uint4*>(lcodes + row * kCodeRowBytes + ((2 * pc) ^ s) * 8);
+        *reinterpret_cast<uint4*>(codes + ((c0 + row) * ngroups + g0 + 2 * pc) * 8) = v;
+    }
+    // scales: ncol rows x ntg bytes, 16-byte pieces (bytes keep the swizzle of 8-slot blocks)
+    const int spr = ntg / 16;
+    for (int idx = t; idx < ncol * spr; idx += kThreads) {
+        const int row = idx / spr, pc = idx % spr;
+        const int s = 8 * (row >> 3);
+        uint32_t w4[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            uint32_t wv = 0;
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+                wv |= (uint32_t)lscales[row * kGrpTile + ((16 * pc + 4 * k + b) ^ s)] << (8 * b);
+            w4[k] = wv;
+        }
+        *reinterpret_cast<uint4*>(scales + (c0 + row) * ngroups + g0 + 16 * pc) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+    }
+}
+
 __global__ void write_scalar(float* p, float v) { *p = v; }
 
 // ------------------------------------------------------------- launcher
@@ -237,11 +396,37 @@ static inline int strided_vec_ok(const QuantArgs& a)
     return (reinterpret_cast<uintptr_t>(a.x) % 16 == 0 && a.ld % 8 == 0) ? 1 : 0;
 }
 
+// The register path loads 16 bytes (8 columns) per lane and row and stores
+// 16-byte pieces of codes and scales: 4-bit formats, 16-byte aligned rows of
+// X, cols % 8 == 0, and 16 groups per output row multiple (rows % 256 == 0)
+// with 16-byte aligned code and scale buffers.
+static inline bool strided_load_ok(const QuantArgs& a)
+{
+    return reinterpret_cast<uintptr_t>(a.x) % 16 == 0 && a.ld % 8 == 0 && a.cols % 8 == 0;
+}
+
+template <int FMT>
+static inline bool strided_cols_ok(const QuantArgs& a)
+{
+    return Fmt<FMT>::BITS == 4 && strided_load_ok(a) && (a.rows / kGroup) % 16 == 0 &&
+           a.rows / kGroup / kGrpTile < 65536 && reinterpret_cast<uintptr_t>(a.codes) % 16 == 0 &&
+           reinterpret_cast<uintptr_t>(a.scales) % 16 == 0;
+}
+
 template <int FMT, bool RHT, bool SR>
 static hipError_t launch_q(const QuantArgs& a, hipStream_t s, int npartials, float scale_max,
                            float denom_alpha)
 {
     const int scale_in = (a.flags & IFQ_SCALE_IN) ? 1 : 0;
+    if constexpr (Fmt<FMT>::BITS == 4) {
+        if ((a.flags & IFQ_AXIS_STRIDED) && strided_cols_ok<FMT>(a)) {
+            dim3 grid((unsigned)cdiv(a.cols, kColTile), (unsigned)cdiv(a.rows / kGroup, kGrpTile));
+            hipLaunchKernelGGL((quantize_cols<FMT, RHT, SR>), grid, dim3(kThreads), 0, s, a.x, a.rows,
+                               a.cols, a.ld, a.signs, a.seed, scale_max, denom_alpha, scale_in, a.partials,
+                               npartials, a.codes, a.scales, a.tensor_scale);
+            return hipGetLastError();
+        }
+    }
     if (a.flags & IFQ_AXIS_STRIDED) {
         dim3 grid((unsigned)cdiv(a.cols, kTC), (unsigned)std::min<int64_t>(cdiv(a.rows, kTR), 65535));
         hipLaunchKernelGGL((quantize_strided<FMT, RHT, SR>), grid, dim3(kThreads), 0, s, a.x,
@@ -263,7 +448,13 @@ static hipError_t launch_q(const QuantArgs& a, hipStream_t s, int npartials, flo
 template <bool RHT>
 static hipError_t launch_tensor_max(const QuantArgs& a, hipStream_t s, int* npartials)
 {
-    if (a.flags & IFQ_AXIS_STRIDED) {
+    if ((a.flags & IFQ_AXIS_STRIDED) && strided_load_ok(a)) {
+        int64_t bx = std::min<int64_t>(cdiv(a.cols, kColsPerBlock), kMaxPartials);
+        int64_t by = std::max<int64_t>(1, std::min<int64_t>(cdiv(a.rows / kGroup, 4), kMaxPartials / bx));
+        *npartials = (int)(bx * by);
+        hipLaunchKernelGGL((tensor_max_cols<RHT>), dim3((unsigned)bx, (unsigned)by), dim3(kThreads), 0,
+                           s, a.x, a.rows, a.cols, a.ld, a.signs, a.partials);
+    } else if (a.flags & IFQ_AXIS_STRIDED) {
         int64_t tx = cdiv(a.cols, kTC), ty = cdiv(a.rows, kTR);
         int64_t bx = std::min<int64_t>(tx, kMaxPartials);
         int64_t by = std::max<int64_t>(1, std::min<int64_t>(ty, kMaxPartials / bx));

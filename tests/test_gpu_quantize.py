@@ -52,8 +52,12 @@ def test_rowwise_all_formats_and_flags(fmt, flags):
 @pytest.mark.parametrize("fmt", FORMATS)
 @pytest.mark.parametrize("flags", FLAG_SETS)
 def test_strided_axis(fmt, flags):
+    # 4-bit formats with cols % 8 == 0 and rows % 256 == 0 take the register
+    # path (here (512, 1032), with a partial last 64-column tile); the other
+    # shapes and formats the LDS-tile path
     for shape, kind, seed in [((48, 37), "normal", 5), ((256, 100), "outliers", 6),
-                              ((16, 1), "normal", 7), ((128, 64), "wide", 8)]:
+                              ((16, 1), "normal", 7), ((128, 64), "wide", 8),
+                              ((512, 1032), "outliers", 9), ((272, 520), "normal", 10)]:
         x = rand_bf16(shape, seed + 10 * fmt, kind)
         assert_quant_equal(fmt, x, flags | ops.AXIS_STRIDED, signs=0x3C5A, seed=777,
                            tag=f"strided fmt {fmt} flags {flags} {shape}")
@@ -73,6 +77,13 @@ def test_non_contiguous_rows():
     for fmt in (ops.IF4, ops.IF3, ops.IF6_E2M3):
         assert_quant_equal(fmt, x, 0, ld_pad=24, tag="ld padded")
         assert_quant_equal(fmt, x, ops.RHT | ops.SR, signs=0x1234, seed=5, ld_pad=8, tag="ld padded rht sr")
+    # strided axis: ld % 8 == 0 keeps the register path, ld % 8 != 0 the LDS path
+    xs = rand_bf16((256, 328), 12, "outliers")
+    for fmt in (ops.IF4, ops.NVFP4, ops.IF3):
+        for pad in (8, 3):
+            assert_quant_equal(fmt, xs, ops.AXIS_STRIDED, ld_pad=pad, tag=f"strided ld +{pad}")
+            assert_quant_equal(fmt, xs, ops.AXIS_STRIDED | ops.RHT | ops.SR, signs=0x4321, seed=6,
+                               ld_pad=pad, tag=f"strided ld +{pad} rht sr")
 
 
 def test_ties_and_signed_zero():
@@ -150,6 +161,16 @@ def test_full_size_quant_sweep():
     for fmt in (ops.IF4, ops.NVFP4):
         assert_quant_equal(fmt, x, 0, tag="full sweep")
         assert_quant_equal(fmt, x, ops.RHT, signs=w.info["rht_signs"], tag="full sweep rht")
+
+
+def test_full_size_wgrad_operands():
+    """The weight-gradient operands at full size (dY 8192 x 14336, X 8192 x
+    4096), quantized along the token axis with RHT, SR and the 16/17 margin:
+    bit-exact over the whole tensors."""
+    w = workloads.wgrad()
+    fl = ops.AXIS_STRIDED | ops.RHT | ops.SR | ops.MARGIN_16_17
+    assert_quant_equal(ops.IF4, w.tensors["dY"], fl, w.info["rht_signs"], w.info["sr_seed_dY"], tag="dY")
+    assert_quant_equal(ops.IF4, w.tensors["X"], fl, w.info["rht_signs"], w.info["sr_seed_X"], tag="X")
 
 
 def test_determinism_repeat():
