@@ -164,7 +164,10 @@ int ifx_dequantize(int format, const uint8_t* codes, const uint8_t* scales,
  * that carries its group scale exactly (7 q Delta for FP groups, 6 q Delta
  * for INT groups), so one FP32 accumulation over all of K applies every
  * block's scale pair and range alignment; alpha_A * alpha_B / 49 is applied
- * once at the end.
+ * once at the end.  NVFP4 and IF3 operands are exact the same way; IF6
+ * operands (62 q Delta and 15 q Delta for E2M3, 31 q Delta and 28 q Delta
+ * for E3M2, Sec. 5.1 ratios) need up to 13 significant bits and are rounded
+ * once to FP16 (relative error at most 2^-12 per operand).
  *   a_codes, a_scales  (device) A packed [M, K]; b_* : B packed [N, K]
  *   a_tensor_scale, b_tensor_scale  (device) alpha of A and of B
  *   c                  (device) [M, ldc] fp32 or bf16 (out_dtype); ldc >= N

@@ -98,7 +98,6 @@ int gemm_impl(int fmt, const uint8_t* a_codes, const uint8_t* a_scales, const fl
     if ((M > 0 && K > kMaxElems / M) || (N > 0 && K > kMaxElems / N) ||
         (M > 0 && N > 0 && M > kMaxElems / N))
         return IFQ_ESHAPE;
-    if (fmt == IFQ_FMT_IF6_E2M3 || fmt == IFQ_FMT_IF6_E3M2) return IFQ_EUNSUPPORTED;
     if (M == 0 || N == 0) return IFQ_OK;
     if (ldc < N) return IFQ_ESHAPE;
     if (!c || !a_ts || !b_ts) return IFQ_EINVAL;

@@ -56,6 +56,18 @@ template <> struct Fold<IFQ_FMT_IF4> {
 };
 template <> struct Fold<IFQ_FMT_NVFP4> { static constexpr float FP = 1.0f, INT = 1.0f, EPI = 1.0f; };
 template <> struct Fold<IFQ_FMT_IF3> { static constexpr float FP = 3.0f, INT = 4.0f, EPI = 1.0f / 9.0f; };
+// IF6: FP x 62 and INT x 15 (E2M3, ratio 7.5/31) or x 31 and x 28 (E3M2,
+// ratio 28/31), times lambda = 1/4 or 1/8 so that 7.5*62*448*lambda and
+// 28*31*448*lambda stay below the FP16 maximum.  With Delta the operand has
+// up to 13 significant bits and is rounded once to FP16 (relative error at
+// most 2^-12 per operand; the only inexact step of the GEMM besides FP32
+// accumulation).
+template <> struct Fold<IFQ_FMT_IF6_E2M3> {
+    static constexpr float FP = 62.0f / 4.0f, INT = 15.0f / 4.0f, EPI = 1.0f / (15.5f * 15.5f);
+};
+template <> struct Fold<IFQ_FMT_IF6_E3M2> {
+    static constexpr float FP = 31.0f / 8.0f, INT = 28.0f / 8.0f, EPI = 64.0f / 961.0f;
+};
 
 __device__ __forceinline__ uint32_t h2_as_u32(half2v h) { return __builtin_bit_cast(uint32_t, h); }
 __device__ __forceinline__ half2v u32_as_h2(uint32_t u) { return __builtin_bit_cast(half2v, u); }
@@ -150,6 +162,32 @@ __device__ __forceinline__ void decode_if3_group(uint64_t bitsv, bool is_int, ui
     }
 }
 
+// Sixteen six-bit IF6 codes (96 bits in w[0..2], code j at bits 6j) -> 8
+// FP16 operand pairs: Fold::FP * q (FP, sign-magnitude ExMy) or Fold::INT * q
+// (INT6 two's complement), times Delta, rounded once to FP16.
+template <int FMT>
+__device__ __forceinline__ void decode_if6_group(const uint32_t* w, uint32_t sbyte, uint32_t (&out)[8])
+{
+    const bool is_int = (sbyte >> 7) & 1u;
+    const float delta = e4m3_value(sbyte & 0x7Fu);
+    const uint64_t lo = (uint64_t)w[0] | ((uint64_t)w[1] << 32);
+    const uint64_t hi = (uint64_t)w[1] | ((uint64_t)w[2] << 32);  // bits 32 .. 95
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        half2v hv;
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int bit = 6 * (2 * i + e);
+            const uint32_t c = (uint32_t)((bit <= 58 ? (lo >> bit) : (hi >> (bit - 32))) & 63u);
+            const float qi = (float)((int)(c << 26) >> 26);
+            const float mag = fp_magnitude<FMT>(c & 31u);
+            const float qf = (c & 32u) ? -mag : mag;
+            hv[e] = (_Float16)((is_int ? qi * Fold<FMT>::INT : qf * Fold<FMT>::FP) * delta);
+        }
+        out[i] = h2_as_u32(hv);
+    }
+}
+
 // ------------------------------------------------------------ raw chunks
 // A: one lane's 32 k-values of one row for one step (2 groups);
 // B: one thread's 64 k-values of one row (4 groups).  IF3 keeps 6-byte groups.
@@ -157,6 +195,10 @@ template <int FMT> struct RawA { uint32_t w[4]; uint32_t sb; };
 template <> struct RawA<IFQ_FMT_IF3> { uint16_t h[6]; uint32_t sb; };
 template <int FMT> struct RawB { uint32_t w[8]; uint32_t sb; };
 template <> struct RawB<IFQ_FMT_IF3> { uint16_t h[12]; uint32_t sb; };
+template <> struct RawA<IFQ_FMT_IF6_E2M3> { uint32_t w[6]; uint32_t sb; };
+template <> struct RawA<IFQ_FMT_IF6_E3M2> { uint32_t w[6]; uint32_t sb; };
+template <> struct RawB<IFQ_FMT_IF6_E2M3> { uint32_t w[12]; uint32_t sb; };
+template <> struct RawB<IFQ_FMT_IF6_E3M2> { uint32_t w[12]; uint32_t sb; };
 
 // Load `ng` groups (2 or 4) of one row starting at group g0 into words /
 // halves.  Interior tiles (EDGE = false) load without guards.
@@ -189,6 +231,11 @@ __device__ __forceinline__ void load_groups(const uint8_t* __restrict__ codes,
                 const uint2 t = ok ? *reinterpret_cast<const uint2*>(cp + 8 * g) : make_uint2(0, 0);
                 w[2 * g] = t.x;
                 w[2 * g + 1] = t.y;
+            } else if constexpr (BITS == 6) {
+                const uint32_t* p = reinterpret_cast<const uint32_t*>(cp + 12 * g);
+                w[3 * g] = ok ? p[0] : 0u;
+                w[3 * g + 1] = ok ? p[1] : 0u;
+                w[3 * g + 2] = ok ? p[2] : 0u;
             } else {
                 const uint16_t* p = reinterpret_cast<const uint16_t*>(cp + 6 * g);
                 h[3 * g] = ok ? p[0] : (uint16_t)0;
@@ -204,7 +251,7 @@ template <int FMT, bool EDGE>
 __device__ __forceinline__ void load_a(const uint8_t* __restrict__ codes, const uint8_t* __restrict__ scales,
                                        int64_t row, int64_t nrows, int64_t gpr, int64_t g0, RawA<FMT>& r)
 {
-    if constexpr (Fmt<FMT>::BITS == 4)
+    if constexpr (Fmt<FMT>::BITS != 3)
         load_groups<FMT, EDGE, 2>(codes, scales, row, nrows, gpr, g0, r.w, nullptr, r.sb);
     else
         load_groups<FMT, EDGE, 2>(codes, scales, row, nrows, gpr, g0, nullptr, r.h, r.sb);
@@ -214,7 +261,7 @@ template <int FMT, bool EDGE>
 __device__ __forceinline__ void load_b(const uint8_t* __restrict__ codes, const uint8_t* __restrict__ scales,
                                        int64_t row, int64_t nrows, int64_t gpr, int64_t g0, RawB<FMT>& r)
 {
-    if constexpr (Fmt<FMT>::BITS == 4)
+    if constexpr (Fmt<FMT>::BITS != 3)
         load_groups<FMT, EDGE, 4>(codes, scales, row, nrows, gpr, g0, r.w, nullptr, r.sb);
     else
         load_groups<FMT, EDGE, 4>(codes, scales, row, nrows, gpr, g0, nullptr, r.h, r.sb);
@@ -240,6 +287,8 @@ __device__ __forceinline__ void decode_group(const uint32_t* w, const uint16_t* 
             out[i] = o0[i];
             out[4 + i] = o1[i];
         }
+    } else if constexpr (Fmt<FMT>::BITS == 6) {
+        decode_if6_group<FMT>(w + 3 * g, (sb >> (8 * g)) & 0xFFu, out);
     } else {
         const uint64_t bitsv = (uint64_t)h[3 * g] | ((uint64_t)h[3 * g + 1] << 16) |
                                ((uint64_t)h[3 * g + 2] << 32);
@@ -252,7 +301,7 @@ template <int FMT>
 __device__ __forceinline__ void decode_b(const RawB<FMT>& r, _Float16* stage, int t, int g)
 {
     uint32_t v[8];
-    if constexpr (Fmt<FMT>::BITS == 4)
+    if constexpr (Fmt<FMT>::BITS != 3)
         decode_group<FMT>(r.w, nullptr, r.sb, g, v);
     else
         decode_group<FMT>(nullptr, r.h, r.sb, g, v);
@@ -267,7 +316,7 @@ template <int FMT>
 __device__ __forceinline__ void decode_a(const RawA<FMT>& r, int gg, half8& f0, half8& f1)
 {
     uint32_t v[8];
-    if constexpr (Fmt<FMT>::BITS == 4)
+    if constexpr (Fmt<FMT>::BITS != 3)
         decode_group<FMT>(r.w, nullptr, r.sb, gg, v);
     else
         decode_group<FMT>(nullptr, r.h, r.sb, gg, v);
@@ -1048,6 +1097,8 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s)
         case IFQ_FMT_IF4: return launch_g<IFQ_FMT_IF4>(a, s);
         case IFQ_FMT_NVFP4: return launch_g<IFQ_FMT_NVFP4>(a, s);
         case IFQ_FMT_IF3: return launch_g<IFQ_FMT_IF3>(a, s);
+        case IFQ_FMT_IF6_E2M3: return launch_g<IFQ_FMT_IF6_E2M3>(a, s);
+        case IFQ_FMT_IF6_E3M2: return launch_g<IFQ_FMT_IF6_E3M2>(a, s);
         default: return hipErrorNotSupported;
     }
 }

@@ -8,7 +8,7 @@ import oracle as O
 from paper_2603_28765_amd import ops
 
 FORMATS = [ops.IF4, ops.NVFP4, ops.IF3, ops.IF6_E2M3, ops.IF6_E3M2]
-GEMM_FORMATS = [ops.IF4, ops.NVFP4, ops.IF3]
+GEMM_FORMATS = [ops.IF4, ops.NVFP4, ops.IF3, ops.IF6_E2M3, ops.IF6_E3M2]
 
 
 def require_gpu():

@@ -99,7 +99,8 @@ def test_gemm_validation(L):
     assert g(L, ts=None) == EINVAL
     assert g(L, dtype=5) == EINVAL
     assert g(L, a=P16 + 4) == EALIGN
-    assert g(L, fmt=3) == EUNSUPPORTED   # IF6 GEMM: not exact in FP16 operands
+    assert g(L, fmt=3, K=40) == ESHAPE    # IF6 GEMM is validated like the others
+    assert g(L, fmt=4, ldc=32) == ESHAPE
     assert g(L, fmt=7) == EINVAL
 
 

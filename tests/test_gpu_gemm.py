@@ -25,12 +25,30 @@ def _quantized_pair(fmt, a_cpu, b_cpu, flags=0, signs=0, seeds=(0, 0)):
     return pa, oa, pb, ob
 
 
+EXACT_OPERANDS = (ops.IF4, ops.NVFP4, ops.IF3)  # IF6 operands are rounded to FP16
+
+
 def _check(fmt, pa, oa, pb, ob, dtype=ops.F32, tag=""):
+    """fp32 out: relative Frobenius error vs the fp64 reference <= TOL.
+    bf16 out: no further from the fp64 reference than its own bf16 rounding
+    plus TOL; formats whose FP16 operands are exact must also match the bf16
+    rounding of the reference to TOL.  (IF6 operands carry up to 2^-12
+    relative rounding, which flips a share of bf16 outputs by one ulp.)"""
     c = ops.ifx_gemm(pa, pb, dtype).float().cpu().numpy()
     ref = O.gemm_ref(oa[0], oa[1], oa[2], ob[0], ob[1], ob[2], fmt)
-    target = ref if dtype == ops.F32 else bf16_round(ref)
-    err = rel_fro(c, target) if np.linalg.norm(ref) > 0 else np.abs(c).max()
-    assert err <= TOL, (tag, err)
+    if np.linalg.norm(ref) == 0:
+        err = np.abs(c).max()
+        assert err <= TOL, (tag, err)
+        return err
+    if dtype == ops.F32:
+        err = rel_fro(c, ref)
+        assert err <= TOL, (tag, err)
+        return err
+    err = rel_fro(c, ref)
+    assert err <= rel_fro(bf16_round(ref), ref) + TOL, (tag, err)
+    if fmt in EXACT_OPERANDS:
+        err = rel_fro(c, bf16_round(ref))
+        assert err <= TOL, (tag, err)
     return err
 
 
