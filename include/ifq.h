@@ -82,7 +82,11 @@ enum {
     IFQ_SR = 2u,           /* stochastic rounding of both candidates */
     IFQ_MARGIN_16_17 = 4u, /* scales computed against M_FP * 16/17 (Sec. 4.1) */
     IFQ_SCALE_IN = 8u,     /* *tensor_scale is an input instead of Eq. 1's output */
-    IFQ_AXIS_STRIDED = 16u /* groups run along rows; output describes X transposed */
+    IFQ_AXIS_STRIDED = 16u, /* groups run along rows; output describes X transposed */
+    IFQ_SR_RTN_TYPE = 32u   /* with IFQ_SR: decide FP or INT on the round-to-nearest
+                               candidates, then round stochastically in that type
+                               (the unbiased alternative of App. B); no effect
+                               without IFQ_SR */
 };
 
 /* ------------------------------------------------------------ quantize --

@@ -24,7 +24,7 @@ FORMATS = {"if4": FMT_IF4, "nvfp4": FMT_NVFP4, "if3": FMT_IF3,
            "if6_e2m3": FMT_IF6_E2M3, "if6_e3m2": FMT_IF6_E3M2}
 BITS = {FMT_IF4: 4, FMT_NVFP4: 4, FMT_IF3: 3, FMT_IF6_E2M3: 6, FMT_IF6_E3M2: 6}
 
-RHT, SR, MARGIN, SCALE_IN, STRIDED = 1, 2, 4, 8, 16
+RHT, SR, MARGIN, SCALE_IN, STRIDED, SR_RTN_TYPE = 1, 2, 4, 8, 16, 32
 GROUP = 16
 
 _lib = None

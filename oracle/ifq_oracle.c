@@ -39,7 +39,7 @@
 /* format ids: must match the numbering the tests use */
 enum { FMT_IF4 = 0, FMT_NVFP4 = 1, FMT_IF3 = 2, FMT_IF6_E2M3 = 3, FMT_IF6_E3M2 = 4, FMT_COUNT = 5 };
 /* flag bits */
-enum { F_RHT = 1, F_SR = 2, F_MARGIN = 4, F_SCALE_IN = 8, F_STRIDED = 16 };
+enum { F_RHT = 1, F_SR = 2, F_MARGIN = 4, F_SCALE_IN = 8, F_STRIDED = 16, F_SR_RTN_TYPE = 32 };
 
 #define GROUP 16
 
@@ -254,53 +254,15 @@ float oracle_tensor_scale(int fmt, float amax, uint32_t flags)
 
 /* ------------------------------------------------------ one group -- */
 
-/* Quantize one group of 16 values v (already transformed when the RHT is
- * on) under tensor scale alpha; Fig. 3a lines 1-10 with alpha restored
- * (Eq. 2 divides by alpha * M_FP).
- *   h      16-bit uniforms for stochastic rounding (ignored without F_SR)
- *   codes  out: 16 element codes (low `bits` bits used)
- *   scale  out: E4M3 code of Delta, bit 7 set when the group is INT
- *   e_fp, e_int  out: the two candidate errors (sum of squares, x-bar units)
- */
-void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t flags,
-                           const uint16_t h[GROUP], uint8_t codes[GROUP], uint8_t* scale,
-                           float* e_fp, float* e_int)
+/* The two candidates of one group (Fig. 3a lines 4-9) for scaled values
+ * xb: codes cf (FP) and ci (INT) and their squared errors, with
+ * round-to-nearest-even or, with sr, stochastic rounding by h. */
+static void candidates(const fmt_desc* f, const float xb[GROUP], int sr, const uint16_t h[GROUP],
+                       uint8_t cf[GROUP], uint8_t ci[GROUP], float* e_fp, float* e_int)
 {
-    ensure_init();
-    const fmt_desc* f = &g_fmt[fmt];
-    const int sr = (flags & F_SR) != 0;
     const int sign_bit = 1 << (f->bits - 1);
     const int code_mask = (1 << f->bits) - 1;
-
-    /* Fig. 3a line 1 / Eq. (2): Delta = max|X_g| / (alpha * M_FP). */
-    float amax_g = 0.0f;
-    for (int j = 0; j < GROUP; ++j) {
-        float a = fabsf(v[j]);
-        if (a > amax_g) amax_g = a;
-    }
-    float denom = alpha * scale_max(f, flags);
-    float delta_raw = amax_g / denom;
-    /* Fig. 3a line 2: cast to E4M3 (round to nearest even, saturating). */
-    int dcode = (denom > 0.0f) ? oracle_e4m3_encode(delta_raw) : 0;
-    float delta = (float)oracle_e4m3_value(dcode);
-
-    /* Scaled values x-bar = X / (alpha * Delta) (Fig. 3a line 3, alpha from
-     * Eq. 1), as a multiply by the rounded reciprocal.  A group whose
-     * combined scale is zero or below the smallest normal fp32 stores zeros. */
-    float s = alpha * delta;
-    if (!(s >= FLT_MIN)) {
-        memset(codes, 0, GROUP);
-        *scale = 0;
-        *e_fp = 0.0f;
-        *e_int = 0.0f;
-        return;
-    }
-    float inv = 1.0f / s;
-    float xb[GROUP];
-    for (int j = 0; j < GROUP; ++j) xb[j] = v[j] * inv;
-
     /* FP candidate (Fig. 3a lines 4-6). */
-    uint8_t cf[GROUP];
     float ef = 0.0f;
     for (int j = 0; j < GROUP; ++j) {
         double m = fabs((double)xb[j]);
@@ -329,7 +291,6 @@ void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t 
 
     /* INT candidate (Fig. 3a lines 7-9): int(x-bar * M_I/M_FP), clamped to
      * +-M_I, reconstructed as code * M_FP/M_I. */
-    uint8_t ci[GROUP];
     float ei = 0.0f;
     for (int j = 0; j < GROUP; ++j) {
         double r;
@@ -352,13 +313,72 @@ void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t 
         ei = fmaf(d, d, ei);
     }
 
-    /* Fig. 3a line 10: INT only if strictly better; Sec. 3: the choice is
-     * recorded in the scale's sign bit. */
-    int use_int = f->adaptive && (ei < ef);
-    memcpy(codes, use_int ? ci : cf, GROUP);
-    *scale = (uint8_t)(dcode | (use_int ? 0x80 : 0));
     *e_fp = ef;
     *e_int = ei;
+}
+
+/* Quantize one group of 16 values v (already transformed when the RHT is
+ * on) under tensor scale alpha; Fig. 3a lines 1-10 with alpha restored
+ * (Eq. 2 divides by alpha * M_FP).
+ *   h      16-bit uniforms for stochastic rounding (ignored without F_SR)
+ *   codes  out: 16 element codes (low `bits` bits used)
+ *   scale  out: E4M3 code of Delta, bit 7 set when the group is INT
+ *   e_fp, e_int  out: the two candidate errors (sum of squares, x-bar units)
+ */
+void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t flags,
+                           const uint16_t h[GROUP], uint8_t codes[GROUP], uint8_t* scale,
+                           float* e_fp, float* e_int)
+{
+    ensure_init();
+    const fmt_desc* f = &g_fmt[fmt];
+    const int sr = (flags & F_SR) != 0;
+
+    /* Fig. 3a line 1 / Eq. (2): Delta = max|X_g| / (alpha * M_FP). */
+    float amax_g = 0.0f;
+    for (int j = 0; j < GROUP; ++j) {
+        float a = fabsf(v[j]);
+        if (a > amax_g) amax_g = a;
+    }
+    float denom = alpha * scale_max(f, flags);
+    float delta_raw = amax_g / denom;
+    /* Fig. 3a line 2: cast to E4M3 (round to nearest even, saturating). */
+    int dcode = (denom > 0.0f) ? oracle_e4m3_encode(delta_raw) : 0;
+    float delta = (float)oracle_e4m3_value(dcode);
+
+    /* Scaled values x-bar = X / (alpha * Delta) (Fig. 3a line 3, alpha from
+     * Eq. 1), as a multiply by the rounded reciprocal.  A group whose
+     * combined scale is zero or below the smallest normal fp32 stores zeros. */
+    float s = alpha * delta;
+    if (!(s >= FLT_MIN)) {
+        memset(codes, 0, GROUP);
+        *scale = 0;
+        *e_fp = 0.0f;
+        *e_int = 0.0f;
+        return;
+    }
+    float inv = 1.0f / s;
+    float xb[GROUP];
+    for (int j = 0; j < GROUP; ++j) xb[j] = v[j] * inv;
+
+    uint8_t cf[GROUP], ci[GROUP];
+    float ef, ei;
+    candidates(f, xb, sr, h, cf, ci, &ef, &ei);
+    /* App. B variant: the type is decided on the round-to-nearest candidates
+     * (independent of the random draws), and the group is then rounded
+     * stochastically in that type. */
+    float sel_f = ef, sel_i = ei;
+    if (sr && (flags & F_SR_RTN_TYPE)) {
+        uint8_t rf[GROUP], ri[GROUP];
+        candidates(f, xb, 0, h, rf, ri, &sel_f, &sel_i);
+    }
+
+    /* Fig. 3a line 10: INT only if strictly better; Sec. 3: the choice is
+     * recorded in the scale's sign bit. */
+    int use_int = f->adaptive && (sel_i < sel_f);
+    memcpy(codes, use_int ? ci : cf, GROUP);
+    *scale = (uint8_t)(dcode | (use_int ? 0x80 : 0));
+    *e_fp = sel_f;
+    *e_int = sel_i;
 }
 
 /* Dense little-endian bit stream: code j of a group at bits [j*b, j*b+b). */

@@ -208,8 +208,10 @@ template <int FMT> __device__ __forceinline__ uint32_t fp_sr_index(float m, floa
 // (low bits of each byte) and returns the scale byte.  Fig. 3a: Delta, the FP
 // candidate, the INT candidate scaled by c_up, and INT iff its error is
 // strictly smaller.  Errors are sums of squares in x-bar units, accumulated
-// in element order with fused multiply-adds.
-template <int FMT, bool SR>
+// in element order with fused multiply-adds.  RTN_TYPE (with SR): the type is
+// decided on the round-to-nearest candidates' errors and the stored codes
+// are the stochastic candidate of that type (the App. B alternative).
+template <int FMT, bool SR, bool RTN_TYPE = false>
 __device__ __forceinline__ uint32_t quantize_group(const float (&v)[kGroup], float alpha,
                                                    float denom, const uint32_t (&w)[8],
                                                    uint32_t (&code)[kGroup])
@@ -229,10 +231,22 @@ __device__ __forceinline__ uint32_t quantize_group(const float (&v)[kGroup], flo
     float inv = 1.0f / s;
 
     float ef = 0.0f, ei = 0.0f;
+    float rf = 0.0f, ri = 0.0f;  // RTN errors (RTN_TYPE only)
     uint32_t cf[kGroup], ci[kGroup];
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) {
         float xb = v[j] * inv;
+        if constexpr (SR && RTN_TYPE && F::ADAPTIVE) {
+            const float m0 = fabsf(xb);
+            const uint32_t n0 = __float_as_uint(xb) >> 31;
+            const float q0 = __uint_as_float(__float_as_uint(fp_magnitude<FMT>(fp_rtn_index<FMT>(m0))) | (n0 << 31));
+            const float d0 = q0 - xb;
+            rf = __builtin_fmaf(d0, d0, rf);
+            const float xc = __builtin_amdgcn_fmed3f(xb, -F::FP_MAX, F::FP_MAX);
+            const float r0 = __builtin_fmaf(xc, D::C_UP, 12582912.0f) - 12582912.0f;
+            const float e0 = __builtin_fmaf(r0, D::K_DN, -xb);
+            ri = __builtin_fmaf(e0, e0, ri);
+        }
         float m = fabsf(xb);
         uint32_t neg = __float_as_uint(xb) >> 31;
         // FP candidate
@@ -265,7 +279,11 @@ __device__ __forceinline__ uint32_t quantize_group(const float (&v)[kGroup], flo
             ei = __builtin_fmaf(di, di, ei);
         }
     }
-    bool use_int = F::ADAPTIVE && (ei < ef);
+    bool use_int;
+    if constexpr (SR && RTN_TYPE)
+        use_int = F::ADAPTIVE && (ri < rf);
+    else
+        use_int = F::ADAPTIVE && (ei < ef);
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) code[j] = use_int ? ci[j] : cf[j];
     return dcode | (use_int ? 0x80u : 0u);

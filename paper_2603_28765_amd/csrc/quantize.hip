@@ -68,7 +68,7 @@ __device__ __forceinline__ float resolve_alpha(bool scale_in, float* tensor_scal
 template <int FMT, bool SR>
 __device__ __forceinline__ void quantize_store(const float (&v)[kGroup], float alpha, float denom,
                                                uint64_t seed, int64_t gi, uint8_t* __restrict__ codes,
-                                               uint8_t* __restrict__ scales)
+                                               uint8_t* __restrict__ scales, bool sr_rtn)
 {
     constexpr int BITS = Fmt<FMT>::BITS;
     if constexpr (BITS == 4 && !SR) {
@@ -80,7 +80,8 @@ __device__ __forceinline__ void quantize_store(const float (&v)[kGroup], float a
         uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
         if constexpr (SR) sr_words(seed, (uint64_t)gi, w);
         uint32_t c[kGroup];
-        const uint32_t sb = quantize_group<FMT, SR>(v, alpha, denom, w, c);
+        const uint32_t sb = (SR && sr_rtn) ? quantize_group<FMT, SR, true>(v, alpha, denom, w, c)
+                                           : quantize_group<FMT, SR, false>(v, alpha, denom, w, c);
         store_packed<BITS>(codes + gi * (2 * BITS), pack16<BITS>(c));
         scales[gi] = (uint8_t)sb;
     }
@@ -127,7 +128,7 @@ __global__ __launch_bounds__(kThreads) void tensor_max_rows(const uint16_t* __re
 template <int FMT, bool RHT, bool SR>
 __global__ __launch_bounds__(kThreads) void quantize_rows(
     const uint16_t* __restrict__ x, int64_t nrows, int64_t gpr, int64_t ld, uint32_t signs,
-    uint64_t seed, float scale_max, float denom_alpha, int scale_in,
+    uint64_t seed, int sr_rtn, float scale_max, float denom_alpha, int scale_in,
     const float* __restrict__ partials, int npartials, uint8_t* __restrict__ codes,
     uint8_t* __restrict__ scales, float* tensor_scale)
 {
@@ -142,7 +143,7 @@ __global__ __launch_bounds__(kThreads) void quantize_rows(
             load_group_rowwise(x + r * ld + gc * kGroup, v);
             if constexpr (RHT) rht16(v, signs);
             const int64_t gi = r * gpr + gc;
-            quantize_store<FMT, SR>(v, alpha, denom, seed, gi, codes, scales);
+            quantize_store<FMT, SR>(v, alpha, denom, seed, gi, codes, scales, sr_rtn != 0);
         }
     }
 }
@@ -209,7 +210,7 @@ __global__ __launch_bounds__(kThreads) void tensor_max_strided(const uint16_t* _
 template <int FMT, bool RHT, bool SR>
 __global__ __launch_bounds__(kThreads) void quantize_strided(
     const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t ld, int vec,
-    uint32_t signs, uint64_t seed, float scale_max, float denom_alpha, int scale_in,
+    uint32_t signs, uint64_t seed, int sr_rtn, float scale_max, float denom_alpha, int scale_in,
     const float* __restrict__ partials, int npartials, uint8_t* __restrict__ codes,
     uint8_t* __restrict__ scales, float* tensor_scale)
 {
@@ -232,7 +233,7 @@ __global__ __launch_bounds__(kThreads) void quantize_strided(
                     v[j] = __uint_as_float((uint32_t)tile[q * kGroup + j][c] << 16);
                 if constexpr (RHT) rht16(v, signs);
                 const int64_t gi = col * gpr + g;
-                quantize_store<FMT, SR>(v, alpha, denom, seed, gi, codes, scales);
+                quantize_store<FMT, SR>(v, alpha, denom, seed, gi, codes, scales, sr_rtn != 0);
             }
             __syncthreads();
         }
@@ -311,7 +312,7 @@ constexpr int kCodeRowBytes = kGrpTile * 8;
 template <int FMT, bool RHT, bool SR>
 __global__ __launch_bounds__(kThreads) void quantize_cols(
     const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t ld, uint32_t signs,
-    uint64_t seed, float scale_max, float denom_alpha, int scale_in,
+    uint64_t seed, int sr_rtn, float scale_max, float denom_alpha, int scale_in,
     const float* __restrict__ partials, int npartials, uint8_t* __restrict__ codes,
     uint8_t* __restrict__ scales, float* tensor_scale)
 {
@@ -347,7 +348,8 @@ __global__ __launch_bounds__(kThreads) void quantize_cols(
                     uint32_t w[8];
                     sr_words(seed, (uint64_t)gi, w);
                     uint32_t cq[kGroup];
-                    sb = quantize_group<FMT, true>(v, alpha, denom, w, cq);
+                    sb = sr_rtn ? quantize_group<FMT, true, true>(v, alpha, denom, w, cq)
+                                : quantize_group<FMT, true, false>(v, alpha, denom, w, cq);
                     const Packed<4> pp = pack16<4>(cq);
                     pk = make_uint2(pp.w[0], pp.w[1]);
                 }
@@ -418,11 +420,12 @@ static hipError_t launch_q(const QuantArgs& a, hipStream_t s, int npartials, flo
                            float denom_alpha)
 {
     const int scale_in = (a.flags & IFQ_SCALE_IN) ? 1 : 0;
+    const int sr_rtn = (a.flags & IFQ_SR_RTN_TYPE) ? 1 : 0;
     if constexpr (Fmt<FMT>::BITS == 4) {
         if ((a.flags & IFQ_AXIS_STRIDED) && strided_cols_ok<FMT>(a)) {
             dim3 grid((unsigned)cdiv(a.cols, kColTile), (unsigned)cdiv(a.rows / kGroup, kGrpTile));
             hipLaunchKernelGGL((quantize_cols<FMT, RHT, SR>), grid, dim3(kThreads), 0, s, a.x, a.rows,
-                               a.cols, a.ld, a.signs, a.seed, scale_max, denom_alpha, scale_in, a.partials,
+                               a.cols, a.ld, a.signs, a.seed, sr_rtn, scale_max, denom_alpha, scale_in, a.partials,
                                npartials, a.codes, a.scales, a.tensor_scale);
             return hipGetLastError();
         }
@@ -430,7 +433,7 @@ static hipError_t launch_q(const QuantArgs& a, hipStream_t s, int npartials, flo
     if (a.flags & IFQ_AXIS_STRIDED) {
         dim3 grid((unsigned)cdiv(a.cols, kTC), (unsigned)std::min<int64_t>(cdiv(a.rows, kTR), 65535));
         hipLaunchKernelGGL((quantize_strided<FMT, RHT, SR>), grid, dim3(kThreads), 0, s, a.x,
-                           a.rows, a.cols, a.ld, strided_vec_ok(a), a.signs, a.seed, scale_max, denom_alpha, scale_in,
+                           a.rows, a.cols, a.ld, strided_vec_ok(a), a.signs, a.seed, sr_rtn, scale_max, denom_alpha, scale_in,
                            a.partials, npartials, a.codes, a.scales, a.tensor_scale);
     } else {
         const bool flat = a.ld == a.cols;
@@ -439,7 +442,7 @@ static hipError_t launch_q(const QuantArgs& a, hipStream_t s, int npartials, flo
         const int64_t ld = flat ? 0 : a.ld;
         dim3 grid((unsigned)cdiv(gpr, kThreads), (unsigned)std::min<int64_t>(nrows, 65535));
         hipLaunchKernelGGL((quantize_rows<FMT, RHT, SR>), grid, dim3(kThreads), 0, s, a.x, nrows,
-                           gpr, ld, a.signs, a.seed, scale_max, denom_alpha, scale_in, a.partials,
+                           gpr, ld, a.signs, a.seed, sr_rtn, scale_max, denom_alpha, scale_in, a.partials,
                            npartials, a.codes, a.scales, a.tensor_scale);
     }
     return hipGetLastError();

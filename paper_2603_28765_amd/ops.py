@@ -22,7 +22,7 @@ IF4, NVFP4, IF3, IF6_E2M3, IF6_E3M2 = range(5)
 FORMAT_NAMES = {IF4: "if4", NVFP4: "nvfp4", IF3: "if3", IF6_E2M3: "if6_e2m3", IF6_E3M2: "if6_e3m2"}
 BITS = {IF4: 4, NVFP4: 4, IF3: 3, IF6_E2M3: 6, IF6_E3M2: 6}
 
-RHT, SR, MARGIN_16_17, SCALE_IN, AXIS_STRIDED = 1, 2, 4, 8, 16
+RHT, SR, MARGIN_16_17, SCALE_IN, AXIS_STRIDED, SR_RTN_TYPE = 1, 2, 4, 8, 16, 32
 F32, BF16 = 0, 1
 
 STATUS = {0: "ok", -1: "invalid argument", -2: "invalid shape", -3: "misaligned",

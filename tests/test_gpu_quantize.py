@@ -12,7 +12,8 @@ from tests.gpu_common import (FORMATS, assert_quant_equal, bits, gpu_quantize, r
 
 pytestmark = pytest.mark.gpu
 
-FLAG_SETS = [0, ops.RHT, ops.SR, ops.MARGIN_16_17, ops.RHT | ops.SR | ops.MARGIN_16_17]
+FLAG_SETS = [0, ops.RHT, ops.SR, ops.MARGIN_16_17, ops.RHT | ops.SR | ops.MARGIN_16_17,
+             ops.SR | ops.SR_RTN_TYPE, ops.RHT | ops.SR | ops.MARGIN_16_17 | ops.SR_RTN_TYPE]
 
 
 @pytest.fixture(scope="module", autouse=True)

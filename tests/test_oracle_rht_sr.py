@@ -121,6 +121,37 @@ def test_sr_if4_biases_large_values_up(oracle):
     assert m_if - m_nv > 4 * np.hypot(s_if, s_nv)
 
 
+def test_sr_rtn_type_is_unbiased(oracle):
+    """App. B's alternative: decide FP or INT on the round-to-nearest
+    candidates, then round stochastically in that type.  The type no longer
+    depends on the random draws (every trial keeps the RTN scale byte), the
+    group is unbiased element by element, and the upward bias of the largest
+    values that the default IF4-SR shows disappears."""
+    v = np.array([6.0, 0.3, 1.2, -2.7, 4.9, -3.3, 0.05, 5.5, -0.8, 2.2, 3.9, -1.6,
+                  0.7, -4.2, 1.9, 0.0], np.float32)
+    _, sb_rtn, _, _ = oracle.quantize_group(v, 1.0, oracle.FMT_IF4, oracle.SCALE_IN)
+    for t in range(50):
+        h = oracle.sr_bits(t, 0)
+        _, sb, _, _ = oracle.quantize_group(v, 1.0, oracle.FMT_IF4,
+                                            oracle.SCALE_IN | oracle.SR | oracle.SR_RTN_TYPE, h)
+        assert sb == sb_rtn
+    trials = 4000
+    deq = _sr_trials(oracle, oracle.FMT_IF4, v, trials, flags=oracle.SR_RTN_TYPE)
+    sem = np.maximum(deq.std(0), 1e-3) / np.sqrt(trials)
+    assert np.all(np.abs(deq.mean(0) - v) <= 5 * sem + 1e-4), (deq.mean(0) - v) / sem
+    m, s = _group_max_bias(oracle, oracle.FMT_IF4, oracle.MARGIN | oracle.SR_RTN_TYPE)
+    assert abs(m) < 3 * s + 1e-3, (m, s)
+
+
+def test_sr_rtn_type_without_sr_is_plain_rtn(oracle):
+    rng = np.random.default_rng(17)
+    for _ in range(200):
+        v = (rng.standard_t(3, 16) * rng.uniform(0.1, 10)).astype(np.float32)
+        a = oracle.quantize_group(v, 1.0, oracle.FMT_IF4, oracle.SCALE_IN)
+        b = oracle.quantize_group(v, 1.0, oracle.FMT_IF4, oracle.SCALE_IN | oracle.SR_RTN_TYPE)
+        assert np.array_equal(a[0], b[0]) and a[1] == b[1]
+
+
 def test_sr_bits_layout(oracle):
     seed, group = 0x0123456789ABCDEF, 77
     key = [seed & 0xFFFFFFFF, seed >> 32]
