@@ -1,4 +1,5 @@
-"""CPU oracle for the adaptive block-scaled formats (IF3, IF4, IF6, NVFP4).
+"""CPU oracle for the adaptive block-scaled formats (IF3, IF4, IF6) and the
+comparison formats NVFP4, NVINT4 and NVFP4 with 4/6.
 
 TEST INFRASTRUCTURE.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 ``cpu_baseline`` leg of ``bench.py`` may import this package.  The product
@@ -19,10 +20,13 @@ import numpy as np
 
 from . import build as _build
 
-FMT_IF4, FMT_NVFP4, FMT_IF3, FMT_IF6_E2M3, FMT_IF6_E3M2 = range(5)
+(FMT_IF4, FMT_NVFP4, FMT_IF3, FMT_IF6_E2M3, FMT_IF6_E3M2, FMT_NVINT4,
+ FMT_NVFP4_46) = range(7)
 FORMATS = {"if4": FMT_IF4, "nvfp4": FMT_NVFP4, "if3": FMT_IF3,
-           "if6_e2m3": FMT_IF6_E2M3, "if6_e3m2": FMT_IF6_E3M2}
-BITS = {FMT_IF4: 4, FMT_NVFP4: 4, FMT_IF3: 3, FMT_IF6_E2M3: 6, FMT_IF6_E3M2: 6}
+           "if6_e2m3": FMT_IF6_E2M3, "if6_e3m2": FMT_IF6_E3M2, "nvint4": FMT_NVINT4,
+           "nvfp4_46": FMT_NVFP4_46}
+BITS = {FMT_IF4: 4, FMT_NVFP4: 4, FMT_IF3: 3, FMT_IF6_E2M3: 6, FMT_IF6_E3M2: 6,
+        FMT_NVINT4: 4, FMT_NVFP4_46: 4}
 
 RHT, SR, MARGIN, SCALE_IN, STRIDED, SR_RTN_TYPE = 1, 2, 4, 8, 16, 32
 GROUP = 16
@@ -142,7 +146,8 @@ def rht16(x, signs: int) -> np.ndarray:
 # ------------------------------------------------------------ one group --
 
 def quantize_group(v, alpha: float, fmt: int = FMT_IF4, flags: int = 0, h=None):
-    """Returns (codes[16] uint8, scale byte, E_FP, E_INT) for one group."""
+    """Returns (codes[16] uint8, scale byte, E_FP, E_INT) for one group
+    (for 4/6: the errors of the scalings to 6 and to 4 in alpha units)."""
     vv = np.ascontiguousarray(np.asarray(v, dtype=np.float32))
     assert vv.shape == (GROUP,)
     hh = np.zeros(GROUP, dtype=np.uint16) if h is None else \

@@ -1,7 +1,8 @@
 /*
  * ifq_oracle.c -- plain, slow, scalar CPU oracle for the adaptive
  * block-scaled formats of "Adaptive Block-Scaled Data Types"
- * (IF3, IF4, IF6-E2M3, IF6-E3M2) and the NVFP4 comparison format.
+ * (IF3, IF4, IF6-E2M3, IF6-E3M2) and the comparison formats NVFP4,
+ * NVINT4 and NVFP4 with Four Over Six (4/6).
  *
  * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
  * call this file; only tests/, the smoke check and the CPU-baseline leg of
@@ -25,7 +26,10 @@
  *   the Fig. 3a worked example, brute force over tiny groups, the
  *   IF4 <= NVFP4 error invariant, Table 1 MSE values, exact round trips,
  *   RHT orthonormality, SR unbiasedness, and the Philox4x32-10 stream
- *   against an independent installed implementation.
+ *   against an independent installed implementation.  NVINT4 and 4/6:
+ *   Table 1 MSE and maxima, brute force in exact rationals (nearest codes,
+ *   nearest E4M3 scales, the smaller-error scaling), agreement with the
+ *   independent numpy implementation, round trips and the 4/6 tie rule.
  * The fp32 operation order itself (reciprocal-multiply scaling, the error
  * accumulation order) is not fixed by the paper: parity unpinned beyond the
  * self-consistency of oracle and kernels, as recorded in the design notes.
@@ -37,7 +41,23 @@
 #include <string.h>
 
 /* format ids: must match the numbering the tests use */
-enum { FMT_IF4 = 0, FMT_NVFP4 = 1, FMT_IF3 = 2, FMT_IF6_E2M3 = 3, FMT_IF6_E3M2 = 4, FMT_COUNT = 5 };
+enum {
+    FMT_IF4 = 0,
+    FMT_NVFP4 = 1,
+    FMT_IF3 = 2,
+    FMT_IF6_E2M3 = 3,
+    FMT_IF6_E3M2 = 4,
+    FMT_NVINT4 = 5,
+    FMT_NVFP4_46 = 6,
+    FMT_COUNT = 7
+};
+/* element-type rule of a format */
+enum {
+    KIND_FP = 0,        /* FP elements only (NVFP4) */
+    KIND_ADAPTIVE = 1,  /* per-group FP or INT by squared error (IF formats) */
+    KIND_INT = 2,       /* INT elements only (NVINT4) */
+    KIND_FOUR_SIX = 3   /* FP elements, group scaled to a maximum of 6 or 4 (4/6) */
+};
 /* flag bits */
 enum { F_RHT = 1, F_SR = 2, F_MARGIN = 4, F_SCALE_IN = 8, F_STRIDED = 16, F_SR_RTN_TYPE = 32 };
 
@@ -46,7 +66,10 @@ enum { F_RHT = 1, F_SR = 2, F_MARGIN = 4, F_SCALE_IN = 8, F_STRIDED = 16, F_SR_R
 typedef struct {
     int bits;          /* bits per stored code */
     int ebits, mbits;  /* FP element: exponent and mantissa field widths */
-    int adaptive;      /* 1: per-group FP/INT choice (IF formats); 0: FP only */
+    int kind;          /* KIND_* */
+    int adaptive;      /* kind == KIND_ADAPTIVE */
+    float m_scale;     /* M of Eq. 1-2: the element maximum a group is scaled to */
+    float alpha_fp8;   /* the E4M3 factor of Eq. 1: 448, or 256 for 4/6 */
     int n_mag;         /* number of non-negative FP codes = 2^(bits-1) */
     double mag[32];    /* FP magnitude of each non-negative code (exact) */
     float fp_max;      /* M_FP: largest FP magnitude */
@@ -69,12 +92,13 @@ static double exmy_value(int ebits, int mbits, int code)
     return ldexp((double)((1 << mbits) + M), E - bias - mbits);
 }
 
-static void init_fmt(fmt_desc* f, int bits, int ebits, int mbits, int adaptive)
+static void init_fmt(fmt_desc* f, int bits, int ebits, int mbits, int kind)
 {
     f->bits = bits;
     f->ebits = ebits;
     f->mbits = mbits;
-    f->adaptive = adaptive;
+    f->kind = kind;
+    f->adaptive = kind == KIND_ADAPTIVE;
     f->n_mag = 1 << (bits - 1);
     for (int i = 0; i < f->n_mag; ++i) f->mag[i] = exmy_value(ebits, mbits, i);
     f->fp_max = (float)f->mag[f->n_mag - 1];
@@ -84,16 +108,31 @@ static void init_fmt(fmt_desc* f, int bits, int ebits, int mbits, int adaptive)
      * types span [0, M_FP * Delta].  Each ratio is rounded once to fp32. */
     f->c_up = (float)f->int_max / f->fp_max;
     f->k_dn = f->fp_max / (float)f->int_max;
+    f->m_scale = f->fp_max;
+    f->alpha_fp8 = 448.0f;
+    if (kind == KIND_INT) {
+        /* NVINT4 (Sec. 2, Table 1): INT4 elements scaled straight to
+         * M_I = 7, so neither range factor applies; max value 7 x 448. */
+        f->m_scale = (float)f->int_max;
+        f->c_up = 1.0f;
+        f->k_dn = 1.0f;
+    } else if (kind == KIND_FOUR_SIX) {
+        /* 4/6 (Sec. 3 and Table 1): the tensor scale uses 6 x 256 so that
+         * the group with the tensor maximum can still be scaled to 4. */
+        f->alpha_fp8 = 256.0f;
+    }
 }
 
 static void ensure_init(void)
 {
     if (g_init) return;
-    init_fmt(&g_fmt[FMT_IF4], 4, 2, 1, 1);       /* E2M1 / INT4, Sec. 3 */
-    init_fmt(&g_fmt[FMT_NVFP4], 4, 2, 1, 0);     /* E2M1 only, Fig. 3a lines 1-4 */
-    init_fmt(&g_fmt[FMT_IF3], 3, 2, 0, 1);       /* E2M0 / INT3, Sec. 5.1 */
-    init_fmt(&g_fmt[FMT_IF6_E2M3], 6, 2, 3, 1);  /* E2M3 / INT6, Table 6 */
-    init_fmt(&g_fmt[FMT_IF6_E3M2], 6, 3, 2, 1);  /* E3M2 / INT6, Table 6 */
+    init_fmt(&g_fmt[FMT_IF4], 4, 2, 1, KIND_ADAPTIVE);       /* E2M1 / INT4, Sec. 3 */
+    init_fmt(&g_fmt[FMT_NVFP4], 4, 2, 1, KIND_FP);           /* E2M1 only, Fig. 3a lines 1-4 */
+    init_fmt(&g_fmt[FMT_IF3], 3, 2, 0, KIND_ADAPTIVE);       /* E2M0 / INT3, Sec. 5.1 */
+    init_fmt(&g_fmt[FMT_IF6_E2M3], 6, 2, 3, KIND_ADAPTIVE);  /* E2M3 / INT6, Table 6 */
+    init_fmt(&g_fmt[FMT_IF6_E3M2], 6, 3, 2, KIND_ADAPTIVE);  /* E3M2 / INT6, Table 6 */
+    init_fmt(&g_fmt[FMT_NVINT4], 4, 2, 1, KIND_INT);         /* INT4 only, Sec. 2 */
+    init_fmt(&g_fmt[FMT_NVFP4_46], 4, 2, 1, KIND_FOUR_SIX);  /* E2M1, max 6 or 4, Sec. 3 */
     g_init = 1;
 }
 
@@ -237,18 +276,22 @@ void oracle_rht16(const float x[GROUP], uint32_t signs, float v[GROUP])
 
 /* ------------------------------------------------------ scale factors -- */
 
-/* M_FP, or M_FP * 16/17 when the gradient margin of Sec. 4.1 is on. */
-static float scale_max(const fmt_desc* f, uint32_t flags)
+/* A group target m (M_FP, M_I for NVINT4, 6 or 4 for 4/6), or m * 16/17
+ * when the gradient margin of Sec. 4.1 is on. */
+static float with_margin(float m, uint32_t flags)
 {
-    if (flags & F_MARGIN) return (float)((double)f->fp_max * 16.0 / 17.0);
-    return f->fp_max;
+    if (flags & F_MARGIN) return (float)((double)m * 16.0 / 17.0);
+    return m;
 }
 
-/* Eq. (1): alpha = max|X| / (M_FP * M_FP8), M_FP8 = 448. */
+static float scale_max(const fmt_desc* f, uint32_t flags) { return with_margin(f->m_scale, flags); }
+
+/* Eq. (1): alpha = max|X| / (M * M_FP8) with M_FP8 = 448 (256 for 4/6). */
 float oracle_tensor_scale(int fmt, float amax, uint32_t flags)
 {
     ensure_init();
-    float denom = scale_max(&g_fmt[fmt], flags) * 448.0f;
+    const fmt_desc* f = &g_fmt[fmt];
+    float denom = scale_max(f, flags) * f->alpha_fp8;
     return amax / denom;
 }
 
@@ -325,6 +368,66 @@ static void candidates(const fmt_desc* f, const float xb[GROUP], int sr, const u
  *   scale  out: E4M3 code of Delta, bit 7 set when the group is INT
  *   e_fp, e_int  out: the two candidate errors (sum of squares, x-bar units)
  */
+/* 4/6 (Sec. 3, following Four Over Six): the group is scaled twice, to a
+ * maximum of 6 and to a maximum of 4 (Eq. 2 with M = 6 or 4), rounded onto
+ * E2M1 each time, and the scaling whose dequantized values have the smaller
+ * squared error is kept (ties keep 6).  With x-bar_t = X / (alpha Delta_t) the
+ * squared error of scaling t divided by alpha^2 is
+ * Delta_t^2 * sum_j (q_j - x-bar_j)^2; that product, rounded to fp32, is
+ * what is compared.  Delta_4 >= Delta_6, so a scaling to 4 whose combined
+ * scale is below FLT_MIN leaves none: the group stores zeros; when only the
+ * scaling to 6 falls below FLT_MIN, 4 is kept.  With SR both scalings round
+ * stochastically with the same draws; with F_SR_RTN_TYPE the comparison uses
+ * their round-to-nearest candidates instead. */
+static void four_six_group(const fmt_desc* f, const float v[GROUP], float alpha, uint32_t flags,
+                           const uint16_t h[GROUP], uint8_t codes[GROUP], uint8_t* scale,
+                           float* e6, float* e4)
+{
+    const int sr = (flags & F_SR) != 0;
+    float amax_g = 0.0f;
+    for (int j = 0; j < GROUP; ++j) {
+        float a = fabsf(v[j]);
+        if (a > amax_g) amax_g = a;
+    }
+    const float target[2] = {scale_max(f, flags), with_margin(4.0f, flags)};
+    uint8_t cand[2][GROUP];
+    int dcode[2];
+    float err[2] = {0.0f, 0.0f};
+    int ok[2];
+    for (int t = 0; t < 2; ++t) {
+        float denom = alpha * target[t];
+        dcode[t] = (denom > 0.0f) ? oracle_e4m3_encode(amax_g / denom) : 0;
+        float delta = (float)oracle_e4m3_value(dcode[t]);
+        float s = alpha * delta;
+        ok[t] = s >= FLT_MIN;
+        if (!ok[t]) continue;
+        float inv = 1.0f / s;
+        float xb[GROUP];
+        for (int j = 0; j < GROUP; ++j) xb[j] = v[j] * inv;
+        uint8_t ci[GROUP];
+        float ef, ei;
+        candidates(f, xb, sr, h, cand[t], ci, &ef, &ei);
+        if (sr && (flags & F_SR_RTN_TYPE)) {
+            uint8_t rf[GROUP];
+            candidates(f, xb, 0, h, rf, ci, &ef, &ei);
+        }
+        err[t] = (delta * delta) * ef;
+    }
+    *e6 = err[0];
+    *e4 = err[1];
+    if (!ok[1]) {
+        memset(codes, 0, GROUP);
+        *scale = 0;
+        return;
+    }
+    int pick = (ok[0] && !(err[1] < err[0])) ? 0 : 1;
+    memcpy(codes, cand[pick], GROUP);
+    *scale = (uint8_t)dcode[pick];
+}
+
+/* One group.  IF formats and NVFP4: Fig. 3a.  NVINT4: the INT candidate
+ * alone, scaled to M_I (c_up = 1).  4/6: four_six_group, which reports the
+ * two scalings' errors in e_fp (to 6) and e_int (to 4). */
 void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t flags,
                            const uint16_t h[GROUP], uint8_t codes[GROUP], uint8_t* scale,
                            float* e_fp, float* e_int)
@@ -332,8 +435,12 @@ void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t 
     ensure_init();
     const fmt_desc* f = &g_fmt[fmt];
     const int sr = (flags & F_SR) != 0;
+    if (f->kind == KIND_FOUR_SIX) {
+        four_six_group(f, v, alpha, flags, h, codes, scale, e_fp, e_int);
+        return;
+    }
 
-    /* Fig. 3a line 1 / Eq. (2): Delta = max|X_g| / (alpha * M_FP). */
+    /* Fig. 3a line 1 / Eq. (2): Delta = max|X_g| / (alpha * M). */
     float amax_g = 0.0f;
     for (int j = 0; j < GROUP; ++j) {
         float a = fabsf(v[j]);
@@ -373,10 +480,16 @@ void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t 
     }
 
     /* Fig. 3a line 10: INT only if strictly better; Sec. 3: the choice is
-     * recorded in the scale's sign bit. */
+     * recorded in the scale's sign bit.  NVINT4 always stores INT codes and
+     * its scale is a plain E4M3 value (bit 7 clear). */
     int use_int = f->adaptive && (sel_i < sel_f);
-    memcpy(codes, use_int ? ci : cf, GROUP);
-    *scale = (uint8_t)(dcode | (use_int ? 0x80 : 0));
+    if (f->kind == KIND_INT) {
+        memcpy(codes, ci, GROUP);
+        *scale = (uint8_t)dcode;
+    } else {
+        memcpy(codes, use_int ? ci : cf, GROUP);
+        *scale = (uint8_t)(dcode | (use_int ? 0x80 : 0));
+    }
     *e_fp = sel_f;
     *e_int = sel_i;
 }
@@ -500,12 +613,13 @@ int oracle_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int6
 }
 
 /* Dequantized value of one element (Fig. 3a lines 5 and 8 with alpha):
- * q * Delta, times M_FP/M_I for INT groups, times alpha, each step an fp32
+ * q * Delta, times M_FP/M_I for INT groups of the IF formats (1 for
+ * NVINT4), times alpha, each step an fp32
  * multiply in that order (q * Delta is exact). */
 static float dequant_element(const fmt_desc* f, uint8_t code, uint8_t sbyte, float alpha)
 {
     float delta = (float)oracle_e4m3_value(sbyte & 0x7F);
-    int is_int = f->adaptive && (sbyte & 0x80);
+    int is_int = f->kind == KIND_INT || (f->adaptive && (sbyte & 0x80));
     float q;
     if (is_int) {
         int c = code;
@@ -554,14 +668,14 @@ int oracle_dequantize_f64(int fmt, const uint8_t* codes, const uint8_t* scales, 
     const fmt_desc* f = &g_fmt[fmt];
     const int64_t gpr = cols / GROUP;
     const int64_t code_bytes_row = cols * f->bits / 8;
-    const double kdn = (double)f->fp_max / (double)f->int_max;
+    const double kdn = f->kind == KIND_INT ? 1.0 : (double)f->fp_max / (double)f->int_max;
     for (int64_t r = 0; r < rows; ++r) {
         for (int64_t g = 0; g < gpr; ++g) {
             uint8_t cg[GROUP];
             unpack_group(f->bits, codes + r * code_bytes_row + g * 2 * f->bits, cg);
             uint8_t sb = scales[r * gpr + g];
             double delta = oracle_e4m3_value(sb & 0x7F);
-            int is_int = f->adaptive && (sb & 0x80);
+            int is_int = f->kind == KIND_INT || (f->adaptive && (sb & 0x80));
             for (int j = 0; j < GROUP; ++j) {
                 double q;
                 if (is_int) {
