@@ -40,7 +40,8 @@ def parse():
     p.add_argument("--traffic-from", metavar="DIR",
                    help="read rocprofv3 FETCH_SIZE/WRITE_SIZE counter CSVs of a --mode step run "
                         "(DIR/pmc_FETCH_SIZE, DIR/pmc_WRITE_SIZE) and write profiles/hbm_traffic.json")
-    p.add_argument("--format", choices=["if4", "nvfp4"], default="if4",
+    p.add_argument("--format", choices=["if4", "nvfp4", "if3", "if6_e2m3", "if6_e3m2", "nvint4",
+                                        "nvfp4_46"], default="if4",
                    help="format of the --mode step run")
     p.add_argument("--small", action="store_true", help="1/8-size shapes (quick checks)")
     p.add_argument("--mode", choices=["full", "step", "copy"], default="full",
@@ -90,14 +91,12 @@ def main():
     Y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
 
     def run(fmt, pa, pw, ev=None):
-        q = ops.if4_quantize if fmt == ops.IF4 else ops.nvfp4_quantize
-        g = ops.if4_gemm if fmt == ops.IF4 else ops.nvfp4_gemm
         if ev: ev[0].record()
-        q(A, out=pa, workspace=ws)
+        ops.ifx_quantize(fmt, A, out=pa, workspace=ws)
         if ev: ev[1].record()
-        q(W, out=pw, workspace=ws)
+        ops.ifx_quantize(fmt, W, out=pw, workspace=ws)
         if ev: ev[2].record()
-        g(pa, pw, ops.BF16, Y)
+        ops.ifx_gemm(pa, pw, ops.BF16, Y)
         if ev: ev[3].record()
 
     def timed(fmt, steps, warmup):
@@ -138,10 +137,11 @@ def main():
         return float(np.mean(times))
 
     if args.mode == "step":
-        fmt = ops.IF4 if args.format == "if4" else ops.NVFP4
+        fmt = {v: k for k, v in ops.FORMAT_NAMES.items()}[args.format]
         r = timed(fmt, args.steps, args.warmup)
         print(json.dumps({"mode": "step", "format": args.format, "ms_per_step": r["step_s"] * 1e3,
-                          "gemm_us": r["gemm_s"] * 1e6}))
+                          "gemm_us": r["gemm_s"] * 1e6, "quant_A_us": r["quant_A_s"] * 1e6,
+                          "quant_W_us": r["quant_W_s"] * 1e6}))
         return
     res = timed(ops.IF4, args.steps, args.warmup)
     res_nv = timed(ops.NVFP4, max(5, args.steps // 2), 2)

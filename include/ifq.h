@@ -1,8 +1,8 @@
 /*
  * ifq.h -- C ABI of the IF4 quantized-linear hot path on AMD Instinct
  * MI355X (gfx950): the adaptive block-scaled quantizer and the block-scaled
- * GEMM of "Adaptive Block-Scaled Data Types", with NVFP4, IF3 and IF6
- * variants for comparison.
+ * GEMM of "Adaptive Block-Scaled Data Types", with NVFP4, IF3, IF6, NVINT4
+ * and NVFP4-with-4/6 variants for comparison.
  *
  * Format (Sec. 3).  A tensor X is stored as
  *   - one FP32 tensor scale  alpha = max|X| / (M_FP * 448)           (Eq. 1)
@@ -25,6 +25,16 @@
  *   IF3         3     E2M0           4      INT3   3     (Sec. 5.1, Table 6)
  *   IF6_E2M3    6     E2M3           7.5    INT6   31    (Sec. 5.1, Table 6)
  *   IF6_E3M2    6     E3M2           28     INT6   31    (Sec. 5.1, Table 6)
+ *   NVINT4      4     --             --     INT4   7     (INT only, Sec. 2)
+ *   NVFP4_46    4     E2M1           6      --     --    (FP only, 4/6, Sec. 3)
+ *
+ * NVINT4 groups are scaled straight to M_I = 7 (Delta = max|X_g| / (alpha * 7),
+ * alpha = max|X| / (7 * 448), Table 1), decode as q * Delta * alpha, and keep
+ * bit 7 of the scale clear.  NVFP4_46 (Four Over Six) computes alpha =
+ * max|X| / (6 * 256) (Table 1), scales each group both to a maximum of 6 and
+ * to a maximum of 4, rounds onto E2M1 each time and keeps the scaling whose
+ * dequantized group has the smaller squared error (ties keep 6); the stored
+ * data then decode exactly like NVFP4.
  *
  * Layouts (row-major, no padding):
  *   codes   uint8 [R, K * bits / 8]      scales  uint8 [R, K / 16]
@@ -71,7 +81,9 @@ typedef enum ifq_format {
     IFQ_FMT_NVFP4 = 1,
     IFQ_FMT_IF3 = 2,
     IFQ_FMT_IF6_E2M3 = 3,
-    IFQ_FMT_IF6_E3M2 = 4
+    IFQ_FMT_IF6_E3M2 = 4,
+    IFQ_FMT_NVINT4 = 5,
+    IFQ_FMT_NVFP4_46 = 6
 } ifq_format;
 
 typedef enum ifq_dtype { IFQ_F32 = 0, IFQ_BF16 = 1 } ifq_dtype;
@@ -80,13 +92,15 @@ typedef enum ifq_dtype { IFQ_F32 = 0, IFQ_BF16 = 1 } ifq_dtype;
 enum {
     IFQ_RHT = 1u,          /* 16-point random Hadamard transform of each group first */
     IFQ_SR = 2u,           /* stochastic rounding of both candidates */
-    IFQ_MARGIN_16_17 = 4u, /* scales computed against M_FP * 16/17 (Sec. 4.1) */
+    IFQ_MARGIN_16_17 = 4u, /* scales computed against M * 16/17 (Sec. 4.1); for
+                              NVFP4_46 both targets, 6 and 4, take the factor */
     IFQ_SCALE_IN = 8u,     /* *tensor_scale is an input instead of Eq. 1's output */
     IFQ_AXIS_STRIDED = 16u, /* groups run along rows; output describes X transposed */
-    IFQ_SR_RTN_TYPE = 32u   /* with IFQ_SR: decide FP or INT on the round-to-nearest
+    IFQ_SR_RTN_TYPE = 32u   /* with IFQ_SR: decide FP or INT (for NVFP4_46: the
+                               scaling to 6 or 4) on the round-to-nearest
                                candidates, then round stochastically in that type
                                (the unbiased alternative of App. B); no effect
-                               without IFQ_SR */
+                               without IFQ_SR or for NVFP4 and NVINT4 */
 };
 
 /* ------------------------------------------------------------ quantize --
@@ -118,7 +132,9 @@ enum {
  *   tensor_scale  (device) one float: written with alpha, or read when
  *                 IFQ_SCALE_IN is set.  A group whose alpha * Delta is zero or
  *                 below FLT_MIN (this includes alpha = 0 and an all-zero
- *                 tensor) is stored as scale 0 and codes 0.
+ *                 tensor) is stored as scale 0 and codes 0; for NVFP4_46 that
+ *                 is decided on the scaling to 4 (the larger Delta), and a
+ *                 scaling to 6 below FLT_MIN leaves the scaling to 4.
  *   workspace     (device) at least ifq_quantize_workspace_bytes() bytes,
  *                 256-byte aligned, no initial contents required; may be
  *                 NULL when that size is 0.
@@ -132,7 +148,8 @@ int nvfp4_quantize(const void* x, int64_t rows, int64_t cols, int64_t ld_x, uint
                    uint32_t rht_signs, uint64_t seed, uint8_t* codes, uint8_t* scales,
                    float* tensor_scale, void* workspace, size_t workspace_bytes, void* stream);
 
-/* Any format (IF3 and IF6 of Sec. 5.1 included); same arguments. */
+/* Any format (IF3 and IF6 of Sec. 5.1, NVINT4 and NVFP4_46 included); same
+ * arguments. */
 int ifx_quantize(int format, const void* x, int64_t rows, int64_t cols, int64_t ld_x,
                  uint32_t flags, uint32_t rht_signs, uint64_t seed, uint8_t* codes,
                  uint8_t* scales, float* tensor_scale, void* workspace, size_t workspace_bytes,
@@ -142,8 +159,8 @@ int ifx_quantize(int format, const void* x, int64_t rows, int64_t cols, int64_t 
 size_t ifq_quantize_workspace_bytes(int format, int64_t rows, int64_t cols, uint32_t flags);
 
 /* ---------------------------------------------------------- dequantize --
- * out[r, k] = q * Delta * (M_FP/M_I if INT) * alpha, evaluated as three fp32
- * multiplies in that order (Fig. 3a lines 5 and 8 with alpha restored); the
+ * out[r, k] = q * Delta * (M_FP/M_I if INT) * alpha (the factor is 1 for
+ * NVINT4), evaluated as three fp32 multiplies in that order (Fig. 3a lines 5 and 8 with alpha restored); the
  * bf16 output is the round-to-nearest-even of that fp32 value.
  *   codes, scales  (device) packed [R, K] as written by the quantizer
  *   tensor_scale   (device) alpha
@@ -168,7 +185,8 @@ int ifx_dequantize(int format, const uint8_t* codes, const uint8_t* scales,
  * that carries its group scale exactly (7 q Delta for FP groups, 6 q Delta
  * for INT groups), so one FP32 accumulation over all of K applies every
  * block's scale pair and range alignment; alpha_A * alpha_B / 49 is applied
- * once at the end.  NVFP4 and IF3 operands are exact the same way; IF6
+ * once at the end.  NVFP4, NVFP4_46, NVINT4 (q Delta / 4) and IF3 operands
+ * are exact the same way; IF6
  * operands (62 q Delta and 15 q Delta for E2M3, 31 q Delta and 28 q Delta
  * for E3M2, Sec. 5.1 ratios) need up to 13 significant bits and are rounded
  * once to FP16 (relative error at most 2^-12 per operand).

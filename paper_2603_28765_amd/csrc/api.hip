@@ -11,7 +11,7 @@ constexpr uint32_t kKnownFlags =
     IFQ_RHT | IFQ_SR | IFQ_MARGIN_16_17 | IFQ_SCALE_IN | IFQ_AXIS_STRIDED | IFQ_SR_RTN_TYPE;
 constexpr int64_t kMaxElems = int64_t(1) << 40;  // keeps every index product in int64
 
-bool valid_format(int f) { return f >= IFQ_FMT_IF4 && f <= IFQ_FMT_IF6_E3M2; }
+bool valid_format(int f) { return f >= IFQ_FMT_IF4 && f <= IFQ_FMT_NVFP4_46; }
 
 int bits_of(int f)
 {

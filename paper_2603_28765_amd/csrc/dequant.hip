@@ -23,7 +23,7 @@ __global__ __launch_bounds__(kDqThreads) void dequantize_groups(const uint8_t* _
         load_unpack16<F::BITS>(codes + g * (2 * F::BITS), c);
         const uint32_t sb = scales[g];
         const float delta = e4m3_value(sb);
-        const bool is_int = F::ADAPTIVE && (sb & 0x80u);
+        const bool is_int = F::KIND == kKindInt || (F::ADAPTIVE && (sb & 0x80u));
         float o[kGroup];
 #pragma unroll
         for (int j = 0; j < kGroup; ++j) {
@@ -80,7 +80,11 @@ hipError_t launch_dequantize(int fmt, const uint8_t* codes, const uint8_t* scale
         case IFQ_FMT_NVFP4: return launch_dq<IFQ_FMT_NVFP4>(codes, scales, ts, ngroups, out, bf16, s);
         case IFQ_FMT_IF3: return launch_dq<IFQ_FMT_IF3>(codes, scales, ts, ngroups, out, bf16, s);
         case IFQ_FMT_IF6_E2M3: return launch_dq<IFQ_FMT_IF6_E2M3>(codes, scales, ts, ngroups, out, bf16, s);
-        default: return launch_dq<IFQ_FMT_IF6_E3M2>(codes, scales, ts, ngroups, out, bf16, s);
+        case IFQ_FMT_IF6_E3M2: return launch_dq<IFQ_FMT_IF6_E3M2>(codes, scales, ts, ngroups, out, bf16, s);
+        case IFQ_FMT_NVINT4: return launch_dq<IFQ_FMT_NVINT4>(codes, scales, ts, ngroups, out, bf16, s);
+        // 4/6 data decode exactly like NVFP4
+        case IFQ_FMT_NVFP4_46: return launch_dq<IFQ_FMT_NVFP4>(codes, scales, ts, ngroups, out, bf16, s);
+        default: return hipErrorInvalidValue;
     }
 }
 

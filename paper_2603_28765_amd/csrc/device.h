@@ -20,44 +20,68 @@ constexpr int kGroup = 16;
 // ------------------------------------------------------------ format traits
 // EB/MB: exponent and mantissa widths of the FP element (ExMy, bias
 // 2^(EB-1)-1, subnormals, no Inf/NaN).  INT elements are two's complement
-// in [-IMAX, IMAX].  c_up = fp32(IMAX / FP_MAX), k_dn =
+// in [-IMAX, IMAX].  KIND says how a group's element type is chosen:
+// FP only (NVFP4), adaptive FP/INT by squared error (IF formats, Fig. 3a),
+// INT only (NVINT4, Sec. 2) or FP scaled to a maximum of 6 or 4 (4/6,
+// Sec. 3).  M is the group target of Eq. 2 and A8 the E4M3 factor of Eq. 1
+// (alpha = max|X| / (M * A8)).  c_up = fp32(IMAX / FP_MAX), k_dn =
 // fp32(FP_MAX / IMAX) realise the 6/7 method (Sec. 3) and its IF3/IF6
-// analogues (Sec. 5.1 footnote).
+// analogues (Sec. 5.1 footnote); NVINT4 scales straight to IMAX (both 1).
+enum FmtKind { kKindFP = 0, kKindAdaptive = 1, kKindInt = 2, kKindFourSix = 3 };
+
 template <int FMT> struct Fmt;
 template <> struct Fmt<IFQ_FMT_IF4> {
-    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7;
+    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7, KIND = kKindAdaptive;
     static constexpr bool ADAPTIVE = true;
-    static constexpr float FP_MAX = 6.0f;
+    static constexpr float FP_MAX = 6.0f, M = 6.0f, A8 = 448.0f;
 };
 template <> struct Fmt<IFQ_FMT_NVFP4> {
-    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7;
+    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7, KIND = kKindFP;
     static constexpr bool ADAPTIVE = false;
-    static constexpr float FP_MAX = 6.0f;
+    static constexpr float FP_MAX = 6.0f, M = 6.0f, A8 = 448.0f;
 };
 template <> struct Fmt<IFQ_FMT_IF3> {
-    static constexpr int BITS = 3, EB = 2, MB = 0, IMAX = 3;
+    static constexpr int BITS = 3, EB = 2, MB = 0, IMAX = 3, KIND = kKindAdaptive;
     static constexpr bool ADAPTIVE = true;
-    static constexpr float FP_MAX = 4.0f;
+    static constexpr float FP_MAX = 4.0f, M = 4.0f, A8 = 448.0f;
 };
 template <> struct Fmt<IFQ_FMT_IF6_E2M3> {
-    static constexpr int BITS = 6, EB = 2, MB = 3, IMAX = 31;
+    static constexpr int BITS = 6, EB = 2, MB = 3, IMAX = 31, KIND = kKindAdaptive;
     static constexpr bool ADAPTIVE = true;
-    static constexpr float FP_MAX = 7.5f;
+    static constexpr float FP_MAX = 7.5f, M = 7.5f, A8 = 448.0f;
 };
 template <> struct Fmt<IFQ_FMT_IF6_E3M2> {
-    static constexpr int BITS = 6, EB = 3, MB = 2, IMAX = 31;
+    static constexpr int BITS = 6, EB = 3, MB = 2, IMAX = 31, KIND = kKindAdaptive;
     static constexpr bool ADAPTIVE = true;
-    static constexpr float FP_MAX = 28.0f;
+    static constexpr float FP_MAX = 28.0f, M = 28.0f, A8 = 448.0f;
+};
+template <> struct Fmt<IFQ_FMT_NVINT4> {
+    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7, KIND = kKindInt;
+    static constexpr bool ADAPTIVE = false;
+    static constexpr float FP_MAX = 6.0f, M = 7.0f, A8 = 448.0f;
+};
+template <> struct Fmt<IFQ_FMT_NVFP4_46> {
+    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7, KIND = kKindFourSix;
+    static constexpr bool ADAPTIVE = false;
+    static constexpr float FP_MAX = 6.0f, M = 6.0f, A8 = 256.0f;
 };
 
 template <int FMT> struct FmtDerived {
     using F = Fmt<FMT>;
     static constexpr int BIAS = (1 << (F::EB - 1)) - 1;
-    static constexpr float C_UP = (float)F::IMAX / F::FP_MAX;
-    static constexpr float K_DN = F::FP_MAX / (float)F::IMAX;
+    static constexpr float C_UP = F::KIND == kKindInt ? 1.0f : (float)F::IMAX / F::FP_MAX;
+    static constexpr float K_DN = F::KIND == kKindInt ? 1.0f : F::FP_MAX / (float)F::IMAX;
     static constexpr uint32_t CODE_MASK = (1u << F::BITS) - 1u;
     static constexpr uint32_t SIGN_BIT = 1u << (F::BITS - 1);
 };
+
+// Kernel-side quantizer options (the `qflags` argument of the quantize
+// kernels): with SR, decide the type / scaling on round-to-nearest
+// candidates; the 16/17 margin of Sec. 4.1 (needed for 4/6's second target).
+constexpr int kQSrRtnType = 1, kQMargin = 2;
+// 4 and 4 * 16/17 rounded once to fp32: the second target of 4/6.
+constexpr float kFourTarget = 4.0f;
+constexpr float kFourTargetMargin = (float)(4.0 * 16.0 / 17.0);
 
 // ------------------------------------------------------------- bit helpers
 __device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
@@ -290,33 +314,17 @@ __device__ __forceinline__ uint32_t quantize_group(const float (&v)[kGroup], flo
 }
 
 // ------------------------------------------- fast E2M1 group quantizer
-// IF4 / NVFP4 with round-to-nearest.  Same arithmetic as quantize_group, but
-// the FP candidate uses the gfx950 converter v_cvt_scalef32_pk_fp4_f32 (scale
-// 1.0): round to nearest even onto E2M1, saturating at 6, sign kept (a
-// negative value that rounds to zero gives code 0x8) -- identical to the
-// nearest-even rule over every fp32 input -- and v_cvt_scalef32_pk_f32_fp4 to
-// read the candidate back.  The codes come out packed (element 2i in the low
-// nibble of byte i).
-template <bool ADAPTIVE>
-__device__ __forceinline__ uint32_t quantize_group_e2m1(const float (&v)[kGroup], float alpha,
-                                                        float denom, uint2& packed)
+// The E2M1 round-to-nearest candidate of 16 scaled values through the
+// gfx950 converter v_cvt_scalef32_pk_fp4_f32 (scale 1.0): round to nearest
+// even onto E2M1, saturating at 6, sign kept (a negative value that rounds to
+// zero gives code 0x8) -- identical to the nearest-even rule over every fp32
+// input -- and v_cvt_scalef32_pk_f32_fp4 to read the candidate back.  The
+// codes come out packed (element 2i in the low nibble of byte i); returns
+// sum_j (q_j - x_j)^2 accumulated in element order with fused multiply-adds.
+__device__ __forceinline__ float e2m1_candidate(const float (&xb)[kGroup], uint32_t& f0, uint32_t& f1)
 {
-    constexpr float C_UP = 7.0f / 6.0f, K_DN = 6.0f / 7.0f;
-    float amax = 0.0f;
-#pragma unroll
-    for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(v[j]));
-    const uint32_t dcode = e4m3_encode(amax / denom);
-    const float s = alpha * e4m3_value(dcode);
-    if (!(s >= 1.17549435e-38f)) {
-        packed = make_uint2(0, 0);
-        return 0;
-    }
-    const float inv = 1.0f / s;
-    float xb[kGroup];
-#pragma unroll
-    for (int j = 0; j < kGroup; ++j) xb[j] = v[j] * inv;
-
-    uint32_t f0 = 0, f1 = 0;
+    f0 = 0;
+    f1 = 0;
     f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, xb[0], xb[1], 1.0f, 0);
     f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, xb[2], xb[3], 1.0f, 1);
     f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, xb[4], xb[5], 1.0f, 2);
@@ -344,6 +352,55 @@ __device__ __forceinline__ uint32_t quantize_group_e2m1(const float (&v)[kGroup]
         const float d = q[j] - xb[j];
         ef = __builtin_fmaf(d, d, ef);
     }
+    return ef;
+}
+
+// Packed INT4 codes from 16 floats t_j = r_j + 1.5 * 2^23 (r_j integral,
+// |r_j| <= 8): the low nibble of t_j's bit pattern is r_j in two's
+// complement.  Even elements -> low nibbles, odd -> high nibbles.
+__device__ __forceinline__ void pack_int4_biased(const uint32_t (&tb)[kGroup], uint32_t& i0, uint32_t& i1)
+{
+    const uint32_t e0 = __builtin_amdgcn_perm(tb[2], tb[0], 0x0C0C0400u) |
+                        __builtin_amdgcn_perm(tb[6], tb[4], 0x04000C0Cu);
+    const uint32_t o0 = __builtin_amdgcn_perm(tb[3], tb[1], 0x0C0C0400u) |
+                        __builtin_amdgcn_perm(tb[7], tb[5], 0x04000C0Cu);
+    const uint32_t e1 = __builtin_amdgcn_perm(tb[10], tb[8], 0x0C0C0400u) |
+                        __builtin_amdgcn_perm(tb[14], tb[12], 0x04000C0Cu);
+    const uint32_t o1 = __builtin_amdgcn_perm(tb[11], tb[9], 0x0C0C0400u) |
+                        __builtin_amdgcn_perm(tb[15], tb[13], 0x04000C0Cu);
+    i0 = (e0 & 0x0F0F0F0Fu) | ((o0 << 4) & 0xF0F0F0F0u);
+    i1 = (e1 & 0x0F0F0F0Fu) | ((o1 << 4) & 0xF0F0F0F0u);
+}
+
+__device__ __forceinline__ float group_amax(const float (&v)[kGroup])
+{
+    float amax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(v[j]));
+    return amax;
+}
+
+// IF4 / NVFP4 with round-to-nearest.  Same arithmetic as quantize_group,
+// with the FP candidate from e2m1_candidate.
+template <bool ADAPTIVE>
+__device__ __forceinline__ uint32_t quantize_group_e2m1(const float (&v)[kGroup], float alpha,
+                                                        float denom, uint2& packed)
+{
+    constexpr float C_UP = 7.0f / 6.0f, K_DN = 6.0f / 7.0f;
+    const float amax = group_amax(v);
+    const uint32_t dcode = e4m3_encode(amax / denom);
+    const float s = alpha * e4m3_value(dcode);
+    if (!(s >= 1.17549435e-38f)) {
+        packed = make_uint2(0, 0);
+        return 0;
+    }
+    const float inv = 1.0f / s;
+    float xb[kGroup];
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) xb[j] = v[j] * inv;
+
+    uint32_t f0, f1;
+    const float ef = e2m1_candidate(xb, f0, f1);
     if constexpr (!ADAPTIVE) {
         packed = make_uint2(f0, f1);
         return dcode;
@@ -361,20 +418,151 @@ __device__ __forceinline__ uint32_t quantize_group_e2m1(const float (&v)[kGroup]
         const float d = __builtin_fmaf(r, K_DN, -xb[j]);
         ei = __builtin_fmaf(d, d, ei);
     }
-    // gather the low bytes: even elements -> e*, odd -> o*, then nibble-merge
-    const uint32_t e0 = __builtin_amdgcn_perm(tb[2], tb[0], 0x0C0C0400u) |
-                        __builtin_amdgcn_perm(tb[6], tb[4], 0x04000C0Cu);
-    const uint32_t o0 = __builtin_amdgcn_perm(tb[3], tb[1], 0x0C0C0400u) |
-                        __builtin_amdgcn_perm(tb[7], tb[5], 0x04000C0Cu);
-    const uint32_t e1 = __builtin_amdgcn_perm(tb[10], tb[8], 0x0C0C0400u) |
-                        __builtin_amdgcn_perm(tb[14], tb[12], 0x04000C0Cu);
-    const uint32_t o1 = __builtin_amdgcn_perm(tb[11], tb[9], 0x0C0C0400u) |
-                        __builtin_amdgcn_perm(tb[15], tb[13], 0x04000C0Cu);
-    const uint32_t i0 = (e0 & 0x0F0F0F0Fu) | ((o0 << 4) & 0xF0F0F0F0u);
-    const uint32_t i1 = (e1 & 0x0F0F0F0Fu) | ((o1 << 4) & 0xF0F0F0F0u);
+    uint32_t i0, i1;
+    pack_int4_biased(tb, i0, i1);
     const bool use_int = ei < ef;
     packed = use_int ? make_uint2(i0, i1) : make_uint2(f0, f1);
     return dcode | (use_int ? 0x80u : 0u);
+}
+
+// ------------------------------------------------------------ NVINT4
+// INT4 elements scaled straight to 7 (Sec. 2, Table 1): Delta =
+// E4M3(max|X_g| / (alpha * 7)), q = the nearest integer to x-bar clamped to
+// [-7, 7] (ties to even), or with SR up iff u < |x-bar| - floor(|x-bar|)
+// (clamped to 7).  Scale bit 7 stays clear.  Codes come out packed.
+template <bool SR>
+__device__ __forceinline__ uint32_t quantize_group_int4(const float (&v)[kGroup], float alpha,
+                                                        float denom, const uint32_t (&w)[8],
+                                                        uint2& packed)
+{
+    const float amax = group_amax(v);
+    const uint32_t dcode = e4m3_encode(amax / denom);
+    const float s = alpha * e4m3_value(dcode);
+    if (!(s >= 1.17549435e-38f)) {
+        packed = make_uint2(0, 0);
+        return 0;
+    }
+    const float inv = 1.0f / s;
+    uint32_t tb[kGroup];
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+        const float xb = v[j] * inv;
+        float t;
+        if constexpr (SR) {
+            const float a = fabsf(xb);
+            const float lo = __builtin_floorf(a);
+            const float rr = fminf((sr_uniform(w, j) < a - lo) ? lo + 1.0f : lo, 7.0f);
+            t = ((xb < 0.0f) ? -rr : rr) + 12582912.0f;  // exact: an integer
+        } else {
+            t = __builtin_amdgcn_fmed3f(xb, -7.0f, 7.0f) + 12582912.0f;  // rint, ties to even
+        }
+        tb[j] = __float_as_uint(t);
+    }
+    uint32_t i0, i1;
+    pack_int4_biased(tb, i0, i1);
+    packed = make_uint2(i0, i1);
+    return dcode;
+}
+
+// ------------------------------------------------------------ 4/6
+// NVFP4 with Four Over Six (Sec. 3): the group is scaled to a maximum of 6
+// (denom6 = alpha * M) and of 4 (denom4 = alpha * 4, both with the 16/17
+// margin when it is on), rounded onto E2M1 each time, and the scaling with
+// the smaller Delta_t^2 * sum_j (q_j - x-bar_j)^2 (the dequantized squared
+// error over alpha^2) is kept; ties keep 6.  Delta_4 >= Delta_6: when
+// alpha * Delta_4 is below FLT_MIN the group stores zeros, when only
+// alpha * Delta_6 is, the scaling to 4 is kept.
+//
+// FP candidate of one scaling with optional SR: codes and the error sum of
+// the stored candidate, plus (RTN_ERR) the error of the round-to-nearest one.
+template <bool SR, bool RTN_ERR>
+__device__ __forceinline__ void e2m1_candidate_sr(const float (&v)[kGroup], float inv,
+                                                  const uint32_t (&w)[8], uint32_t (&code)[kGroup],
+                                                  float& err, float& err_rtn)
+{
+    err = 0.0f;
+    err_rtn = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+        const float xb = v[j] * inv;
+        const float m = fabsf(xb);
+        const uint32_t neg = __float_as_uint(xb) >> 31;
+        uint32_t idx;
+        if constexpr (SR)
+            idx = fp_sr_index<IFQ_FMT_NVFP4>(m, sr_uniform(w, j));
+        else
+            idx = fp_rtn_index<IFQ_FMT_NVFP4>(m);
+        code[j] = (neg << 3) | idx;
+        const float q = __uint_as_float(__float_as_uint(fp_magnitude<IFQ_FMT_NVFP4>(idx)) | (neg << 31));
+        const float d = q - xb;
+        err = __builtin_fmaf(d, d, err);
+        if constexpr (RTN_ERR) {
+            const float q0 = __uint_as_float(
+                __float_as_uint(fp_magnitude<IFQ_FMT_NVFP4>(fp_rtn_index<IFQ_FMT_NVFP4>(m))) | (neg << 31));
+            const float d0 = q0 - xb;
+            err_rtn = __builtin_fmaf(d0, d0, err_rtn);
+        }
+    }
+}
+
+// Round-to-nearest 4/6 with the converter path; codes packed.
+__device__ __forceinline__ uint32_t quantize_group_46(const float (&v)[kGroup], float alpha,
+                                                      float denom6, float denom4, uint2& packed)
+{
+    const float amax = group_amax(v);
+    const uint32_t dc6 = e4m3_encode(amax / denom6), dc4 = e4m3_encode(amax / denom4);
+    const float d6 = e4m3_value(dc6), d4 = e4m3_value(dc4);
+    const float s6 = alpha * d6, s4 = alpha * d4;
+    if (!(s4 >= 1.17549435e-38f)) {
+        packed = make_uint2(0, 0);
+        return 0;
+    }
+    float xb[kGroup];
+    const float inv4 = 1.0f / s4;
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) xb[j] = v[j] * inv4;
+    uint32_t b0, b1;
+    const float e4 = (d4 * d4) * e2m1_candidate(xb, b0, b1);
+    bool keep4 = true;
+    uint32_t a0 = 0, a1 = 0;
+    if (s6 >= 1.17549435e-38f) {
+        const float inv6 = 1.0f / s6;
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) xb[j] = v[j] * inv6;
+        const float e6 = (d6 * d6) * e2m1_candidate(xb, a0, a1);
+        keep4 = e4 < e6;
+    }
+    packed = keep4 ? make_uint2(b0, b1) : make_uint2(a0, a1);
+    return keep4 ? dc4 : dc6;
+}
+
+// Stochastic 4/6: both scalings round with the same draws; RTN_TYPE compares
+// the round-to-nearest candidates' errors instead (App. B).
+template <bool RTN_TYPE>
+__device__ __forceinline__ uint32_t quantize_group_46_sr(const float (&v)[kGroup], float alpha,
+                                                         float denom6, float denom4,
+                                                         const uint32_t (&w)[8], uint32_t (&code)[kGroup])
+{
+    const float amax = group_amax(v);
+    const uint32_t dc6 = e4m3_encode(amax / denom6), dc4 = e4m3_encode(amax / denom4);
+    const float d6 = e4m3_value(dc6), d4 = e4m3_value(dc4);
+    const float s6 = alpha * d6, s4 = alpha * d4;
+    if (!(s4 >= 1.17549435e-38f)) {
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) code[j] = 0;
+        return 0;
+    }
+    uint32_t c4[kGroup], c6[kGroup];
+    float e4, r4, e6 = 0.0f, r6 = 0.0f;
+    e2m1_candidate_sr<true, RTN_TYPE>(v, 1.0f / s4, w, c4, e4, r4);
+    bool keep4 = true;
+    if (s6 >= 1.17549435e-38f) {
+        e2m1_candidate_sr<true, RTN_TYPE>(v, 1.0f / s6, w, c6, e6, r6);
+        keep4 = RTN_TYPE ? ((d4 * d4) * r4 < (d6 * d6) * r6) : ((d4 * d4) * e4 < (d6 * d6) * e6);
+    }
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) code[j] = keep4 ? c4[j] : c6[j];
+    return keep4 ? dc4 : dc6;
 }
 
 // Dense little-endian bit stream of 16 codes of BITS bits: 2*BITS bytes,
@@ -448,6 +636,57 @@ template <int BITS> __device__ __forceinline__ void load_unpack16(const uint8_t*
         else
             val = (lo >> bit) | (hi << (64 - bit));
         c[j] = (uint32_t)val & ((1u << BITS) - 1u);
+    }
+}
+
+// ------------------------------------------------------ group dispatcher
+// Quantize one (already transformed) group of any format: returns the scale
+// byte and the packed codes.  denom = fp32(alpha * M) with M the format's
+// group target (with the margin when it is on); gi is the group's index for
+// the SR draws.
+template <int FMT, bool SR>
+__device__ __forceinline__ uint32_t quantize_any(const float (&v)[kGroup], float alpha, float denom,
+                                                 int qflags, uint64_t seed, int64_t gi,
+                                                 Packed<Fmt<FMT>::BITS>& out)
+{
+    using F = Fmt<FMT>;
+    constexpr int BITS = F::BITS;
+    uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if constexpr (SR) sr_words(seed, (uint64_t)gi, w);
+    const bool rtn_type = (qflags & kQSrRtnType) != 0;
+    if constexpr (F::KIND == kKindFourSix) {
+        const float denom4 = alpha * ((qflags & kQMargin) ? kFourTargetMargin : kFourTarget);
+        if constexpr (SR) {
+            uint32_t c[kGroup];
+            const uint32_t sb = rtn_type ? quantize_group_46_sr<true>(v, alpha, denom, denom4, w, c)
+                                         : quantize_group_46_sr<false>(v, alpha, denom, denom4, w, c);
+            out = pack16<4>(c);
+            return sb;
+        } else {
+            uint2 pk;
+            const uint32_t sb = quantize_group_46(v, alpha, denom, denom4, pk);
+            out.w[0] = pk.x;
+            out.w[1] = pk.y;
+            return sb;
+        }
+    } else if constexpr (F::KIND == kKindInt) {
+        uint2 pk;
+        const uint32_t sb = quantize_group_int4<SR>(v, alpha, denom, w, pk);
+        out.w[0] = pk.x;
+        out.w[1] = pk.y;
+        return sb;
+    } else if constexpr (BITS == 4 && !SR) {
+        uint2 pk;
+        const uint32_t sb = quantize_group_e2m1<F::ADAPTIVE>(v, alpha, denom, pk);
+        out.w[0] = pk.x;
+        out.w[1] = pk.y;
+        return sb;
+    } else {
+        uint32_t c[kGroup];
+        const uint32_t sb = (SR && rtn_type) ? quantize_group<FMT, SR, true>(v, alpha, denom, w, c)
+                                             : quantize_group<FMT, SR, false>(v, alpha, denom, w, c);
+        out = pack16<BITS>(c);
+        return sb;
     }
 }
 

@@ -55,6 +55,9 @@ template <> struct Fold<IFQ_FMT_IF4> {
     static constexpr float FP = 7.0f / 32.0f, INT = 6.0f / 32.0f, EPI = 1024.0f / 49.0f;
 };
 template <> struct Fold<IFQ_FMT_NVFP4> { static constexpr float FP = 1.0f, INT = 1.0f, EPI = 1.0f; };
+// NVINT4: q Delta / 4 (K = 128 Delta, C = -2 Delta on x = (q + 8) 2^-9); the
+// quarter keeps 128 * 448 below the FP16 maximum.
+template <> struct Fold<IFQ_FMT_NVINT4> { static constexpr float FP = 0.25f, INT = 0.25f, EPI = 16.0f; };
 template <> struct Fold<IFQ_FMT_IF3> { static constexpr float FP = 3.0f, INT = 4.0f, EPI = 1.0f / 9.0f; };
 // IF6: FP x 62 and INT x 15 (E2M3, ratio 7.5/31) or x 31 and x 28 (E3M2,
 // ratio 28/31), times lambda = 1/4 or 1/8 so that 7.5*62*448*lambda and
@@ -86,7 +89,11 @@ template <int FMT>
 __device__ __forceinline__ void pair_scales(uint32_t sw, uint32_t& K, uint32_t& Cb)
 {
     const half2v d = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw & 0x7F7Fu, 1.0f, false);  // E4M3 -> FP16
-    if constexpr (Fmt<FMT>::ADAPTIVE && Fmt<FMT>::BITS == 4) {
+    if constexpr (Fmt<FMT>::KIND == kKindInt) {
+        const half2v ki = {(_Float16)128.0f, (_Float16)128.0f}, cn = {(_Float16)-2.0f, (_Float16)-2.0f};
+        K = h2_as_u32(d * ki);
+        Cb = h2_as_u32(d * cn);
+    } else if constexpr (Fmt<FMT>::ADAPTIVE && Fmt<FMT>::BITS == 4) {
         half2v ki, kf, cn;
         ki[0] = (_Float16)96.0f; ki[1] = (_Float16)96.0f;
         kf[0] = (_Float16)Fold<FMT>::FP; kf[1] = (_Float16)Fold<FMT>::FP;
@@ -134,6 +141,16 @@ __device__ __forceinline__ void decode_word(uint32_t w, bool is_int, uint32_t k2
         x[1] = is_int ? y1 : x[1];
         x[2] = is_int ? y2 : x[2];
         x[3] = is_int ? y3 : x[3];
+    } else if constexpr (Fmt<FMT>::KIND == kKindInt) {
+        (void)is_int;
+        const uint32_t wu = w ^ 0x88888888u;
+        const uint32_t lo = wu & 0x0F0F0F0Fu, hi = (wu >> 4) & 0x0F0F0F0Fu;
+        const uint32_t d0 = __builtin_amdgcn_perm(hi, lo, 0x05010400u);
+        const uint32_t d1 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
+        x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d0, 1.0f, false));
+        x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d0, 1.0f, true));
+        x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d1, 1.0f, false));
+        x[3] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d1, 1.0f, true));
     }
     const half2v K = u32_as_h2(k2), C = u32_as_h2(c2);
 #pragma unroll
@@ -604,11 +621,26 @@ template <int N> __device__ __forceinline__ void vm_wait(u32x4& a, u32x4& b, u32
     asm volatile("s_waitcnt vmcnt(%4)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : "n"(N) : "memory");
 }
 
+// Drain every load before the epilogue.  The A registers of both slots are
+// operands: the compiler cannot see the asm loads as loads, so without them
+// the last (unused) A prefetch's registers count as free after the loop and
+// may be reassigned (e.g. to a store address) while that load is still
+// writing them.
+__device__ __forceinline__ void vm_drain(u32x4 (&a)[2][2][2])
+{
+    asm volatile("s_waitcnt vmcnt(0)"
+                 : "+v"(a[0][0][0]), "+v"(a[0][0][1]), "+v"(a[0][1][0]), "+v"(a[0][1][1]),
+                   "+v"(a[1][0][0]), "+v"(a[1][0][1]), "+v"(a[1][1][0]), "+v"(a[1][1][1])
+                 :
+                 : "memory");
+}
+
 // Fold constants of the two groups whose scale bytes are the low and high
 // byte of sw, one half each: the operand is K x + C, x the converted code.
 //   IF4 FP group : K = 7 Delta / 32, C = 0
 //   IF4 INT group: K = 96 Delta, C = -1.5 Delta (x = (q + 8) 2^-9)
 //   NVFP4        : K = Delta, C = 0
+//   NVINT4       : K = 128 Delta, C = -2 Delta (every group INT)
 // For IF4 the E4M3 conversion keeps the indicator bit as the sign (d = -Delta
 // for INT groups), so max(7 d / 32, -96 d) and min(1.5 d, 0) select the
 // constants without masks; C != 0 marks an INT group (an INT group with
@@ -621,7 +653,12 @@ template <int FMT>
 __device__ __forceinline__ KC pair_kc(uint32_t sw)
 {
     KC r;
-    if constexpr (Fmt<FMT>::ADAPTIVE) {
+    if constexpr (Fmt<FMT>::KIND == kKindInt) {
+        const half2v d = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw & 0x7F7Fu, 1.0f, false);
+        const half2v ki = {(_Float16)128.0f, (_Float16)128.0f}, cn = {(_Float16)-2.0f, (_Float16)-2.0f};
+        r.K = d * ki;
+        r.C = d * cn;
+    } else if constexpr (Fmt<FMT>::ADAPTIVE) {
         const half2v d = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw, 1.0f, false);
         const half2v f = {(_Float16)Fold<FMT>::FP, (_Float16)Fold<FMT>::FP};
         const half2v fi = {(_Float16)-96.0f, (_Float16)-96.0f};
@@ -645,6 +682,19 @@ __device__ __forceinline__ void decode_word_kc(uint32_t w, bool is_int, half2v K
                                                uint32_t (&out)[4])
 {
     uint32_t x[4];
+    if constexpr (Fmt<FMT>::KIND == kKindInt) {
+        (void)is_int;
+        const uint32_t w4 = w >> 4;
+        const uint32_t d0 = (__builtin_amdgcn_perm(w4, w, 0x05010400u) & 0x0F0F0F0Fu) ^ 0x08080808u;
+        const uint32_t d1 = (__builtin_amdgcn_perm(w4, w, 0x07030602u) & 0x0F0F0F0Fu) ^ 0x08080808u;
+        x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d0, 1.0f, false));
+        x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d0, 1.0f, true));
+        x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d1, 1.0f, false));
+        x[3] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d1, 1.0f, true));
+#pragma unroll
+        for (int i = 0; i < 4; ++i) out[i] = h2_as_u32(__builtin_elementwise_fma(u32_as_h2(x[i]), K2, C2));
+        return;
+    }
     x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 0));
     x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 1));
     x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 2));
@@ -973,7 +1023,7 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
         r2 = r0;
         r0 = t0;
     }
-    vm_wait<0>();
+    vm_drain(st.a);
     store_tile<FMT, OUT_BF16, false>(acc, a_ts, b_ts, M, N, C, ldc, m0, n0);
 }
 
@@ -1099,6 +1149,9 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s)
         case IFQ_FMT_IF3: return launch_g<IFQ_FMT_IF3>(a, s);
         case IFQ_FMT_IF6_E2M3: return launch_g<IFQ_FMT_IF6_E2M3>(a, s);
         case IFQ_FMT_IF6_E3M2: return launch_g<IFQ_FMT_IF6_E3M2>(a, s);
+        case IFQ_FMT_NVINT4: return launch_g<IFQ_FMT_NVINT4>(a, s);
+        // 4/6 operands are NVFP4 data (E2M1 codes, E4M3 scales, bit 7 clear)
+        case IFQ_FMT_NVFP4_46: return launch_g<IFQ_FMT_NVFP4>(a, s);
         default: return hipErrorNotSupported;
     }
 }

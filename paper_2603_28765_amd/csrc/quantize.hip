@@ -68,23 +68,13 @@ __device__ __forceinline__ float resolve_alpha(bool scale_in, float* tensor_scal
 template <int FMT, bool SR>
 __device__ __forceinline__ void quantize_store(const float (&v)[kGroup], float alpha, float denom,
                                                uint64_t seed, int64_t gi, uint8_t* __restrict__ codes,
-                                               uint8_t* __restrict__ scales, bool sr_rtn)
+                                               uint8_t* __restrict__ scales, int qflags)
 {
     constexpr int BITS = Fmt<FMT>::BITS;
-    if constexpr (BITS == 4 && !SR) {
-        uint2 pk;
-        const uint32_t sb = quantize_group_e2m1<Fmt<FMT>::ADAPTIVE>(v, alpha, denom, pk);
-        *reinterpret_cast<uint2*>(codes + gi * 8) = pk;
-        scales[gi] = (uint8_t)sb;
-    } else {
-        uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        if constexpr (SR) sr_words(seed, (uint64_t)gi, w);
-        uint32_t c[kGroup];
-        const uint32_t sb = (SR && sr_rtn) ? quantize_group<FMT, SR, true>(v, alpha, denom, w, c)
-                                           : quantize_group<FMT, SR, false>(v, alpha, denom, w, c);
-        store_packed<BITS>(codes + gi * (2 * BITS), pack16<BITS>(c));
-        scales[gi] = (uint8_t)sb;
-    }
+    Packed<BITS> p;
+    const uint32_t sb = quantize_any<FMT, SR>(v, alpha, denom, qflags, seed, gi, p);
+    store_packed<BITS>(codes + gi * (2 * BITS), p);
+    scales[gi] = (uint8_t)sb;
 }
 
 // --------------------------------------------------------------- row-wise
@@ -128,7 +118,7 @@ __global__ __launch_bounds__(kThreads) void tensor_max_rows(const uint16_t* __re
 template <int FMT, bool RHT, bool SR>
 __global__ __launch_bounds__(kThreads) void quantize_rows(
     const uint16_t* __restrict__ x, int64_t nrows, int64_t gpr, int64_t ld, uint32_t signs,
-    uint64_t seed, int sr_rtn, float scale_max, float denom_alpha, int scale_in,
+    uint64_t seed, int qflags, float scale_max, float denom_alpha, int scale_in,
     const float* __restrict__ partials, int npartials, uint8_t* __restrict__ codes,
     uint8_t* __restrict__ scales, float* tensor_scale)
 {
@@ -143,7 +133,7 @@ __global__ __launch_bounds__(kThreads) void quantize_rows(
             load_group_rowwise(x + r * ld + gc * kGroup, v);
             if constexpr (RHT) rht16(v, signs);
             const int64_t gi = r * gpr + gc;
-            quantize_store<FMT, SR>(v, alpha, denom, seed, gi, codes, scales, sr_rtn != 0);
+            quantize_store<FMT, SR>(v, alpha, denom, seed, gi, codes, scales, qflags);
         }
     }
 }
@@ -210,7 +200,7 @@ __global__ __launch_bounds__(kThreads) void tensor_max_strided(const uint16_t* _
 template <int FMT, bool RHT, bool SR>
 __global__ __launch_bounds__(kThreads) void quantize_strided(
     const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t ld, int vec,
-    uint32_t signs, uint64_t seed, int sr_rtn, float scale_max, float denom_alpha, int scale_in,
+    uint32_t signs, uint64_t seed, int qflags, float scale_max, float denom_alpha, int scale_in,
     const float* __restrict__ partials, int npartials, uint8_t* __restrict__ codes,
     uint8_t* __restrict__ scales, float* tensor_scale)
 {
@@ -233,7 +223,7 @@ __global__ __launch_bounds__(kThreads) void quantize_strided(
                     v[j] = __uint_as_float((uint32_t)tile[q * kGroup + j][c] << 16);
                 if constexpr (RHT) rht16(v, signs);
                 const int64_t gi = col * gpr + g;
-                quantize_store<FMT, SR>(v, alpha, denom, seed, gi, codes, scales, sr_rtn != 0);
+                quantize_store<FMT, SR>(v, alpha, denom, seed, gi, codes, scales, qflags);
             }
             __syncthreads();
         }
@@ -312,7 +302,7 @@ constexpr int kCodeRowBytes = kGrpTile * 8;
 template <int FMT, bool RHT, bool SR>
 __global__ __launch_bounds__(kThreads) void quantize_cols(
     const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t ld, uint32_t signs,
-    uint64_t seed, int sr_rtn, float scale_max, float denom_alpha, int scale_in,
+    uint64_t seed, int qflags, float scale_max, float denom_alpha, int scale_in,
     const float* __restrict__ partials, int npartials, uint8_t* __restrict__ codes,
     uint8_t* __restrict__ scales, float* tensor_scale)
 {
@@ -340,19 +330,9 @@ __global__ __launch_bounds__(kThreads) void quantize_cols(
                 column_of(r, c, v);
                 if constexpr (RHT) rht16(v, signs);
                 const int64_t gi = (c0 + 8 * cc + c) * ngroups + g0 + gl;  // SR counter: global group index
-                uint2 pk;
-                uint32_t sb;
-                if constexpr (!SR) {
-                    sb = quantize_group_e2m1<Fmt<FMT>::ADAPTIVE>(v, alpha, denom, pk);
-                } else {
-                    uint32_t w[8];
-                    sr_words(seed, (uint64_t)gi, w);
-                    uint32_t cq[kGroup];
-                    sb = sr_rtn ? quantize_group<FMT, true, true>(v, alpha, denom, w, cq)
-                                : quantize_group<FMT, true, false>(v, alpha, denom, w, cq);
-                    const Packed<4> pp = pack16<4>(cq);
-                    pk = make_uint2(pp.w[0], pp.w[1]);
-                }
+                Packed<4> pp;
+                const uint32_t sb = quantize_any<FMT, SR>(v, alpha, denom, qflags, seed, gi, pp);
+                const uint2 pk = make_uint2(pp.w[0], pp.w[1]);
                 const int row = 8 * cc + c;
                 *reinterpret_cast<uint2*>(lcodes + row * kCodeRowBytes + (gl ^ sw) * 8) = pk;
                 lscales[row * kGrpTile + (gl ^ sw)] = (uint8_t)sb;
@@ -420,12 +400,13 @@ static hipError_t launch_q(const QuantArgs& a, hipStream_t s, int npartials, flo
                            float denom_alpha)
 {
     const int scale_in = (a.flags & IFQ_SCALE_IN) ? 1 : 0;
-    const int sr_rtn = (a.flags & IFQ_SR_RTN_TYPE) ? 1 : 0;
+    const int qflags = ((a.flags & IFQ_SR_RTN_TYPE) ? kQSrRtnType : 0) |
+                       ((a.flags & IFQ_MARGIN_16_17) ? kQMargin : 0);
     if constexpr (Fmt<FMT>::BITS == 4) {
         if ((a.flags & IFQ_AXIS_STRIDED) && strided_cols_ok<FMT>(a)) {
             dim3 grid((unsigned)cdiv(a.cols, kColTile), (unsigned)cdiv(a.rows / kGroup, kGrpTile));
             hipLaunchKernelGGL((quantize_cols<FMT, RHT, SR>), grid, dim3(kThreads), 0, s, a.x, a.rows,
-                               a.cols, a.ld, a.signs, a.seed, sr_rtn, scale_max, denom_alpha, scale_in, a.partials,
+                               a.cols, a.ld, a.signs, a.seed, qflags, scale_max, denom_alpha, scale_in, a.partials,
                                npartials, a.codes, a.scales, a.tensor_scale);
             return hipGetLastError();
         }
@@ -433,7 +414,7 @@ static hipError_t launch_q(const QuantArgs& a, hipStream_t s, int npartials, flo
     if (a.flags & IFQ_AXIS_STRIDED) {
         dim3 grid((unsigned)cdiv(a.cols, kTC), (unsigned)std::min<int64_t>(cdiv(a.rows, kTR), 65535));
         hipLaunchKernelGGL((quantize_strided<FMT, RHT, SR>), grid, dim3(kThreads), 0, s, a.x,
-                           a.rows, a.cols, a.ld, strided_vec_ok(a), a.signs, a.seed, sr_rtn, scale_max, denom_alpha, scale_in,
+                           a.rows, a.cols, a.ld, strided_vec_ok(a), a.signs, a.seed, qflags, scale_max, denom_alpha, scale_in,
                            a.partials, npartials, a.codes, a.scales, a.tensor_scale);
     } else {
         const bool flat = a.ld == a.cols;
@@ -442,7 +423,7 @@ static hipError_t launch_q(const QuantArgs& a, hipStream_t s, int npartials, flo
         const int64_t ld = flat ? 0 : a.ld;
         dim3 grid((unsigned)cdiv(gpr, kThreads), (unsigned)std::min<int64_t>(nrows, 65535));
         hipLaunchKernelGGL((quantize_rows<FMT, RHT, SR>), grid, dim3(kThreads), 0, s, a.x, nrows,
-                           gpr, ld, a.signs, a.seed, sr_rtn, scale_max, denom_alpha, scale_in, a.partials,
+                           gpr, ld, a.signs, a.seed, qflags, scale_max, denom_alpha, scale_in, a.partials,
                            npartials, a.codes, a.scales, a.tensor_scale);
     }
     return hipGetLastError();
@@ -489,23 +470,29 @@ static hipError_t dispatch_fmt(const QuantArgs& a, hipStream_t s, int npartials,
     return launch_q<FMT, false, false>(a, s, npartials, scale_max, denom_alpha);
 }
 
-static float fp_max_of(int fmt)
+template <int FMT> static void targets(float& m, float& a8)
 {
-    switch (fmt) {
-        case IFQ_FMT_IF4: return Fmt<IFQ_FMT_IF4>::FP_MAX;
-        case IFQ_FMT_NVFP4: return Fmt<IFQ_FMT_NVFP4>::FP_MAX;
-        case IFQ_FMT_IF3: return Fmt<IFQ_FMT_IF3>::FP_MAX;
-        case IFQ_FMT_IF6_E2M3: return Fmt<IFQ_FMT_IF6_E2M3>::FP_MAX;
-        default: return Fmt<IFQ_FMT_IF6_E3M2>::FP_MAX;
-    }
+    m = Fmt<FMT>::M;
+    a8 = Fmt<FMT>::A8;
 }
 
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t s)
 {
-    // M of Eq. 1-2: M_FP, or M_FP * 16/17 with the gradient margin (Sec. 4.1)
-    float scale_max = fp_max_of(a.fmt);
+    // M and the E4M3 factor of Eq. 1-2 (M * 16/17 with the gradient margin
+    // of Sec. 4.1)
+    float scale_max = 0.0f, a8 = 0.0f;
+    switch (a.fmt) {
+        case IFQ_FMT_IF4: targets<IFQ_FMT_IF4>(scale_max, a8); break;
+        case IFQ_FMT_NVFP4: targets<IFQ_FMT_NVFP4>(scale_max, a8); break;
+        case IFQ_FMT_IF3: targets<IFQ_FMT_IF3>(scale_max, a8); break;
+        case IFQ_FMT_IF6_E2M3: targets<IFQ_FMT_IF6_E2M3>(scale_max, a8); break;
+        case IFQ_FMT_IF6_E3M2: targets<IFQ_FMT_IF6_E3M2>(scale_max, a8); break;
+        case IFQ_FMT_NVINT4: targets<IFQ_FMT_NVINT4>(scale_max, a8); break;
+        case IFQ_FMT_NVFP4_46: targets<IFQ_FMT_NVFP4_46>(scale_max, a8); break;
+        default: return hipErrorInvalidValue;
+    }
     if (a.flags & IFQ_MARGIN_16_17) scale_max = (float)((double)scale_max * 16.0 / 17.0);
-    const float denom_alpha = scale_max * 448.0f;
+    const float denom_alpha = scale_max * a8;
     const bool scale_in = a.flags & IFQ_SCALE_IN;
 
     if (a.rows == 0 || a.cols == 0) {  // empty tensor: alpha = 0, nothing to quantize
@@ -523,7 +510,9 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t s)
         case IFQ_FMT_NVFP4: return dispatch_fmt<IFQ_FMT_NVFP4>(a, s, npartials, scale_max, denom_alpha);
         case IFQ_FMT_IF3: return dispatch_fmt<IFQ_FMT_IF3>(a, s, npartials, scale_max, denom_alpha);
         case IFQ_FMT_IF6_E2M3: return dispatch_fmt<IFQ_FMT_IF6_E2M3>(a, s, npartials, scale_max, denom_alpha);
-        default: return dispatch_fmt<IFQ_FMT_IF6_E3M2>(a, s, npartials, scale_max, denom_alpha);
+        case IFQ_FMT_IF6_E3M2: return dispatch_fmt<IFQ_FMT_IF6_E3M2>(a, s, npartials, scale_max, denom_alpha);
+        case IFQ_FMT_NVINT4: return dispatch_fmt<IFQ_FMT_NVINT4>(a, s, npartials, scale_max, denom_alpha);
+        default: return dispatch_fmt<IFQ_FMT_NVFP4_46>(a, s, npartials, scale_max, denom_alpha);
     }
 }
 

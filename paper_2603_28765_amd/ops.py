@@ -18,9 +18,10 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libifq.so")
 
-IF4, NVFP4, IF3, IF6_E2M3, IF6_E3M2 = range(5)
-FORMAT_NAMES = {IF4: "if4", NVFP4: "nvfp4", IF3: "if3", IF6_E2M3: "if6_e2m3", IF6_E3M2: "if6_e3m2"}
-BITS = {IF4: 4, NVFP4: 4, IF3: 3, IF6_E2M3: 6, IF6_E3M2: 6}
+IF4, NVFP4, IF3, IF6_E2M3, IF6_E3M2, NVINT4, NVFP4_46 = range(7)
+FORMAT_NAMES = {IF4: "if4", NVFP4: "nvfp4", IF3: "if3", IF6_E2M3: "if6_e2m3", IF6_E3M2: "if6_e3m2",
+                NVINT4: "nvint4", NVFP4_46: "nvfp4_46"}
+BITS = {IF4: 4, NVFP4: 4, IF3: 3, IF6_E2M3: 6, IF6_E3M2: 6, NVINT4: 4, NVFP4_46: 4}
 
 RHT, SR, MARGIN_16_17, SCALE_IN, AXIS_STRIDED, SR_RTN_TYPE = 1, 2, 4, 8, 16, 32
 F32, BF16 = 0, 1

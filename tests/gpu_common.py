@@ -7,8 +7,8 @@ import torch
 import oracle as O
 from paper_2603_28765_amd import ops
 
-FORMATS = [ops.IF4, ops.NVFP4, ops.IF3, ops.IF6_E2M3, ops.IF6_E3M2]
-GEMM_FORMATS = [ops.IF4, ops.NVFP4, ops.IF3, ops.IF6_E2M3, ops.IF6_E3M2]
+FORMATS = [ops.IF4, ops.NVFP4, ops.IF3, ops.IF6_E2M3, ops.IF6_E3M2, ops.NVINT4, ops.NVFP4_46]
+GEMM_FORMATS = FORMATS
 
 
 def require_gpu():

@@ -72,6 +72,8 @@ def test_quantize_validation(L):
     assert q(L, flags=1 << 7) == EINVAL
     assert q(L, signs=1 << 16) == EINVAL
     assert q(L, fmt=9) == EINVAL
+    assert q(L, fmt=7) == EINVAL
+    assert q(L, fmt=6, cols=40) == ESHAPE
     assert q(L, rows=-1) == ESHAPE
     assert q(L, cols=40, ld=40) == ESHAPE                  # K % 16
     assert q(L, rows=40, flags=16) == ESHAPE               # strided: rows % 16
@@ -101,7 +103,10 @@ def test_gemm_validation(L):
     assert g(L, a=P16 + 4) == EALIGN
     assert g(L, fmt=3, K=40) == ESHAPE    # IF6 GEMM is validated like the others
     assert g(L, fmt=4, ldc=32) == ESHAPE
+    assert g(L, fmt=5, K=40) == ESHAPE    # NVINT4 and NVFP4 with 4/6 likewise
+    assert g(L, fmt=6, ldc=32) == ESHAPE
     assert g(L, fmt=7) == EINVAL
+    assert g(L, fmt=-1) == EINVAL
 
 
 def test_dequantize_validation(L):

@@ -25,7 +25,8 @@ def _quantized_pair(fmt, a_cpu, b_cpu, flags=0, signs=0, seeds=(0, 0)):
     return pa, oa, pb, ob
 
 
-EXACT_OPERANDS = (ops.IF4, ops.NVFP4, ops.IF3)  # IF6 operands are rounded to FP16
+# IF6 operands are rounded to FP16; the others are exact
+EXACT_OPERANDS = (ops.IF4, ops.NVFP4, ops.IF3, ops.NVINT4, ops.NVFP4_46)
 
 
 def _check(fmt, pa, oa, pb, ob, dtype=ops.F32, tag=""):

@@ -109,6 +109,33 @@ def test_ties_and_signed_zero():
         assert_quant_equal(fmt, x, 0, tag=f"ties auto fmt {fmt}")
 
 
+def test_nvint4_and_four_six_boundaries():
+    """NVINT4 with alpha = 1 and group maximum 7 (Delta = 1): half-integers
+    are exact rounding ties.  4/6: a group exact only when scaled to 4, a
+    group exact both ways (tie keeps 6), and, at alpha = 2^-120, a group
+    whose scaling to 6 falls below FLT_MIN while the scaling to 4 does not."""
+    halves = [0.5 + k for k in range(7)]
+    rows = [[7.0] + halves + [-h for h in halves] + [7.49],
+            [7.0] + [-7.0, 6.5, -6.5, 0.25, -0.25, 0.75, -0.75, 3.5, -3.5, 0.0, -0.0, 1e-3, 2.4999, 2.5001, 5.0]]
+    x = workloads.to_bf16(np.array(rows))
+    assert_quant_equal(ops.NVINT4, x, ops.SCALE_IN, alpha=1.0, tag="nvint4 ties")
+    assert_quant_equal(ops.NVINT4, x, ops.SCALE_IN | ops.MARGIN_16_17, alpha=1.0, tag="nvint4 margin")
+    rows = [[4.0, -3.0, 2.0, 1.0, 0.5, -1.5] + [0.0] * 10,
+            [3.0, -3.0] * 8,
+            [6.0, 4.5, 3.0, -2.25, 0.75, 1.5, 0.375] + [0.0] * 9,
+            [2.0 ** -124 * 1.25, 2.0 ** -126, -2.0 ** -125] + [0.0] * 13]
+    x = workloads.to_bf16(np.array(rows))
+    assert_quant_equal(ops.NVFP4_46, x, ops.SCALE_IN, alpha=1.0, tag="4/6 exact")
+    oc, osc, _ = O.quantize(bits(x), ops.NVFP4_46, O.SCALE_IN, tensor_scale=1.0)
+    assert O.e4m3_value(osc[0, 0]) == 1.0 and O.e4m3_value(osc[1, 0]) == 0.5
+    assert_quant_equal(ops.NVFP4_46, x, ops.SCALE_IN, alpha=2.0 ** -120, tag="4/6 tiny alpha")
+    oc, osc, _ = O.quantize(bits(x), ops.NVFP4_46, O.SCALE_IN, tensor_scale=2.0 ** -120)
+    assert O.e4m3_value(osc[3, 0]) == 1.25 * 2.0 ** -6  # the scaling to 4
+    for flags in (ops.SR, ops.SR | ops.SR_RTN_TYPE, ops.SR | ops.MARGIN_16_17):
+        assert_quant_equal(ops.NVFP4_46, x, ops.SCALE_IN | flags, alpha=1.0, seed=3,
+                           tag=f"4/6 flags {flags}")
+
+
 def test_zero_and_empty():
     z = torch.zeros((32, 64), dtype=torch.bfloat16)
     for fmt in FORMATS:
