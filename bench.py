@@ -44,7 +44,7 @@ def parse():
                                         "nvfp4_46"], default="if4",
                    help="format of the --mode step run")
     p.add_argument("--small", action="store_true", help="1/8-size shapes (quick checks)")
-    p.add_argument("--mode", choices=["full", "step", "copy"], default="full",
+    p.add_argument("--mode", choices=["full", "step", "copy", "wgrad", "bitwidth"], default="full",
                    help="step: only the timed IF4 step (for counter runs); copy: a plain 1 GiB "
                         "device copy, the reference for scaling the HBM byte counters")
     return p.parse_args()
@@ -74,6 +74,12 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"mode": "copy", "bytes_read_per_launch": n, "bytes_written_per_launch": n}))
+        return
+    if args.mode == "wgrad":
+        print(json.dumps({"mode": "wgrad", **wgrad_times(ops, workloads, torch)}))
+        return
+    if args.mode == "bitwidth":
+        print(json.dumps({"mode": "bitwidth", **bitwidth_times(ops, workloads, torch)}))
         return
     div = 8 if args.small else 1
     M, N, K = 8192 // div, 14336 // div, 4096 // div
@@ -214,6 +220,73 @@ TRAFFIC_KERNELS = {
 # copy (bench.py --mode copy): FETCH_SIZE reads back half the bytes read,
 # WRITE_SIZE the bytes written.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
+
+
+def _event_time(torch, fn, steps, warmup, flush=None):
+    """Mean time of fn() in seconds from HIP events on the current stream;
+    with `flush`, a 512 MiB buffer is rewritten before every launch so the
+    kernel reads from HBM."""
+    times = []
+    for i in range(warmup + steps):
+        if flush is not None:
+            flush.fill_(i & 0xFF)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        if i >= warmup:
+            times.append(e0.elapsed_time(e1) * 1e-3)
+    return float(sum(times) / len(times))
+
+
+def wgrad_times(ops, workloads, torch):
+    """Weight gradient dW = dY^T X (dY 8192 x 14336, X 8192 x 4096, both
+    quantized along the token axis with RHT, SR and the 16/17 margin; fp32
+    out): quantizer times (two-pass, and single-pass with alpha supplied and
+    a cache flush) and the GEMM M = 14336, N = 4096, K = 8192."""
+    w = workloads.wgrad()
+    dy, x = w.tensors["dY"].cuda(), w.tensors["X"].cuda()
+    ws = torch.empty(4096, dtype=torch.uint8, device="cuda")
+    fl = ops.AXIS_STRIDED | ops.RHT | ops.SR | ops.MARGIN_16_17
+    signs = w.info["rht_signs"]
+    sd, sx = w.info["sr_seed_dY"], w.info["sr_seed_X"]
+    pdy = ops.if4_quantize(dy, fl, signs, sd, workspace=ws)
+    px = ops.if4_quantize(x, fl, signs, sx, workspace=ws)
+    flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device="cuda")
+    t_dy = _event_time(torch, lambda: ops.if4_quantize(dy, fl, signs, sd, out=pdy, workspace=ws), 10, 2, flush)
+    t_dy1 = _event_time(torch, lambda: ops.if4_quantize(dy, fl | ops.SCALE_IN, signs, sd,
+                                                        tensor_scale=pdy.tensor_scale, out=pdy), 10, 2, flush)
+    t_x = _event_time(torch, lambda: ops.if4_quantize(x, fl, signs, sx, out=px, workspace=ws), 10, 2, flush)
+    del flush
+    M, N, K = w.info["M"], w.info["N"], w.info["K"]
+    out = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    t_g = _event_time(torch, lambda: ops.if4_gemm(pdy, px, ops.F32, out), 20, 5)
+    n_dy = dy.numel()
+    return {"workload": f"wgrad_{M}x{N}x{K}", "quant_dY_us": round(t_dy * 1e6, 1),
+            "quant_dY_1pass_us": round(t_dy1 * 1e6, 1),
+            "quant_dY_1pass_GBps": round(n_dy * 2.5625 / t_dy1 / 1e9, 1),
+            "quant_X_us": round(t_x * 1e6, 1), "gemm_us": round(t_g * 1e6, 1),
+            "gemm_TFLOPs": round(2.0 * M * N * K / t_g / 1e12, 1)}
+
+
+def bitwidth_times(ops, workloads, torch):
+    """Bit-width study: A, B 8192 x 8192 (N(0,1), 0.05 % of elements x100)
+    quantized along K in every format, then the 8192^3 GEMM with bf16 out."""
+    w = workloads.bitwidth()
+    a, b = w.tensors["A"].cuda(), w.tensors["B"].cuda()
+    n = a.shape[0]
+    ws = torch.empty(4096, dtype=torch.uint8, device="cuda")
+    out = torch.empty((n, n), dtype=torch.bfloat16, device="cuda")
+    res = {"workload": f"bitwidth_{n}^3"}
+    for fmt, name in ops.FORMAT_NAMES.items():
+        pa, pb = ops.ifx_quantize(fmt, a, workspace=ws), ops.ifx_quantize(fmt, b, workspace=ws)
+        t_q = _event_time(torch, lambda: ops.ifx_quantize(fmt, a, out=pa, workspace=ws), 5, 2)
+        t_g = _event_time(torch, lambda: ops.ifx_gemm(pa, pb, ops.BF16, out), 5, 2)
+        res[name] = {"quant_us": round(t_q * 1e6, 1), "gemm_us": round(t_g * 1e6, 1),
+                     "gemm_TFLOPs": round(2.0 * n ** 3 / t_g / 1e12, 1)}
+        del pa, pb
+    return res
 
 
 def _sources_digest(files):

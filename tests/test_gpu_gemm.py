@@ -166,3 +166,65 @@ def test_full_size_fwd_mlp_sampled():
     B = O.dequantize(ob[0][cols], ob[1][cols], ob[2], ops.IF4, np.float64)
     ref = A @ B.T
     assert rel_fro(got, bf16_round(ref)) <= TOL
+
+
+def _sampled_ref(fmt, oa_rows, ob_rows):
+    A = O.dequantize(oa_rows[0], oa_rows[1], oa_rows[2], fmt, np.float64)
+    B = O.dequantize(ob_rows[0], ob_rows[1], ob_rows[2], fmt, np.float64)
+    return A @ B.T
+
+
+def test_full_size_wgrad():
+    """The weight gradient as the benchmark times it: dY 8192 x 14336 and
+    X 8192 x 4096 quantized along the token axis with RHT, SR and the 16/17
+    margin (bit-exact over the whole tensors), then dW = dY^T X with
+    M = 14336, N = 4096, K = 8192 and fp32 out, checked on 256 sampled rows x
+    512 sampled columns against fp64."""
+    w = workloads.wgrad()
+    fl = ops.AXIS_STRIDED | ops.RHT | ops.SR | ops.MARGIN_16_17
+    pdy, ody = assert_quant_equal(ops.IF4, w.tensors["dY"], fl, w.info["rht_signs"],
+                                  w.info["sr_seed_dY"], tag="dY")
+    px, ox = assert_quant_equal(ops.IF4, w.tensors["X"], fl, w.info["rht_signs"],
+                                w.info["sr_seed_X"], tag="X")
+    c = ops.if4_gemm(pdy, px, ops.F32)
+    rng = np.random.default_rng(71)
+    rows = np.sort(rng.choice(14336, 256, replace=False))
+    cols = np.sort(rng.choice(4096, 512, replace=False))
+    got = c.cpu().numpy()[np.ix_(rows, cols)]
+    ref = _sampled_ref(ops.IF4, (ody[0][rows], ody[1][rows], ody[2]),
+                       (ox[0][cols], ox[1][cols], ox[2]))
+    assert rel_fro(got, ref) <= TOL
+
+
+@pytest.mark.parametrize("fmt", GEMM_FORMATS)
+def test_full_size_bitwidth_sampled(fmt):
+    """The 8192^3 bit-width configuration (N(0,1) with 0.05 % of elements
+    x100) in every format, bf16 out.  alpha is checked against Eq. 1 on the
+    whole tensor, the codes and scales of 128 sampled rows of each operand
+    bit-exactly against the oracle (row-wise groups are independent given
+    alpha), and the product on those rows and columns against fp64."""
+    w = workloads.bitwidth()
+    a, b = w.tensors["A"], w.tensors["B"]
+    pa = ops.ifx_quantize(fmt, a.cuda())
+    pb = ops.ifx_quantize(fmt, b.cuda())
+    c = ops.ifx_gemm(pa, pb, ops.BF16)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(72 + fmt)
+    rows = np.sort(rng.choice(8192, 128, replace=False))
+    cols = np.sort(rng.choice(8192, 128, replace=False))
+    sampled = []
+    for p, x, idx in ((pa, a, rows), (pb, b, cols)):
+        xb = x.contiguous().view(torch.int16).numpy().view(np.uint16)
+        amax = float(np.abs(O.bf16_to_f32(xb)).max())
+        alpha = float(p.tensor_scale.cpu()[0])
+        assert alpha == O.tensor_scale(fmt, amax)
+        oc, osc, _ = O.quantize(np.ascontiguousarray(xb[idx]), fmt, O.SCALE_IN, tensor_scale=alpha)
+        np.testing.assert_array_equal(p.codes.cpu().numpy()[idx], oc)
+        np.testing.assert_array_equal(p.scales.cpu().numpy()[idx], osc)
+        sampled.append((oc, osc, alpha))
+    got = c.float().cpu().numpy()[np.ix_(rows, cols)]
+    ref = _sampled_ref(fmt, sampled[0], sampled[1])
+    err = rel_fro(got, ref)
+    assert err <= rel_fro(bf16_round(ref), ref) + TOL
+    if fmt in EXACT_OPERANDS:
+        assert rel_fro(got, bf16_round(ref)) <= TOL

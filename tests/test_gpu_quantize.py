@@ -191,16 +191,6 @@ def test_full_size_quant_sweep():
         assert_quant_equal(fmt, x, ops.RHT, signs=w.info["rht_signs"], tag="full sweep rht")
 
 
-def test_full_size_wgrad_operands():
-    """The weight-gradient operands at full size (dY 8192 x 14336, X 8192 x
-    4096), quantized along the token axis with RHT, SR and the 16/17 margin:
-    bit-exact over the whole tensors."""
-    w = workloads.wgrad()
-    fl = ops.AXIS_STRIDED | ops.RHT | ops.SR | ops.MARGIN_16_17
-    assert_quant_equal(ops.IF4, w.tensors["dY"], fl, w.info["rht_signs"], w.info["sr_seed_dY"], tag="dY")
-    assert_quant_equal(ops.IF4, w.tensors["X"], fl, w.info["rht_signs"], w.info["sr_seed_X"], tag="X")
-
-
 def test_determinism_repeat():
     x = rand_bf16((512, 1024), 31, "outliers")
     p1, c1, s1, a1 = gpu_quantize(ops.IF4, x, ops.RHT | ops.SR, 0x5555, 9)
