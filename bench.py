@@ -44,7 +44,7 @@ def parse():
                                         "nvfp4_46"], default="if4",
                    help="format of the --mode step run")
     p.add_argument("--small", action="store_true", help="1/8-size shapes (quick checks)")
-    p.add_argument("--mode", choices=["full", "step", "copy", "wgrad", "bitwidth"], default="full",
+    p.add_argument("--mode", choices=["full", "step", "copy", "wgrad", "bitwidth", "dual"], default="full",
                    help="step: only the timed IF4 step (for counter runs); copy: a plain 1 GiB "
                         "device copy, the reference for scaling the HBM byte counters")
     return p.parse_args()
@@ -80,6 +80,9 @@ def main():
         return
     if args.mode == "bitwidth":
         print(json.dumps({"mode": "bitwidth", **bitwidth_times(ops, workloads, torch)}))
+        return
+    if args.mode == "dual":
+        print(json.dumps({"mode": "dual", **dual_times(ops, workloads, torch)}))
         return
     div = 8 if args.small else 1
     M, N, K = 8192 // div, 14336 // div, 4096 // div
@@ -286,6 +289,40 @@ def bitwidth_times(ops, workloads, torch):
         res[name] = {"quant_us": round(t_q * 1e6, 1), "gemm_us": round(t_g * 1e6, 1),
                      "gemm_TFLOPs": round(2.0 * n ** 3 / t_g / 1e12, 1)}
         del pa, pb
+    return res
+
+
+def dual_times(ops, workloads, torch):
+    """Training-step quantization of one linear layer's tensors in both
+    layouts (X 8192 x 4096 and W 14336 x 4096 with RTN, RHT on X's token
+    side; dY 8192 x 14336 with SR, RHT + SR + margin on its token side): two
+    separate quantizer calls against one dual call, each with a cache flush;
+    and the activation-gradient GEMM dX = dY W (M = 8192, N = 4096,
+    K = 14336, dY row-wise, W along its rows), bf16 out."""
+    wg = workloads.wgrad()
+    fw = workloads.fwd_mlp()
+    dy, x, W = wg.tensors["dY"].cuda(), fw.tensors["A"].cuda(), fw.tensors["W"].cuda()
+    signs = wg.info["rht_signs"]
+    flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device="cuda")
+    res = {}
+    for name, t, rf, cf in (("X", x, 0, ops.RHT), ("W", W, 0, 0),
+                            ("dY", dy, ops.SR, ops.RHT | ops.SR | ops.MARGIN_16_17)):
+        pr, pc = ops.ifx_quantize_dual(ops.IF4, t, rf, cf, signs, 1, 2)
+        ws = torch.empty(4096, dtype=torch.uint8, device="cuda")
+        sep = _event_time(torch, lambda: (ops.if4_quantize(t, rf, signs, 1, out=pr, workspace=ws),
+                                          ops.if4_quantize(t, cf | ops.AXIS_STRIDED, signs, 2, out=pc,
+                                                           workspace=ws)), 10, 2, flush)
+        dual = _event_time(torch, lambda: ops.ifx_quantize_dual(ops.IF4, t, rf, cf, signs, 1, 2, out_row=pr,
+                                                                out_col=pc, workspace=ws), 10, 2, flush)
+        res[name] = {"shape": list(t.shape), "separate_us": round(sep * 1e6, 1), "dual_us": round(dual * 1e6, 1)}
+    del flush
+    pdy, _ = ops.ifx_quantize_dual(ops.IF4, dy, ops.SR, ops.RHT | ops.SR | ops.MARGIN_16_17, signs, 1, 2)
+    _, pw = ops.ifx_quantize_dual(ops.IF4, W)
+    M, N, K = dy.shape[0], W.shape[1], dy.shape[1]
+    out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    t_g = _event_time(torch, lambda: ops.if4_gemm(pdy, pw, ops.BF16, out), 20, 5)
+    res["dgrad"] = {"workload": f"dgrad_{M}x{N}x{K}", "gemm_us": round(t_g * 1e6, 1),
+                    "gemm_TFLOPs": round(2.0 * M * N * K / t_g / 1e12, 1)}
     return res
 
 

@@ -158,6 +158,41 @@ int ifx_quantize(int format, const void* x, int64_t rows, int64_t cols, int64_t 
 /* Bytes of device workspace the quantizer needs (0 with IFQ_SCALE_IN). */
 size_t ifq_quantize_workspace_bytes(int format, int64_t rows, int64_t cols, uint32_t flags);
 
+/* ------------------------------------------------------- dual quantize --
+ * Both packed layouts of one bf16 matrix X from a single read of it: the
+ * row-wise form (groups along cols: codes [rows, cols*b/8], scales
+ * [rows, cols/16]) and the strided form (groups along rows, describing X^T:
+ * codes [cols, rows*b/8], scales [cols, rows/16]).  A linear layer's
+ * training step needs X, W and dY both ways (Sec. 4.1: the forward GEMM, the
+ * activation gradient dX = dY W and the weight gradient dW = dY^T X contract
+ * over different axes); the results are bit-identical to
+ *   ifx_quantize(format, x, ..., row_flags, rht_signs, row_seed, row_*) and
+ *   ifx_quantize(format, x, ..., col_flags | IFQ_AXIS_STRIDED, rht_signs,
+ *                col_seed, col_*).
+ *   format        IFQ_FMT_IF4, IFQ_FMT_NVFP4, IFQ_FMT_NVINT4 or
+ *                 IFQ_FMT_NVFP4_46 (others: IFQ_EUNSUPPORTED)
+ *   x             (device) bf16 [rows, ld_x], ld_x >= cols, 2-byte aligned;
+ *                 rows % 16 == 0 and cols % 16 == 0
+ *   row_flags, col_flags  IFQ_RHT, IFQ_SR, IFQ_MARGIN_16_17, IFQ_SCALE_IN,
+ *                 IFQ_SR_RTN_TYPE per side (IFQ_AXIS_STRIDED is rejected);
+ *                 each side has its own alpha (its RHT changes the values)
+ *   rht_signs     16-bit sign mask shared by both sides
+ *   row_seed, col_seed  Philox keys of the two sides (IFQ_SR)
+ *   row_codes, col_codes  (device) 16-byte aligned; row_scales, col_scales
+ *   row_tensor_scale, col_tensor_scale  (device) written, or read with
+ *                 IFQ_SCALE_IN on that side
+ *   workspace     (device) ifq_quantize_dual_workspace_bytes() bytes, 16-byte
+ *                 aligned (0 when both sides have IFQ_SCALE_IN)
+ */
+int ifx_quantize_dual(int format, const void* x, int64_t rows, int64_t cols, int64_t ld_x,
+                      uint32_t row_flags, uint32_t col_flags, uint32_t rht_signs, uint64_t row_seed,
+                      uint64_t col_seed, uint8_t* row_codes, uint8_t* row_scales, float* row_tensor_scale,
+                      uint8_t* col_codes, uint8_t* col_scales, float* col_tensor_scale, void* workspace,
+                      size_t workspace_bytes, void* stream);
+
+size_t ifq_quantize_dual_workspace_bytes(int format, int64_t rows, int64_t cols, uint32_t row_flags,
+                                         uint32_t col_flags);
+
 /* ---------------------------------------------------------- dequantize --
  * out[r, k] = q * Delta * (M_FP/M_I if INT) * alpha (the factor is 1 for
  * NVINT4), evaluated as three fp32 multiplies in that order (Fig. 3a lines 5 and 8 with alpha restored); the

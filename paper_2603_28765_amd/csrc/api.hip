@@ -70,6 +70,11 @@ int quantize_impl(int fmt, const void* x, int64_t rows, int64_t cols, int64_t ld
     return ifq::launch_quantize(a, static_cast<hipStream_t>(stream)) == hipSuccess ? IFQ_OK : IFQ_EHIP;
 }
 
+bool dual_format(int f)
+{
+    return f == IFQ_FMT_IF4 || f == IFQ_FMT_NVFP4 || f == IFQ_FMT_NVINT4 || f == IFQ_FMT_NVFP4_46;
+}
+
 int dequantize_impl(int fmt, const uint8_t* codes, const uint8_t* scales, const float* tensor_scale,
                     int64_t rows, int64_t cols, void* out, int out_dtype, void* stream)
 {
@@ -203,6 +208,59 @@ int ifx_gemm(int format, const uint8_t* a_codes, const uint8_t* a_scales,
 {
     return gemm_impl(format, a_codes, a_scales, a_tensor_scale, b_codes, b_scales, b_tensor_scale,
                      M, N, K, c, ldc, out_dtype, stream);
+}
+
+size_t ifq_quantize_dual_workspace_bytes(int format, int64_t rows, int64_t cols, uint32_t row_flags,
+                                         uint32_t col_flags)
+{
+    (void)format;
+    (void)rows;
+    (void)cols;
+    if ((row_flags & IFQ_SCALE_IN) && (col_flags & IFQ_SCALE_IN)) return 0;
+    return (size_t)2 * ifq::kMaxPartials * sizeof(float);
+}
+
+int ifx_quantize_dual(int format, const void* x, int64_t rows, int64_t cols, int64_t ld_x,
+                      uint32_t row_flags, uint32_t col_flags, uint32_t rht_signs, uint64_t row_seed,
+                      uint64_t col_seed, uint8_t* row_codes, uint8_t* row_scales, float* row_tensor_scale,
+                      uint8_t* col_codes, uint8_t* col_scales, float* col_tensor_scale, void* workspace,
+                      size_t workspace_bytes, void* stream)
+{
+    if (!valid_format(format)) return IFQ_EINVAL;
+    if ((row_flags | col_flags) & ~kKnownFlags) return IFQ_EINVAL;
+    if ((row_flags | col_flags) & IFQ_AXIS_STRIDED) return IFQ_EINVAL;
+    if (rht_signs > 0xFFFFu) return IFQ_EINVAL;
+    if (!row_tensor_scale || !col_tensor_scale) return IFQ_EINVAL;
+    if (!dual_format(format)) return IFQ_EUNSUPPORTED;
+    if (rows < 0 || cols < 0) return IFQ_ESHAPE;
+    if (rows > 0 && cols > 0 && rows > kMaxElems / cols) return IFQ_ESHAPE;
+    if (rows % 16 || cols % 16) return IFQ_ESHAPE;
+    if (!aligned(row_tensor_scale, 4) || !aligned(col_tensor_scale, 4)) return IFQ_EALIGN;
+    const bool empty = rows == 0 || cols == 0;
+    const bool need_ws = !((row_flags & IFQ_SCALE_IN) && (col_flags & IFQ_SCALE_IN));
+    if (!empty) {
+        if (!x || !row_codes || !row_scales || !col_codes || !col_scales) return IFQ_EINVAL;
+        if (ld_x < cols) return IFQ_ESHAPE;
+        if (!aligned(x, 2)) return IFQ_EALIGN;
+        if (!aligned(row_codes, 16) || !aligned(col_codes, 16)) return IFQ_EALIGN;
+        if (need_ws) {
+            if (!workspace ||
+                workspace_bytes < ifq_quantize_dual_workspace_bytes(format, rows, cols, row_flags, col_flags))
+                return IFQ_EWORKSPACE;
+            if (!aligned(workspace, 16)) return IFQ_EALIGN;
+        }
+    }
+    ifq::DualArgs a;
+    a.fmt = format;
+    a.x = static_cast<const uint16_t*>(x);
+    a.rows = rows;
+    a.cols = cols;
+    a.ld = ld_x;
+    a.signs = rht_signs;
+    float* ws = (need_ws && !empty) ? static_cast<float*>(workspace) : nullptr;
+    a.row = {row_flags, row_seed, row_codes, row_scales, row_tensor_scale, ws};
+    a.col = {col_flags, col_seed, col_codes, col_scales, col_tensor_scale, ws ? ws + ifq::kMaxPartials : nullptr};
+    return ifq::launch_quantize_dual(a, static_cast<hipStream_t>(stream)) == hipSuccess ? IFQ_OK : IFQ_EHIP;
 }
 
 size_t ifq_codes_bytes(int format, int64_t rows, int64_t cols)

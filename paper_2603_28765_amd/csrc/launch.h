@@ -25,6 +25,26 @@ struct QuantArgs {
 
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream);
 
+// One side of the dual quantizer (row-wise or strided output).
+struct DualSide {
+    uint32_t flags;  // IFQ_* bits of this side (IFQ_AXIS_STRIDED excluded)
+    uint64_t seed;
+    uint8_t* codes;
+    uint8_t* scales;
+    float* tensor_scale;
+    float* partials;  // kMaxPartials floats of workspace (unused with IFQ_SCALE_IN)
+};
+
+struct DualArgs {
+    int fmt;
+    const uint16_t* x;
+    int64_t rows, cols, ld;
+    uint32_t signs;
+    DualSide row, col;
+};
+
+hipError_t launch_quantize_dual(const DualArgs& a, hipStream_t stream);
+
 hipError_t launch_dequantize(int fmt, const uint8_t* codes, const uint8_t* scales,
                              const float* tensor_scale, int64_t rows, int64_t cols, void* out,
                              bool out_bf16, hipStream_t stream);

@@ -368,6 +368,127 @@ __global__ __launch_bounds__(kThreads) void quantize_cols(
 
 __global__ void write_scalar(float* p, float v) { *p = v; }
 
+// ------------------------------------------- dual layouts from one read
+// Training needs each of X, W and dY packed both ways: along its columns
+// (row-wise) and along its rows (strided, the packed form of the
+// transpose).  One launch per pass reads each 64 x 64 tile once into LDS;
+// thread t then takes column group (column t % 64, group t / 64) for the
+// strided output and row group (row t / 4, group t % 4) for the row-wise
+// output, each side with its own RHT / SR / margin / alpha.  Results equal
+// two separate quantizer calls bit for bit.
+struct DualSideK {
+    uint8_t* codes;
+    uint8_t* scales;
+    float* tensor_scale;
+    const float* partials;
+    uint64_t seed;
+    float scale_max, denom_alpha;
+    int qflags, rht, scale_in;
+};
+
+struct DualK {
+    const uint16_t* x;
+    int64_t rows, cols, ld;
+    int vec, npartials;
+    uint32_t signs;
+    DualSideK row, col;
+};
+
+__device__ __forceinline__ void tile_col_group(uint16_t (*tile)[kTC + 2], int c, int q, float (&v)[kGroup])
+{
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) v[j] = __uint_as_float((uint32_t)tile[q * kGroup + j][c] << 16);
+}
+
+__device__ __forceinline__ void tile_row_group(uint16_t (*tile)[kTC + 2], int r, int g, float (&v)[kGroup])
+{
+    // row pitch 132 bytes: 4-byte aligned pairs
+    const uint32_t* p = reinterpret_cast<const uint32_t*>(&tile[r][kGroup * g]);
+#pragma unroll
+    for (int i = 0; i < kGroup / 2; ++i) {
+        const uint32_t w = p[i];
+        v[2 * i] = bf16lo(w);
+        v[2 * i + 1] = bf16hi(w);
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void tensor_max_dual(DualK a, float* __restrict__ part_row,
+                                                            float* __restrict__ part_col)
+{
+    __shared__ __attribute__((aligned(16))) uint16_t tile[kTR][kTC + 2];
+    __shared__ float red[kThreads / 64];
+    float mr = 0.0f, mc = 0.0f;
+    const int t = threadIdx.x;
+    const int c = t % kTC, q = t / kTC, r = t / 4, g = t % 4;
+    for (int64_t c0 = (int64_t)blockIdx.x * kTC; c0 < a.cols; c0 += (int64_t)gridDim.x * kTC) {
+        for (int64_t r0 = (int64_t)blockIdx.y * kTR; r0 < a.rows; r0 += (int64_t)gridDim.y * kTR) {
+            stage_tile(a.x, a.rows, a.cols, a.ld, r0, c0, a.vec != 0, tile);
+            __syncthreads();
+            // elements outside the matrix are staged as zeros: they do not
+            // change a maximum, and an RHT of a zero-padded group is only
+            // taken where the whole group is inside
+            float v[kGroup];
+            if (c0 + c < a.cols && r0 + kGroup * q < a.rows) {
+                tile_col_group(tile, c, q, v);
+                if (a.col.rht) rht16(v, a.signs);
+#pragma unroll
+                for (int j = 0; j < kGroup; ++j) mc = fmaxf(mc, fabsf(v[j]));
+            }
+            if (r0 + r < a.rows && c0 + kGroup * g < a.cols) {
+                tile_row_group(tile, r, g, v);
+                if (a.row.rht) rht16(v, a.signs);
+#pragma unroll
+                for (int j = 0; j < kGroup; ++j) mr = fmaxf(mr, fabsf(v[j]));
+            }
+            __syncthreads();
+        }
+    }
+    mr = block_max(mr, red);
+    mc = block_max(mc, red);
+    if (t == 0) {
+        part_row[blockIdx.y * gridDim.x + blockIdx.x] = mr;
+        part_col[blockIdx.y * gridDim.x + blockIdx.x] = mc;
+    }
+}
+
+template <int FMT, bool SR_ROW, bool SR_COL>
+__global__ __launch_bounds__(kThreads) void quantize_dual(DualK a)
+{
+    __shared__ __attribute__((aligned(16))) uint16_t tile[kTR][kTC + 2];
+    __shared__ float red[kThreads / 64];
+    const float alpha_r = resolve_alpha(a.row.scale_in, a.row.tensor_scale, a.row.partials, a.npartials,
+                                        a.row.denom_alpha, red);
+    const float alpha_c = resolve_alpha(a.col.scale_in, a.col.tensor_scale, a.col.partials, a.npartials,
+                                        a.col.denom_alpha, red);
+    const float denom_r = alpha_r * a.row.scale_max, denom_c = alpha_c * a.col.scale_max;
+    const int64_t gpr_r = a.cols / kGroup, gpr_c = a.rows / kGroup;
+    const int t = threadIdx.x;
+    const int c = t % kTC, q = t / kTC, r = t / 4, g = t % 4;
+    for (int64_t c0 = (int64_t)blockIdx.x * kTC; c0 < a.cols; c0 += (int64_t)gridDim.x * kTC) {
+        for (int64_t r0 = (int64_t)blockIdx.y * kTR; r0 < a.rows; r0 += (int64_t)gridDim.y * kTR) {
+            stage_tile(a.x, a.rows, a.cols, a.ld, r0, c0, a.vec != 0, tile);
+            __syncthreads();
+            float v[kGroup];
+            const int64_t col = c0 + c, gc = r0 / kGroup + q;
+            if (col < a.cols && gc < gpr_c) {
+                tile_col_group(tile, c, q, v);
+                if (a.col.rht) rht16(v, a.signs);
+                quantize_store<FMT, SR_COL>(v, alpha_c, denom_c, a.col.seed, col * gpr_c + gc, a.col.codes,
+                                            a.col.scales, a.col.qflags);
+            }
+            const int64_t row = r0 + r, gr = c0 / kGroup + g;
+            if (row < a.rows && gr < gpr_r) {
+                tile_row_group(tile, r, g, v);
+                if (a.row.rht) rht16(v, a.signs);
+                quantize_store<FMT, SR_ROW>(v, alpha_r, denom_r, a.row.seed, row * gpr_r + gr, a.row.codes,
+                                            a.row.scales, a.row.qflags);
+            }
+            __syncthreads();
+        }
+    }
+}
+
+
 // ------------------------------------------------------------- launcher
 
 static inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -513,6 +634,77 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t s)
         case IFQ_FMT_IF6_E3M2: return dispatch_fmt<IFQ_FMT_IF6_E3M2>(a, s, npartials, scale_max, denom_alpha);
         case IFQ_FMT_NVINT4: return dispatch_fmt<IFQ_FMT_NVINT4>(a, s, npartials, scale_max, denom_alpha);
         default: return dispatch_fmt<IFQ_FMT_NVFP4_46>(a, s, npartials, scale_max, denom_alpha);
+    }
+}
+
+template <int FMT>
+static hipError_t launch_dual_fmt(const DualK& k, dim3 grid, bool sr_r, bool sr_c, hipStream_t s)
+{
+    if (sr_r && sr_c) hipLaunchKernelGGL((quantize_dual<FMT, true, true>), grid, dim3(kThreads), 0, s, k);
+    else if (sr_r) hipLaunchKernelGGL((quantize_dual<FMT, true, false>), grid, dim3(kThreads), 0, s, k);
+    else if (sr_c) hipLaunchKernelGGL((quantize_dual<FMT, false, true>), grid, dim3(kThreads), 0, s, k);
+    else hipLaunchKernelGGL((quantize_dual<FMT, false, false>), grid, dim3(kThreads), 0, s, k);
+    return hipGetLastError();
+}
+
+static void dual_side(const DualSide& d, float m, float a8, DualSideK& k)
+{
+    k.codes = d.codes;
+    k.scales = d.scales;
+    k.tensor_scale = d.tensor_scale;
+    k.partials = d.partials;
+    k.seed = d.seed;
+    k.scale_max = (d.flags & IFQ_MARGIN_16_17) ? (float)((double)m * 16.0 / 17.0) : m;
+    k.denom_alpha = k.scale_max * a8;
+    k.qflags = ((d.flags & IFQ_SR_RTN_TYPE) ? kQSrRtnType : 0) | ((d.flags & IFQ_MARGIN_16_17) ? kQMargin : 0);
+    k.rht = (d.flags & IFQ_RHT) ? 1 : 0;
+    k.scale_in = (d.flags & IFQ_SCALE_IN) ? 1 : 0;
+}
+
+// 4-bit training formats only (the caller has checked the format).
+hipError_t launch_quantize_dual(const DualArgs& a, hipStream_t s)
+{
+    float m = 0.0f, a8 = 0.0f;
+    switch (a.fmt) {
+        case IFQ_FMT_IF4: targets<IFQ_FMT_IF4>(m, a8); break;
+        case IFQ_FMT_NVFP4: targets<IFQ_FMT_NVFP4>(m, a8); break;
+        case IFQ_FMT_NVINT4: targets<IFQ_FMT_NVINT4>(m, a8); break;
+        case IFQ_FMT_NVFP4_46: targets<IFQ_FMT_NVFP4_46>(m, a8); break;
+        default: return hipErrorInvalidValue;
+    }
+    DualK k;
+    k.x = a.x;
+    k.rows = a.rows;
+    k.cols = a.cols;
+    k.ld = a.ld;
+    k.vec = (reinterpret_cast<uintptr_t>(a.x) % 16 == 0 && a.ld % 8 == 0) ? 1 : 0;
+    k.signs = a.signs;
+    dual_side(a.row, m, a8, k.row);
+    dual_side(a.col, m, a8, k.col);
+    if (a.rows == 0 || a.cols == 0) {  // empty tensor: alpha = 0 on each side that computes it
+        if (!k.row.scale_in) hipLaunchKernelGGL(write_scalar, dim3(1), dim3(1), 0, s, a.row.tensor_scale, 0.0f);
+        if (!k.col.scale_in) hipLaunchKernelGGL(write_scalar, dim3(1), dim3(1), 0, s, a.col.tensor_scale, 0.0f);
+        return hipGetLastError();
+    }
+    const int64_t tx = cdiv(a.cols, kTC), ty = cdiv(a.rows, kTR);
+    k.npartials = 0;
+    if (!(k.row.scale_in && k.col.scale_in)) {
+        const int64_t bx = std::min<int64_t>(tx, kMaxPartials);
+        const int64_t by = std::max<int64_t>(1, std::min<int64_t>(ty, kMaxPartials / bx));
+        k.npartials = (int)(bx * by);
+        // both sides' maxima are written (a side with alpha supplied ignores its own)
+        hipLaunchKernelGGL(tensor_max_dual, dim3((unsigned)bx, (unsigned)by), dim3(kThreads), 0, s, k,
+                           a.row.partials, a.col.partials);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const dim3 grid((unsigned)tx, (unsigned)std::min<int64_t>(ty, 65535));
+    const bool sr_r = a.row.flags & IFQ_SR, sr_c = a.col.flags & IFQ_SR;
+    switch (a.fmt) {
+        case IFQ_FMT_IF4: return launch_dual_fmt<IFQ_FMT_IF4>(k, grid, sr_r, sr_c, s);
+        case IFQ_FMT_NVFP4: return launch_dual_fmt<IFQ_FMT_NVFP4>(k, grid, sr_r, sr_c, s);
+        case IFQ_FMT_NVINT4: return launch_dual_fmt<IFQ_FMT_NVINT4>(k, grid, sr_r, sr_c, s);
+        default: return launch_dual_fmt<IFQ_FMT_NVFP4_46>(k, grid, sr_r, sr_c, s);
     }
 }
 

@@ -69,6 +69,13 @@ def lib() -> C.CDLL:
         L.ifq_codes_bytes.restype = C.c_size_t
         L.ifq_scales_bytes.argtypes = [C.c_int64, C.c_int64]
         L.ifq_scales_bytes.restype = C.c_size_t
+        L.ifx_quantize_dual.argtypes = [C.c_int, C.c_void_p, C.c_int64, C.c_int64, C.c_int64,
+                                         C.c_uint32, C.c_uint32, C.c_uint32, C.c_uint64, C.c_uint64,
+                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                         C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
+        L.ifq_quantize_dual_workspace_bytes.argtypes = [C.c_int, C.c_int64, C.c_int64, C.c_uint32,
+                                                        C.c_uint32]
+        L.ifq_quantize_dual_workspace_bytes.restype = C.c_size_t
         L.ifq_status_string.argtypes = [C.c_int]
         L.ifq_status_string.restype = C.c_char_p
         L.ifq_abi_version.restype = C.c_int
@@ -148,6 +155,46 @@ def nvfp4_quantize(x, flags=0, rht_signs=0, seed=0, tensor_scale=None, out=None,
 def ifx_quantize(fmt, x, flags=0, rht_signs=0, seed=0, tensor_scale=None, out=None,
                  workspace=None):
     return _quantize("ifx_quantize", fmt, x, flags, rht_signs, seed, tensor_scale, out, workspace)
+
+
+def _packed_for(fmt: int, R: int, K: int, dev, tensor_scale=None) -> Packed:
+    codes = torch.empty((R, K * BITS[fmt] // 8), dtype=torch.uint8, device=dev)
+    scales = torch.empty((R, K // 16), dtype=torch.uint8, device=dev)
+    ts = torch.empty(1, dtype=torch.float32, device=dev) if tensor_scale is None else tensor_scale
+    return Packed(fmt, codes, scales, ts, R, K)
+
+
+def ifx_quantize_dual(fmt, x, row_flags=0, col_flags=0, rht_signs=0, row_seed=0, col_seed=0,
+                      row_tensor_scale=None, col_tensor_scale=None, out_row=None, out_col=None,
+                      workspace=None):
+    """Both layouts of x from one read: (row-wise Packed [rows, cols],
+    strided Packed describing x^T [cols, rows]); see ifx_quantize_dual in
+    include/ifq.h."""
+    _require_gpu(x)
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D bf16 GPU tensor with unit column stride")
+    rows, cols = x.shape
+    dev = x.device
+    if out_row is None:
+        out_row = _packed_for(fmt, rows, cols, dev, row_tensor_scale)
+    elif row_tensor_scale is not None:
+        out_row.tensor_scale = row_tensor_scale
+    if out_col is None:
+        out_col = _packed_for(fmt, cols, rows, dev, col_tensor_scale)
+    elif col_tensor_scale is not None:
+        out_col.tensor_scale = col_tensor_scale
+    L = lib()
+    wsb = L.ifq_quantize_dual_workspace_bytes(fmt, rows, cols, row_flags, col_flags)
+    if wsb and workspace is None:
+        workspace = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_len = workspace.numel() if workspace is not None else 0
+    _check("ifx_quantize_dual", L.ifx_quantize_dual(
+        fmt, x.data_ptr(), rows, cols, x.stride(0), row_flags, col_flags, rht_signs, row_seed,
+        col_seed, out_row.codes.data_ptr(), out_row.scales.data_ptr(),
+        out_row.tensor_scale.data_ptr(), out_col.codes.data_ptr(), out_col.scales.data_ptr(),
+        out_col.tensor_scale.data_ptr(), ws_ptr, ws_len, _stream(x)))
+    return out_row, out_col
 
 
 def _dequantize(fn: str, p: Packed, out_dtype: int = F32, out: torch.Tensor | None = None):

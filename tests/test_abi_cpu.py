@@ -50,6 +50,9 @@ def test_version_and_strings(L):
     assert L.ifq_scales_bytes(256, 4096) == 256 * 256
     assert L.ifq_quantize_workspace_bytes(0, 8192, 8192, 0) >= 4
     assert L.ifq_quantize_workspace_bytes(0, 8192, 8192, 8) == 0
+    assert L.ifq_quantize_dual_workspace_bytes(0, 8192, 8192, 0, 8) >= 8
+    assert L.ifq_quantize_dual_workspace_bytes(0, 8192, 8192, 8, 8) == 0
+    assert "ifx_quantize_dual" in declared_functions()
 
 
 # fake, never dereferenced device addresses: validation fails first
@@ -107,6 +110,35 @@ def test_gemm_validation(L):
     assert g(L, fmt=6, ldc=32) == ESHAPE
     assert g(L, fmt=7) == EINVAL
     assert g(L, fmt=-1) == EINVAL
+
+
+def qd(L, fmt=0, x=P16, rows=32, cols=64, ld=64, rf=0, cf=0, signs=0, rc=P16, rs=P16, rts=P16,
+       cc=P16, cs=P16, cts=P16, ws=P16, wsb=4096):
+    return L.ifx_quantize_dual(fmt, x, rows, cols, ld, rf, cf, signs, 0, 0, rc, rs, rts, cc, cs, cts,
+                               ws, wsb, None)
+
+
+def test_dual_quantize_validation(L):
+    assert qd(L, rf=16) == EINVAL              # the strided bit is implied, not a flag
+    assert qd(L, cf=16) == EINVAL
+    assert qd(L, cf=1 << 7) == EINVAL
+    assert qd(L, signs=1 << 16) == EINVAL
+    assert qd(L, fmt=7) == EINVAL
+    assert qd(L, rts=None) == EINVAL
+    assert qd(L, cts=None) == EINVAL
+    assert qd(L, fmt=2) == EUNSUPPORTED        # IF3 / IF6: not training formats
+    assert qd(L, fmt=3) == EUNSUPPORTED
+    assert qd(L, rows=40) == ESHAPE            # both axes are grouped
+    assert qd(L, cols=40, ld=40) == ESHAPE
+    assert qd(L, ld=48) == ESHAPE
+    assert qd(L, rows=-16) == ESHAPE
+    assert qd(L, cc=None) == EINVAL
+    assert qd(L, rc=P16 + 8) == EALIGN
+    assert qd(L, cc=P16 + 8) == EALIGN
+    assert qd(L, x=P_ODD) == EALIGN
+    assert qd(L, ws=None) == EWORKSPACE
+    assert qd(L, wsb=16) == EWORKSPACE
+    assert qd(L, ws=P16 + 4) == EALIGN
 
 
 def test_dequantize_validation(L):

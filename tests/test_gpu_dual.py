@@ -1,0 +1,138 @@
+"""GPU parity of the dual-layout quantizer and of the activation-gradient
+GEMM of a training step (Sec. 4.1).
+
+The dual quantizer reads X once and writes its row-wise and strided packed
+forms; both must equal the oracle's separate quantizations bit for bit, and
+the separate GPU calls as well.  dX = dY W contracts over W's rows, so W is
+quantized along its rows (the strided layout, describing W^T) and the TN GEMM
+takes (dY row-wise, W strided)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2603_28765_amd import ops, workloads
+from tests.gpu_common import bf16_round, bits, gpu_quantize, rel_fro, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+DUAL_FORMATS = [ops.IF4, ops.NVFP4, ops.NVINT4, ops.NVFP4_46]
+# (row flags, col flags): forward activations / weights; the gradient recipe
+# (SR on both, RHT + margin on the weight-gradient side); alpha supplied
+FLAG_PAIRS = [(0, 0), (0, ops.RHT), (ops.SR, ops.RHT | ops.SR | ops.MARGIN_16_17),
+              (ops.SR | ops.SR_RTN_TYPE, ops.RHT | ops.SR | ops.SR_RTN_TYPE), (ops.RHT, 0)]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _check_side(p, fmt, x_cpu, flags, signs, seed, alpha, tag):
+    oc, osc, oa = O.quantize(bits(x_cpu), fmt, flags, signs, seed, alpha)
+    got_a = float(p.tensor_scale.cpu()[0])
+    assert got_a == oa, (tag, "alpha", got_a, oa)
+    np.testing.assert_array_equal(p.scales.cpu().numpy(), osc, err_msg=f"{tag} scales")
+    np.testing.assert_array_equal(p.codes.cpu().numpy(), oc, err_msg=f"{tag} codes")
+
+
+def _dual(fmt, x_cpu, rf, cf, signs=0x5A3C, rs=11, cs=12, alphas=(None, None)):
+    ts_r = None if alphas[0] is None else torch.tensor([alphas[0]], dtype=torch.float32, device="cuda")
+    ts_c = None if alphas[1] is None else torch.tensor([alphas[1]], dtype=torch.float32, device="cuda")
+    pr, pc = ops.ifx_quantize_dual(fmt, x_cpu.cuda(), rf, cf, signs, rs, cs, ts_r, ts_c)
+    torch.cuda.synchronize()
+    _check_side(pr, fmt, x_cpu, rf, signs, rs, alphas[0], f"fmt {fmt} row {rf}")
+    _check_side(pc, fmt, x_cpu, cf | ops.AXIS_STRIDED, signs, cs, alphas[1], f"fmt {fmt} col {cf}")
+    return pr, pc
+
+
+@pytest.mark.parametrize("fmt", DUAL_FORMATS)
+@pytest.mark.parametrize("flags", FLAG_PAIRS)
+def test_dual_matches_oracle(fmt, flags):
+    rng = np.random.default_rng(80 + fmt)
+    for shape in [(64, 64), (272, 528), (80, 1040), (1024, 48)]:
+        x = workloads.to_bf16(rng.standard_t(3, shape) * np.exp(rng.normal(0, 1, shape[1])))
+        _dual(fmt, x, *flags)
+
+
+def test_dual_equals_separate_gpu_calls():
+    rng = np.random.default_rng(90)
+    x = workloads.to_bf16(rng.laplace(0, 1e-3, (512, 768)))
+    rf, cf = ops.SR, ops.RHT | ops.SR | ops.MARGIN_16_17
+    pr, pc = ops.ifx_quantize_dual(ops.IF4, x.cuda(), rf, cf, 0x1234, 5, 6)
+    _, c1, s1, a1 = gpu_quantize(ops.IF4, x, rf, 0x1234, 5)
+    _, c2, s2, a2 = gpu_quantize(ops.IF4, x, cf | ops.AXIS_STRIDED, 0x1234, 6)
+    assert float(pr.tensor_scale.cpu()[0]) == a1 and float(pc.tensor_scale.cpu()[0]) == a2
+    assert np.array_equal(pr.codes.cpu().numpy(), c1) and np.array_equal(pr.scales.cpu().numpy(), s1)
+    assert np.array_equal(pc.codes.cpu().numpy(), c2) and np.array_equal(pc.scales.cpu().numpy(), s2)
+
+
+def test_dual_scale_in_and_padded_rows():
+    """alpha supplied on one side or both; a row stride wider than cols."""
+    rng = np.random.default_rng(91)
+    x = workloads.to_bf16(rng.standard_normal((96, 160)))
+    _dual(ops.IF4, x, ops.SCALE_IN, 0, alphas=(0.01, None))
+    _dual(ops.NVFP4, x, 0, ops.SCALE_IN | ops.RHT, alphas=(None, 0.002))
+    _dual(ops.IF4, x, ops.SCALE_IN, ops.SCALE_IN, alphas=(0.01, 0.003))
+    big = torch.zeros((96, 200), dtype=torch.bfloat16)
+    big[:, :160] = x
+    xs = big.cuda()[:, :160]
+    pr, pc = ops.ifx_quantize_dual(ops.IF4, xs, 0, ops.RHT, 0x0F0F, 0, 0)
+    torch.cuda.synchronize()
+    _check_side(pr, ops.IF4, x, 0, 0x0F0F, 0, None, "padded row")
+    _check_side(pc, ops.IF4, x, ops.RHT | ops.AXIS_STRIDED, 0x0F0F, 0, None, "padded col")
+
+
+def test_dual_zero_and_empty():
+    z = torch.zeros((32, 64), dtype=torch.bfloat16)
+    _dual(ops.IF4, z, 0, ops.RHT)
+    pr, pc = ops.ifx_quantize_dual(ops.IF4, torch.zeros((0, 64), dtype=torch.bfloat16, device="cuda"))
+    torch.cuda.synchronize()
+    assert float(pr.tensor_scale.cpu()[0]) == 0.0 and float(pc.tensor_scale.cpu()[0]) == 0.0
+
+
+@pytest.mark.parametrize("fmt", DUAL_FORMATS)
+def test_dgrad_gemm(fmt):
+    """dX = dY W with dY [T, N_out] (SR, row-wise) and W [N_out, N_in]
+    quantized along N_out (strided): C = dY_hat (W^T)_hat^T, fp32 out,
+    against fp64 of the oracle-dequantized operands."""
+    w = workloads.small_like("wgrad", 16)
+    dy = w.tensors["dY"]                       # [512, 896]
+    rng = np.random.default_rng(92)
+    W = workloads.to_bf16(rng.normal(0, 0.02, (dy.shape[1], 256)))   # [N_out, N_in]
+    pdy = ops.ifx_quantize(fmt, dy.cuda(), ops.SR, 0, 7)
+    pw_row, pw_col = ops.ifx_quantize_dual(fmt, W.cuda())
+    c = ops.ifx_gemm(pdy, pw_col, ops.F32).cpu().numpy()
+    ody = O.quantize(bits(dy), fmt, O.SR, 0, 7)
+    ow = O.quantize(bits(W), fmt, O.STRIDED)
+    np.testing.assert_array_equal(pw_col.codes.cpu().numpy(), ow[0])
+    ref = O.gemm_ref(ody[0], ody[1], ody[2], ow[0], ow[1], ow[2], fmt)
+    assert rel_fro(c, ref) <= 1e-3
+    # and the product approximates dY W itself
+    exact = O.bf16_to_f32(bits(dy)).astype(np.float64) @ O.bf16_to_f32(bits(W)).astype(np.float64)
+    assert rel_fro(c, exact) < 0.3
+
+
+def test_full_size_dual_dy_and_dgrad_sampled():
+    """dY 8192 x 14336 in both layouts with the gradient recipe (bit-exact
+    over the whole tensors), W 14336 x 4096 along N_out, and the dgrad GEMM
+    M = 8192, N = 4096, K = 14336 on 256 x 256 sampled outputs."""
+    w = workloads.wgrad()
+    dy = w.tensors["dY"]
+    sd = w.info["sr_seed_dY"]
+    rf, cf = ops.SR, ops.RHT | ops.SR | ops.MARGIN_16_17
+    pr, pc = _dual(ops.IF4, dy, rf, cf, signs=w.info["rht_signs"], rs=sd + 1, cs=sd)
+    rng = np.random.default_rng(93)
+    W = workloads.to_bf16(rng.normal(0, 0.02, (14336, 4096)))
+    _, pw = ops.ifx_quantize_dual(ops.IF4, W.cuda())
+    c = ops.if4_gemm(pr, pw, ops.F32)
+    rows = np.sort(rng.choice(8192, 256, replace=False))
+    cols = np.sort(rng.choice(4096, 256, replace=False))
+    got = c.cpu().numpy()[np.ix_(rows, cols)]
+    A = O.dequantize(pr.codes.cpu().numpy()[rows], pr.scales.cpu().numpy()[rows],
+                     float(pr.tensor_scale.cpu()[0]), ops.IF4, np.float64)
+    ow = O.quantize(np.ascontiguousarray(bits(W)[:, cols]), ops.IF4, O.STRIDED | O.SCALE_IN,
+                    tensor_scale=float(pw.tensor_scale.cpu()[0]))
+    np.testing.assert_array_equal(pw.codes.cpu().numpy()[cols], ow[0])
+    B = O.dequantize(ow[0], ow[1], ow[2], ops.IF4, np.float64)
+    assert rel_fro(got, A @ B.T) <= 1e-3
