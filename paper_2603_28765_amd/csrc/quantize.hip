@@ -637,6 +637,173 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t s)
     }
 }
 
+// Register path of the dual quantizer (the strided register layout of
+// quantize_cols / tensor_max_cols, same conditions).  A lane holds 16 rows x
+// 8 columns; the lane holding the other 8 columns of the same 16 rows is its
+// DPP partner (CTRL: row_ror:8 for lane ^ 8, quad_perm [1,0,3,2] for
+// lane ^ 1).  Each sends the half the other needs -- the even-chunk lane keeps
+// rows 0-7, the odd one rows 8-15 -- so after 32 dword moves each lane holds 8
+// complete row groups: row 8 * odd + j, columns 0-15 of the pair.
+template <int CTRL>
+__device__ __forceinline__ void row_group_of_pair(const u32x4v (&r)[kGroup], bool odd, int j, float (&v)[kGroup])
+{
+    u32x4v send = odd ? r[j] : r[8 + j];
+    u32x4v recv;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        recv[e] = (uint32_t)__builtin_amdgcn_mov_dpp((int)send[e], CTRL, 0xF, 0xF, false);
+    const u32x4v lo = odd ? recv : r[j];
+    const u32x4v hi = odd ? r[8 + j] : recv;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        v[2 * i] = bf16lo(lo[i]);
+        v[2 * i + 1] = bf16hi(lo[i]);
+        v[8 + 2 * i] = bf16lo(hi[i]);
+        v[8 + 2 * i + 1] = bf16hi(hi[i]);
+    }
+}
+
+constexpr int kDppRor8 = 0x128;    // row_ror:8 -> lane ^ 8 within 16-lane rows
+constexpr int kDppSwap1 = 0xB1;    // quad_perm [1,0,3,2] -> lane ^ 1
+
+__global__ __launch_bounds__(kThreads) void tensor_max_cols_dual(DualK a, float* __restrict__ part_row,
+                                                                 float* __restrict__ part_col)
+{
+    __shared__ float red[kThreads / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t ngroups = a.rows / kGroup;
+    const bool odd = lane & 1;  // chunk 8 * lane: partner lane ^ 1
+    float mr = 0.0f, mc = 0.0f;
+    for (int64_t cb = blockIdx.x; cb * kColsPerBlock < a.cols; cb += gridDim.x) {
+        const int64_t col = cb * kColsPerBlock + 8 * lane;
+        if (col >= a.cols) continue;  // cols % 16 == 0: partners leave together
+        for (int64_t g = (int64_t)blockIdx.y * 4 + wave; g < ngroups; g += (int64_t)gridDim.y * 4) {
+            u32x4v r[kGroup];
+            load_col_block(a.x + g * kGroup * a.ld + col, a.ld, r);
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                float v[kGroup];
+                column_of(r, c, v);
+                if (!a.row.rht) {
+#pragma unroll
+                    for (int j = 0; j < kGroup; ++j) mr = fmaxf(mr, fabsf(v[j]));
+                }
+                if (a.col.rht) rht16(v, a.signs);
+#pragma unroll
+                for (int j = 0; j < kGroup; ++j) mc = fmaxf(mc, fabsf(v[j]));
+            }
+            if (a.row.rht) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    float v[kGroup];
+                    row_group_of_pair<kDppSwap1>(r, odd, j, v);
+                    rht16(v, a.signs);
+#pragma unroll
+                    for (int e = 0; e < kGroup; ++e) mr = fmaxf(mr, fabsf(v[e]));
+                }
+            }
+        }
+    }
+    mr = block_max(mr, red);
+    mc = block_max(mc, red);
+    if (threadIdx.x == 0) {
+        part_row[blockIdx.y * gridDim.x + blockIdx.x] = mr;
+        part_col[blockIdx.y * gridDim.x + blockIdx.x] = mc;
+    }
+}
+
+// Pass 2: quantize_cols' tile (64 columns x 2048 rows, strided output staged
+// in LDS and written as whole lines) plus the row-wise groups of the same
+// registers, stored directly (8 code bytes and one scale byte per group;
+// the four groups of a lane quad-row are contiguous).
+template <int FMT, bool SR_ROW, bool SR_COL>
+__global__ __launch_bounds__(kThreads) void quantize_cols_dual(DualK a)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t lcodes[kColTile * kCodeRowBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t lscales[kColTile * kGrpTile];
+    __shared__ float red[kThreads / 64];
+    const float alpha_r = resolve_alpha(a.row.scale_in, a.row.tensor_scale, a.row.partials, a.npartials,
+                                        a.row.denom_alpha, red);
+    const float alpha_c = resolve_alpha(a.col.scale_in, a.col.tensor_scale, a.col.partials, a.npartials,
+                                        a.col.denom_alpha, red);
+    const float denom_r = alpha_r * a.row.scale_max, denom_c = alpha_c * a.col.scale_max;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int64_t ngroups = a.rows / kGroup, gpr_r = a.cols / kGroup;
+    const int64_t c0 = (int64_t)blockIdx.x * kColTile, g0 = (int64_t)blockIdx.y * kGrpTile;
+    const int ntg = (int)min<int64_t>(kGrpTile, ngroups - g0);
+    const int ncol = (int)min<int64_t>(kColTile, a.cols - c0);
+    const int cc = lane >> 3, q = lane & 7;
+    const bool odd = cc & 1;
+    const int sw = 8 * cc;
+    for (int rg = 0; rg < ntg; rg += 32) {
+        const int gl = rg + 8 * wave + q;
+        // ncol is a multiple of 16, so both chunks of a pair pass or fail together
+        if (gl < ntg && 8 * cc < ncol) {
+            u32x4v r[kGroup];
+            load_col_block(a.x + (g0 + gl) * kGroup * a.ld + c0 + 8 * cc, a.ld, r);
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                float v[kGroup];
+                column_of(r, c, v);
+                if (a.col.rht) rht16(v, a.signs);
+                const int64_t gi = (c0 + 8 * cc + c) * ngroups + g0 + gl;
+                Packed<4> pp;
+                const uint32_t sb = quantize_any<FMT, SR_COL>(v, alpha_c, denom_c, a.col.qflags, a.col.seed, gi, pp);
+                const int row = 8 * cc + c;
+                *reinterpret_cast<uint2*>(lcodes + row * kCodeRowBytes + (gl ^ sw) * 8) = make_uint2(pp.w[0], pp.w[1]);
+                lscales[row * kGrpTile + (gl ^ sw)] = (uint8_t)sb;
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                float v[kGroup];
+                row_group_of_pair<kDppRor8>(r, odd, j, v);
+                if (a.row.rht) rht16(v, a.signs);
+                const int64_t row = (g0 + gl) * kGroup + 8 * (odd ? 1 : 0) + j;
+                const int64_t gi = row * gpr_r + c0 / kGroup + (cc >> 1);
+                Packed<4> pp;
+                const uint32_t sb = quantize_any<FMT, SR_ROW>(v, alpha_r, denom_r, a.row.qflags, a.row.seed, gi, pp);
+                *reinterpret_cast<uint2*>(a.row.codes + gi * 8) = make_uint2(pp.w[0], pp.w[1]);
+                a.row.scales[gi] = (uint8_t)sb;
+            }
+        }
+    }
+    __syncthreads();
+    uint8_t* codes = a.col.codes;
+    uint8_t* scales = a.col.scales;
+    const int ppr = ntg / 2;
+    for (int idx = t; idx < ncol * ppr; idx += kThreads) {
+        const int row = idx / ppr, pc = idx % ppr;
+        const int s = 8 * (row >> 3);
+        const uint4 v = *reinterpret_cast<const uint4*>(lcodes + row * kCodeRowBytes + ((2 * pc) ^ s) * 8);
+        *reinterpret_cast<uint4*>(codes + ((c0 + row) * ngroups + g0 + 2 * pc) * 8) = v;
+    }
+    const int spr = ntg / 16;
+    for (int idx = t; idx < ncol * spr; idx += kThreads) {
+        const int row = idx / spr, pc = idx % spr;
+        const int s = 8 * (row >> 3);
+        uint32_t w4[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            uint32_t wv = 0;
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+                wv |= (uint32_t)lscales[row * kGrpTile + ((16 * pc + 4 * k + b) ^ s)] << (8 * b);
+            w4[k] = wv;
+        }
+        *reinterpret_cast<uint4*>(scales + (c0 + row) * ngroups + g0 + 16 * pc) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+    }
+}
+
+template <int FMT>
+static hipError_t launch_cols_dual_fmt(const DualK& k, dim3 grid, bool sr_r, bool sr_c, hipStream_t s)
+{
+    if (sr_r && sr_c) hipLaunchKernelGGL((quantize_cols_dual<FMT, true, true>), grid, dim3(kThreads), 0, s, k);
+    else if (sr_r) hipLaunchKernelGGL((quantize_cols_dual<FMT, true, false>), grid, dim3(kThreads), 0, s, k);
+    else if (sr_c) hipLaunchKernelGGL((quantize_cols_dual<FMT, false, true>), grid, dim3(kThreads), 0, s, k);
+    else hipLaunchKernelGGL((quantize_cols_dual<FMT, false, false>), grid, dim3(kThreads), 0, s, k);
+    return hipGetLastError();
+}
+
 template <int FMT>
 static hipError_t launch_dual_fmt(const DualK& k, dim3 grid, bool sr_r, bool sr_c, hipStream_t s)
 {
@@ -685,6 +852,31 @@ hipError_t launch_quantize_dual(const DualArgs& a, hipStream_t s)
         if (!k.row.scale_in) hipLaunchKernelGGL(write_scalar, dim3(1), dim3(1), 0, s, a.row.tensor_scale, 0.0f);
         if (!k.col.scale_in) hipLaunchKernelGGL(write_scalar, dim3(1), dim3(1), 0, s, a.col.tensor_scale, 0.0f);
         return hipGetLastError();
+    }
+    // register path: 16-byte aligned rows of X, 16 groups per output row
+    // multiple (rows % 256 == 0), 16-byte aligned strided codes and scales
+    const bool regs = k.vec && (a.rows / kGroup) % 16 == 0 && a.rows / kGroup / kGrpTile < 65536 &&
+                      reinterpret_cast<uintptr_t>(a.col.codes) % 16 == 0 &&
+                      reinterpret_cast<uintptr_t>(a.col.scales) % 16 == 0;
+    if (regs) {
+        k.npartials = 0;
+        if (!(k.row.scale_in && k.col.scale_in)) {
+            const int64_t bx = std::min<int64_t>(cdiv(a.cols, kColsPerBlock), kMaxPartials);
+            const int64_t by = std::max<int64_t>(1, std::min<int64_t>(cdiv(a.rows / kGroup, 4), kMaxPartials / bx));
+            k.npartials = (int)(bx * by);
+            hipLaunchKernelGGL(tensor_max_cols_dual, dim3((unsigned)bx, (unsigned)by), dim3(kThreads), 0, s, k,
+                               a.row.partials, a.col.partials);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+        const dim3 grid((unsigned)cdiv(a.cols, kColTile), (unsigned)cdiv(a.rows / kGroup, kGrpTile));
+        const bool sr_r = a.row.flags & IFQ_SR, sr_c = a.col.flags & IFQ_SR;
+        switch (a.fmt) {
+            case IFQ_FMT_IF4: return launch_cols_dual_fmt<IFQ_FMT_IF4>(k, grid, sr_r, sr_c, s);
+            case IFQ_FMT_NVFP4: return launch_cols_dual_fmt<IFQ_FMT_NVFP4>(k, grid, sr_r, sr_c, s);
+            case IFQ_FMT_NVINT4: return launch_cols_dual_fmt<IFQ_FMT_NVINT4>(k, grid, sr_r, sr_c, s);
+            default: return launch_cols_dual_fmt<IFQ_FMT_NVFP4_46>(k, grid, sr_r, sr_c, s);
+        }
     }
     const int64_t tx = cdiv(a.cols, kTC), ty = cdiv(a.rows, kTR);
     k.npartials = 0;

@@ -50,7 +50,8 @@ def _dual(fmt, x_cpu, rf, cf, signs=0x5A3C, rs=11, cs=12, alphas=(None, None)):
 @pytest.mark.parametrize("flags", FLAG_PAIRS)
 def test_dual_matches_oracle(fmt, flags):
     rng = np.random.default_rng(80 + fmt)
-    for shape in [(64, 64), (272, 528), (80, 1040), (1024, 48)]:
+    # register path: rows % 256 == 0 (and 16-byte aligned rows); others: LDS tiles
+    for shape in [(64, 64), (272, 528), (80, 1040), (1024, 48), (256, 64), (512, 1040), (2304, 80)]:
         x = workloads.to_bf16(rng.standard_t(3, shape) * np.exp(rng.normal(0, 1, shape[1])))
         _dual(fmt, x, *flags)
 
@@ -74,13 +75,15 @@ def test_dual_scale_in_and_padded_rows():
     _dual(ops.IF4, x, ops.SCALE_IN, 0, alphas=(0.01, None))
     _dual(ops.NVFP4, x, 0, ops.SCALE_IN | ops.RHT, alphas=(None, 0.002))
     _dual(ops.IF4, x, ops.SCALE_IN, ops.SCALE_IN, alphas=(0.01, 0.003))
-    big = torch.zeros((96, 200), dtype=torch.bfloat16)
-    big[:, :160] = x
-    xs = big.cuda()[:, :160]
-    pr, pc = ops.ifx_quantize_dual(ops.IF4, xs, 0, ops.RHT, 0x0F0F, 0, 0)
-    torch.cuda.synchronize()
-    _check_side(pr, ops.IF4, x, 0, 0x0F0F, 0, None, "padded row")
-    _check_side(pc, ops.IF4, x, ops.RHT | ops.AXIS_STRIDED, 0x0F0F, 0, None, "padded col")
+    for rows in (96, 256):  # LDS tiles, then the register path
+        x = workloads.to_bf16(rng.standard_normal((rows, 160)))
+        big = torch.zeros((rows, 200), dtype=torch.bfloat16)
+        big[:, :160] = x
+        xs = big.cuda()[:, :160]
+        pr, pc = ops.ifx_quantize_dual(ops.IF4, xs, ops.RHT, ops.RHT | ops.SR, 0x0F0F, 0, 4)
+        torch.cuda.synchronize()
+        _check_side(pr, ops.IF4, x, ops.RHT, 0x0F0F, 0, None, f"padded row {rows}")
+        _check_side(pc, ops.IF4, x, ops.RHT | ops.SR | ops.AXIS_STRIDED, 0x0F0F, 4, None, f"padded col {rows}")
 
 
 def test_dual_zero_and_empty():
