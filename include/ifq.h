@@ -159,10 +159,13 @@ int ifx_quantize(int format, const void* x, int64_t rows, int64_t cols, int64_t 
 size_t ifq_quantize_workspace_bytes(int format, int64_t rows, int64_t cols, uint32_t flags);
 
 /* ------------------------------------------------------- dual quantize --
- * Both packed layouts of one bf16 matrix X from a single read of it: the
- * row-wise form (groups along cols: codes [rows, cols*b/8], scales
- * [rows, cols/16]) and the strided form (groups along rows, describing X^T:
- * codes [cols, rows*b/8], scales [cols, rows/16]).  A linear layer's
+ * Both packed layouts of one bf16 matrix X: the row-wise form (groups along
+ * cols: codes [rows, cols*b/8], scales [rows, cols/16]) and the strided form
+ * (groups along rows, describing X^T: codes [cols, rows*b/8], scales
+ * [cols, rows/16]).  One pass reads X once for both tensor maxima; the
+ * quantize pass reads it once more for both layouts when neither side uses
+ * IFQ_SR, and once per layout otherwise (stochastic rounding makes that pass
+ * arithmetic-bound, where separate kernels are faster).  A linear layer's
  * training step needs X, W and dY both ways (Sec. 4.1: the forward GEMM, the
  * activation gradient dX = dY W and the weight gradient dW = dY^T X contract
  * over different axes); the results are bit-identical to

@@ -712,10 +712,11 @@ __global__ __launch_bounds__(kThreads) void tensor_max_cols_dual(DualK a, float*
     }
 }
 
-// Pass 2: quantize_cols' tile (64 columns x 2048 rows, strided output staged
-// in LDS and written as whole lines) plus the row-wise groups of the same
-// registers, stored directly (8 code bytes and one scale byte per group;
-// the four groups of a lane quad-row are contiguous).
+// Pass 2 with round-to-nearest on both sides: quantize_cols' tile (64
+// columns x 2048 rows, strided output staged in LDS and written as whole
+// lines) plus the row-wise groups of the same registers, stored directly
+// (8 code bytes and one scale byte per group; the four groups of a pair row
+// are contiguous).
 template <int FMT, bool SR_ROW, bool SR_COL>
 __global__ __launch_bounds__(kThreads) void quantize_cols_dual(DualK a)
 {
@@ -794,13 +795,11 @@ __global__ __launch_bounds__(kThreads) void quantize_cols_dual(DualK a)
     }
 }
 
+// Round-to-nearest on both sides only (SR sides take the single-layout kernels).
 template <int FMT>
-static hipError_t launch_cols_dual_fmt(const DualK& k, dim3 grid, bool sr_r, bool sr_c, hipStream_t s)
+static hipError_t launch_cols_dual_fmt(const DualK& k, dim3 grid, hipStream_t s)
 {
-    if (sr_r && sr_c) hipLaunchKernelGGL((quantize_cols_dual<FMT, true, true>), grid, dim3(kThreads), 0, s, k);
-    else if (sr_r) hipLaunchKernelGGL((quantize_cols_dual<FMT, true, false>), grid, dim3(kThreads), 0, s, k);
-    else if (sr_c) hipLaunchKernelGGL((quantize_cols_dual<FMT, false, true>), grid, dim3(kThreads), 0, s, k);
-    else hipLaunchKernelGGL((quantize_cols_dual<FMT, false, false>), grid, dim3(kThreads), 0, s, k);
+    hipLaunchKernelGGL((quantize_cols_dual<FMT, false, false>), grid, dim3(kThreads), 0, s, k);
     return hipGetLastError();
 }
 
@@ -869,13 +868,48 @@ hipError_t launch_quantize_dual(const DualArgs& a, hipStream_t s)
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }
-        const dim3 grid((unsigned)cdiv(a.cols, kColTile), (unsigned)cdiv(a.rows / kGroup, kGrpTile));
         const bool sr_r = a.row.flags & IFQ_SR, sr_c = a.col.flags & IFQ_SR;
+        if (sr_r || sr_c) {
+            // Stochastic rounding makes the quantize pass VALU-bound with
+            // long dependent chains: one fused kernel (about 250 VGPRs, one
+            // wavefront per SIMD) loses to the single-layout kernels, which
+            // run at higher occupancy; reading X twice costs nothing there.
+            // Both take their alpha from the fused maxima above.
+            QuantArgs qr{a.fmt, a.x, a.rows, a.cols, a.ld, a.row.flags, a.signs, a.row.seed, a.row.codes,
+                         a.row.scales, a.row.tensor_scale, a.row.partials};
+            QuantArgs qc{a.fmt, a.x, a.rows, a.cols, a.ld, a.col.flags | IFQ_AXIS_STRIDED, a.signs, a.col.seed,
+                         a.col.codes, a.col.scales, a.col.tensor_scale, a.col.partials};
+            hipError_t e = hipSuccess;
+            switch (a.fmt) {
+                case IFQ_FMT_IF4:
+                    e = dispatch_fmt<IFQ_FMT_IF4>(qr, s, k.npartials, k.row.scale_max, k.row.denom_alpha);
+                    if (e == hipSuccess)
+                        e = dispatch_fmt<IFQ_FMT_IF4>(qc, s, k.npartials, k.col.scale_max, k.col.denom_alpha);
+                    break;
+                case IFQ_FMT_NVFP4:
+                    e = dispatch_fmt<IFQ_FMT_NVFP4>(qr, s, k.npartials, k.row.scale_max, k.row.denom_alpha);
+                    if (e == hipSuccess)
+                        e = dispatch_fmt<IFQ_FMT_NVFP4>(qc, s, k.npartials, k.col.scale_max, k.col.denom_alpha);
+                    break;
+                case IFQ_FMT_NVINT4:
+                    e = dispatch_fmt<IFQ_FMT_NVINT4>(qr, s, k.npartials, k.row.scale_max, k.row.denom_alpha);
+                    if (e == hipSuccess)
+                        e = dispatch_fmt<IFQ_FMT_NVINT4>(qc, s, k.npartials, k.col.scale_max, k.col.denom_alpha);
+                    break;
+                default:
+                    e = dispatch_fmt<IFQ_FMT_NVFP4_46>(qr, s, k.npartials, k.row.scale_max, k.row.denom_alpha);
+                    if (e == hipSuccess)
+                        e = dispatch_fmt<IFQ_FMT_NVFP4_46>(qc, s, k.npartials, k.col.scale_max, k.col.denom_alpha);
+                    break;
+            }
+            return e;
+        }
+        const dim3 grid((unsigned)cdiv(a.cols, kColTile), (unsigned)cdiv(a.rows / kGroup, kGrpTile));
         switch (a.fmt) {
-            case IFQ_FMT_IF4: return launch_cols_dual_fmt<IFQ_FMT_IF4>(k, grid, sr_r, sr_c, s);
-            case IFQ_FMT_NVFP4: return launch_cols_dual_fmt<IFQ_FMT_NVFP4>(k, grid, sr_r, sr_c, s);
-            case IFQ_FMT_NVINT4: return launch_cols_dual_fmt<IFQ_FMT_NVINT4>(k, grid, sr_r, sr_c, s);
-            default: return launch_cols_dual_fmt<IFQ_FMT_NVFP4_46>(k, grid, sr_r, sr_c, s);
+            case IFQ_FMT_IF4: return launch_cols_dual_fmt<IFQ_FMT_IF4>(k, grid, s);
+            case IFQ_FMT_NVFP4: return launch_cols_dual_fmt<IFQ_FMT_NVFP4>(k, grid, s);
+            case IFQ_FMT_NVINT4: return launch_cols_dual_fmt<IFQ_FMT_NVINT4>(k, grid, s);
+            default: return launch_cols_dual_fmt<IFQ_FMT_NVFP4_46>(k, grid, s);
         }
     }
     const int64_t tx = cdiv(a.cols, kTC), ty = cdiv(a.rows, kTR);
