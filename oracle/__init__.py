@@ -21,12 +21,15 @@ import numpy as np
 from . import build as _build
 
 (FMT_IF4, FMT_NVFP4, FMT_IF3, FMT_IF6_E2M3, FMT_IF6_E3M2, FMT_NVINT4,
- FMT_NVFP4_46) = range(7)
+ FMT_NVFP4_46, FMT_IF4_BS8, FMT_IF3_BS8, FMT_NVFP4_BS8) = range(10)
 FORMATS = {"if4": FMT_IF4, "nvfp4": FMT_NVFP4, "if3": FMT_IF3,
            "if6_e2m3": FMT_IF6_E2M3, "if6_e3m2": FMT_IF6_E3M2, "nvint4": FMT_NVINT4,
-           "nvfp4_46": FMT_NVFP4_46}
+           "nvfp4_46": FMT_NVFP4_46, "if4_bs8": FMT_IF4_BS8, "if3_bs8": FMT_IF3_BS8,
+           "nvfp4_bs8": FMT_NVFP4_BS8}
 BITS = {FMT_IF4: 4, FMT_NVFP4: 4, FMT_IF3: 3, FMT_IF6_E2M3: 6, FMT_IF6_E3M2: 6,
-        FMT_NVINT4: 4, FMT_NVFP4_46: 4}
+        FMT_NVINT4: 4, FMT_NVFP4_46: 4, FMT_IF4_BS8: 4, FMT_IF3_BS8: 3, FMT_NVFP4_BS8: 4}
+# values per group (one scale byte each): block size 8 for the *_BS8 formats (Sec. 6)
+GSIZE = {f: (8 if f in (FMT_IF4_BS8, FMT_IF3_BS8, FMT_NVFP4_BS8) else 16) for f in BITS}
 
 RHT, SR, MARGIN, SCALE_IN, STRIDED, SR_RTN_TYPE = 1, 2, 4, 8, 16, 32
 GROUP = 16
@@ -52,6 +55,8 @@ def lib():
         L.oracle_fp_round_index.restype = C.c_int
         L.oracle_fp_magnitude.argtypes = [C.c_int, C.c_int]
         L.oracle_fp_magnitude.restype = C.c_double
+        L.oracle_group_size.argtypes = [C.c_int]
+        L.oracle_group_size.restype = C.c_int
         L.oracle_fmt_constants.argtypes = [C.c_int, f32p, C.POINTER(C.c_int), f32p, f32p,
                                            C.POINTER(C.c_int)]
         L.oracle_philox4x32_10.argtypes = [u32p, u32p, u32p]
@@ -145,25 +150,37 @@ def rht16(x, signs: int) -> np.ndarray:
 
 # ------------------------------------------------------------ one group --
 
+def group_size(fmt: int) -> int:
+    return lib().oracle_group_size(fmt)
+
+
 def quantize_group(v, alpha: float, fmt: int = FMT_IF4, flags: int = 0, h=None):
-    """Returns (codes[16] uint8, scale byte, E_FP, E_INT) for one group
-    (for 4/6: the errors of the scalings to 6 and to 4 in alpha units)."""
-    vv = np.ascontiguousarray(np.asarray(v, dtype=np.float32))
-    assert vv.shape == (GROUP,)
-    hh = np.zeros(GROUP, dtype=np.uint16) if h is None else \
-        np.ascontiguousarray(np.asarray(h, dtype=np.uint16))
+    """Returns (codes[n] uint8, scale byte, E_FP, E_INT) for one group of
+    n = GSIZE[fmt] values (for 4/6: the errors of the scalings to 6 and to 4
+    in alpha units)."""
+    n = GSIZE[fmt]
+    vv = np.zeros(GROUP, dtype=np.float32)
+    vin = np.asarray(v, dtype=np.float32)
+    assert vin.shape == (n,)
+    vv[:n] = vin
+    hh = np.zeros(GROUP, dtype=np.uint16)
+    if h is not None:
+        hin = np.asarray(h, dtype=np.uint16)
+        hh[: len(hin)] = hin
     codes = np.zeros(GROUP, dtype=np.uint8)
     sb = np.zeros(1, dtype=np.uint8)
     ef, ei = C.c_float(), C.c_float()
     lib().oracle_quantize_group(fmt, _ptr(vv, C.c_float), float(alpha), flags,
                                 _ptr(hh, C.c_uint16), _ptr(codes, C.c_uint8),
                                 _ptr(sb, C.c_uint8), C.byref(ef), C.byref(ei))
-    return codes, int(sb[0]), ef.value, ei.value
+    return codes[:n], int(sb[0]), ef.value, ei.value
 
 
 def pack_group(fmt: int, codes) -> np.ndarray:
-    c = np.ascontiguousarray(np.asarray(codes, dtype=np.uint8))
-    out = np.zeros(2 * BITS[fmt], dtype=np.uint8)
+    c = np.zeros(GROUP, dtype=np.uint8)
+    cin = np.asarray(codes, dtype=np.uint8)
+    c[: len(cin)] = cin
+    out = np.zeros(GSIZE[fmt] * BITS[fmt] // 8, dtype=np.uint8)
     lib().oracle_pack_group(fmt, _ptr(c, C.c_uint8), _ptr(out, C.c_uint8))
     return out
 
@@ -172,14 +189,14 @@ def unpack_group(fmt: int, packed) -> np.ndarray:
     p = np.ascontiguousarray(np.asarray(packed, dtype=np.uint8))
     out = np.zeros(GROUP, dtype=np.uint8)
     lib().oracle_unpack_group(fmt, _ptr(p, C.c_uint8), _ptr(out, C.c_uint8))
-    return out
+    return out[: GSIZE[fmt]]
 
 
 # --------------------------------------------------------- whole tensors --
 
 def codes_shape(fmt: int, rows: int, cols: int, flags: int = 0):
     out_rows, k = (cols, rows) if flags & STRIDED else (rows, cols)
-    return (out_rows, k * BITS[fmt] // 8), (out_rows, k // GROUP)
+    return (out_rows, k * BITS[fmt] // 8), (out_rows, k // GSIZE[fmt])
 
 
 def quantize(x_bf16_bits: np.ndarray, fmt: int = FMT_IF4, flags: int = 0, rht_signs: int = 0,
@@ -215,7 +232,7 @@ def dequantize(codes: np.ndarray, scales: np.ndarray, alpha: float, fmt: int = F
     """fp32 dequantization (q * Delta [* M_FP/M_I] * alpha, in that order)."""
     codes = np.ascontiguousarray(codes, dtype=np.uint8)
     scales = np.ascontiguousarray(scales, dtype=np.uint8)
-    rows, cols = scales.shape[0], scales.shape[1] * GROUP
+    rows, cols = scales.shape[0], scales.shape[1] * GSIZE[fmt]
     if dtype == np.float64:
         out = np.zeros((rows, cols), dtype=np.float64)
         rc = lib().oracle_dequantize_f64(fmt, _ptr(codes, C.c_uint8), _ptr(scales, C.c_uint8),

@@ -1,8 +1,9 @@
 /*
  * ifq_oracle.c -- plain, slow, scalar CPU oracle for the adaptive
  * block-scaled formats of "Adaptive Block-Scaled Data Types"
- * (IF3, IF4, IF6-E2M3, IF6-E3M2) and the comparison formats NVFP4,
- * NVINT4 and NVFP4 with Four Over Six (4/6).
+ * (IF3, IF4, IF6-E2M3, IF6-E3M2, and IF4 / IF3 with block size 8) and the
+ * comparison formats NVFP4 (also with block size 8), NVINT4 and NVFP4 with
+ * Four Over Six (4/6).
  *
  * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
  * call this file; only tests/, the smoke check and the CPU-baseline leg of
@@ -30,6 +31,9 @@
  *   Table 1 MSE and maxima, brute force in exact rationals (nearest codes,
  *   nearest E4M3 scales, the smaller-error scaling), agreement with the
  *   independent numpy implementation, round trips and the 4/6 tie rule.
+ *   Block size 8 (IF4-BS8, IF3-BS8, NVFP4-BS8): Table 6's bits per
+ *   parameter, reduction to the 16-value algorithm with zero padding, brute
+ *   force over tiny groups, lower error than block size 16.
  * The fp32 operation order itself (reciprocal-multiply scaling, the error
  * accumulation order) is not fixed by the paper: parity unpinned beyond the
  * self-consistency of oracle and kernels, as recorded in the design notes.
@@ -49,7 +53,10 @@ enum {
     FMT_IF6_E3M2 = 4,
     FMT_NVINT4 = 5,
     FMT_NVFP4_46 = 6,
-    FMT_COUNT = 7
+    FMT_IF4_BS8 = 7,
+    FMT_IF3_BS8 = 8,
+    FMT_NVFP4_BS8 = 9,
+    FMT_COUNT = 10
 };
 /* element-type rule of a format */
 enum {
@@ -61,12 +68,13 @@ enum {
 /* flag bits */
 enum { F_RHT = 1, F_SR = 2, F_MARGIN = 4, F_SCALE_IN = 8, F_STRIDED = 16, F_SR_RTN_TYPE = 32 };
 
-#define GROUP 16
+#define GROUP 16 /* the largest group; also the RHT block and the K granularity */
 
 typedef struct {
     int bits;          /* bits per stored code */
     int ebits, mbits;  /* FP element: exponent and mantissa field widths */
     int kind;          /* KIND_* */
+    int gsize;         /* values per group (one scale each): 16, or 8 (Sec. 6) */
     int adaptive;      /* kind == KIND_ADAPTIVE */
     float m_scale;     /* M of Eq. 1-2: the element maximum a group is scaled to */
     float alpha_fp8;   /* the E4M3 factor of Eq. 1: 448, or 256 for 4/6 */
@@ -98,6 +106,7 @@ static void init_fmt(fmt_desc* f, int bits, int ebits, int mbits, int kind)
     f->ebits = ebits;
     f->mbits = mbits;
     f->kind = kind;
+    f->gsize = GROUP;
     f->adaptive = kind == KIND_ADAPTIVE;
     f->n_mag = 1 << (bits - 1);
     for (int i = 0; i < f->n_mag; ++i) f->mag[i] = exmy_value(ebits, mbits, i);
@@ -133,6 +142,13 @@ static void ensure_init(void)
     init_fmt(&g_fmt[FMT_IF6_E3M2], 6, 3, 2, KIND_ADAPTIVE);  /* E3M2 / INT6, Table 6 */
     init_fmt(&g_fmt[FMT_NVINT4], 4, 2, 1, KIND_INT);         /* INT4 only, Sec. 2 */
     init_fmt(&g_fmt[FMT_NVFP4_46], 4, 2, 1, KIND_FOUR_SIX);  /* E2M1, max 6 or 4, Sec. 3 */
+    /* block size 8: one scale per 8 values (Sec. 6, Table 6) */
+    init_fmt(&g_fmt[FMT_IF4_BS8], 4, 2, 1, KIND_ADAPTIVE);
+    init_fmt(&g_fmt[FMT_IF3_BS8], 3, 2, 0, KIND_ADAPTIVE);
+    init_fmt(&g_fmt[FMT_NVFP4_BS8], 4, 2, 1, KIND_FP);
+    g_fmt[FMT_IF4_BS8].gsize = 8;
+    g_fmt[FMT_IF3_BS8].gsize = 8;
+    g_fmt[FMT_NVFP4_BS8].gsize = 8;
     g_init = 1;
 }
 
@@ -196,6 +212,12 @@ double oracle_fp_magnitude(int fmt, int idx)
 {
     ensure_init();
     return g_fmt[fmt].mag[idx];
+}
+
+int oracle_group_size(int fmt)
+{
+    ensure_init();
+    return g_fmt[fmt].gsize;
 }
 
 void oracle_fmt_constants(int fmt, float* fp_max, int* int_max, float* c_up, float* k_dn, int* bits)
@@ -303,11 +325,12 @@ float oracle_tensor_scale(int fmt, float amax, uint32_t flags)
 static void candidates(const fmt_desc* f, const float xb[GROUP], int sr, const uint16_t h[GROUP],
                        uint8_t cf[GROUP], uint8_t ci[GROUP], float* e_fp, float* e_int)
 {
+    const int n = f->gsize;
     const int sign_bit = 1 << (f->bits - 1);
     const int code_mask = (1 << f->bits) - 1;
     /* FP candidate (Fig. 3a lines 4-6). */
     float ef = 0.0f;
-    for (int j = 0; j < GROUP; ++j) {
+    for (int j = 0; j < n; ++j) {
         double m = fabs((double)xb[j]);
         int idx;
         if (!sr) {
@@ -335,7 +358,7 @@ static void candidates(const fmt_desc* f, const float xb[GROUP], int sr, const u
     /* INT candidate (Fig. 3a lines 7-9): int(x-bar * M_I/M_FP), clamped to
      * +-M_I, reconstructed as code * M_FP/M_I. */
     float ei = 0.0f;
-    for (int j = 0; j < GROUP; ++j) {
+    for (int j = 0; j < n; ++j) {
         double r;
         if (!sr) {
             /* nearest integer to the exact product, ties to even */
@@ -384,8 +407,9 @@ static void four_six_group(const fmt_desc* f, const float v[GROUP], float alpha,
                            float* e6, float* e4)
 {
     const int sr = (flags & F_SR) != 0;
+    const int n = f->gsize;
     float amax_g = 0.0f;
-    for (int j = 0; j < GROUP; ++j) {
+    for (int j = 0; j < n; ++j) {
         float a = fabsf(v[j]);
         if (a > amax_g) amax_g = a;
     }
@@ -403,7 +427,7 @@ static void four_six_group(const fmt_desc* f, const float v[GROUP], float alpha,
         if (!ok[t]) continue;
         float inv = 1.0f / s;
         float xb[GROUP];
-        for (int j = 0; j < GROUP; ++j) xb[j] = v[j] * inv;
+        for (int j = 0; j < n; ++j) xb[j] = v[j] * inv;
         uint8_t ci[GROUP];
         float ef, ei;
         candidates(f, xb, sr, h, cand[t], ci, &ef, &ei);
@@ -416,16 +440,17 @@ static void four_six_group(const fmt_desc* f, const float v[GROUP], float alpha,
     *e6 = err[0];
     *e4 = err[1];
     if (!ok[1]) {
-        memset(codes, 0, GROUP);
+        memset(codes, 0, (size_t)n);
         *scale = 0;
         return;
     }
     int pick = (ok[0] && !(err[1] < err[0])) ? 0 : 1;
-    memcpy(codes, cand[pick], GROUP);
+    memcpy(codes, cand[pick], (size_t)n);
     *scale = (uint8_t)dcode[pick];
 }
 
-/* One group.  IF formats and NVFP4: Fig. 3a.  NVINT4: the INT candidate
+/* One group of the format's size (v, h and codes hold that many; 16 or 8).
+ * IF formats and NVFP4: Fig. 3a.  NVINT4: the INT candidate
  * alone, scaled to M_I (c_up = 1).  4/6: four_six_group, which reports the
  * two scalings' errors in e_fp (to 6) and e_int (to 4). */
 void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t flags,
@@ -435,6 +460,7 @@ void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t 
     ensure_init();
     const fmt_desc* f = &g_fmt[fmt];
     const int sr = (flags & F_SR) != 0;
+    const int n = f->gsize;
     if (f->kind == KIND_FOUR_SIX) {
         four_six_group(f, v, alpha, flags, h, codes, scale, e_fp, e_int);
         return;
@@ -442,7 +468,7 @@ void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t 
 
     /* Fig. 3a line 1 / Eq. (2): Delta = max|X_g| / (alpha * M). */
     float amax_g = 0.0f;
-    for (int j = 0; j < GROUP; ++j) {
+    for (int j = 0; j < n; ++j) {
         float a = fabsf(v[j]);
         if (a > amax_g) amax_g = a;
     }
@@ -457,7 +483,7 @@ void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t 
      * combined scale is zero or below the smallest normal fp32 stores zeros. */
     float s = alpha * delta;
     if (!(s >= FLT_MIN)) {
-        memset(codes, 0, GROUP);
+        memset(codes, 0, (size_t)n);
         *scale = 0;
         *e_fp = 0.0f;
         *e_int = 0.0f;
@@ -465,7 +491,7 @@ void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t 
     }
     float inv = 1.0f / s;
     float xb[GROUP];
-    for (int j = 0; j < GROUP; ++j) xb[j] = v[j] * inv;
+    for (int j = 0; j < n; ++j) xb[j] = v[j] * inv;
 
     uint8_t cf[GROUP], ci[GROUP];
     float ef, ei;
@@ -484,21 +510,22 @@ void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t 
      * its scale is a plain E4M3 value (bit 7 clear). */
     int use_int = f->adaptive && (sel_i < sel_f);
     if (f->kind == KIND_INT) {
-        memcpy(codes, ci, GROUP);
+        memcpy(codes, ci, (size_t)n);
         *scale = (uint8_t)dcode;
     } else {
-        memcpy(codes, use_int ? ci : cf, GROUP);
+        memcpy(codes, use_int ? ci : cf, (size_t)n);
         *scale = (uint8_t)(dcode | (use_int ? 0x80 : 0));
     }
     *e_fp = sel_f;
     *e_int = sel_i;
 }
 
-/* Dense little-endian bit stream: code j of a group at bits [j*b, j*b+b). */
-static void pack_group(int bits, const uint8_t codes[GROUP], uint8_t* out)
+/* Dense little-endian bit stream: code j of a group at bits [j*b, j*b+b);
+ * a group of n codes fills n*b/8 bytes. */
+static void pack_group(int bits, int n, const uint8_t codes[GROUP], uint8_t* out)
 {
-    memset(out, 0, (size_t)(2 * bits));
-    for (int j = 0; j < GROUP; ++j) {
+    memset(out, 0, (size_t)(n * bits / 8));
+    for (int j = 0; j < n; ++j) {
         for (int t = 0; t < bits; ++t) {
             int bit = j * bits + t;
             if ((codes[j] >> t) & 1) out[bit >> 3] |= (uint8_t)(1u << (bit & 7));
@@ -506,9 +533,9 @@ static void pack_group(int bits, const uint8_t codes[GROUP], uint8_t* out)
     }
 }
 
-static void unpack_group(int bits, const uint8_t* in, uint8_t codes[GROUP])
+static void unpack_group(int bits, int n, const uint8_t* in, uint8_t codes[GROUP])
 {
-    for (int j = 0; j < GROUP; ++j) {
+    for (int j = 0; j < n; ++j) {
         int c = 0;
         for (int t = 0; t < bits; ++t) {
             int bit = j * bits + t;
@@ -521,13 +548,13 @@ static void unpack_group(int bits, const uint8_t* in, uint8_t codes[GROUP])
 void oracle_pack_group(int fmt, const uint8_t codes[GROUP], uint8_t* out)
 {
     ensure_init();
-    pack_group(g_fmt[fmt].bits, codes, out);
+    pack_group(g_fmt[fmt].bits, g_fmt[fmt].gsize, codes, out);
 }
 
 void oracle_unpack_group(int fmt, const uint8_t* in, uint8_t codes[GROUP])
 {
     ensure_init();
-    unpack_group(g_fmt[fmt].bits, in, codes);
+    unpack_group(g_fmt[fmt].bits, g_fmt[fmt].gsize, in, codes);
 }
 
 static float bf16_to_float(uint16_t b)
@@ -553,23 +580,26 @@ int oracle_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int6
     ensure_init();
     if (fmt < 0 || fmt >= FMT_COUNT) return -1;
     const fmt_desc* f = &g_fmt[fmt];
+    const int n = f->gsize;
     const int strided = (flags & F_STRIDED) != 0;
     const int64_t out_rows = strided ? cols : rows;   /* logical rows of the output */
     const int64_t out_k = strided ? rows : cols;      /* grouped (K) dimension */
     if (out_k % GROUP) return -1;
-    const int64_t gpr = out_k / GROUP;
+    const int64_t bpr = out_k / GROUP;                /* 16-value blocks (RHT blocks) per row */
+    const int64_t gpr = out_k / n;                    /* groups (scale bytes) per row */
     const int64_t ngroups = out_rows * gpr;
     const int64_t code_bytes_row = out_k * f->bits / 8;
 
-    /* Gather each group (and transform it) into a dense fp32 buffer. */
-    float* vbuf = (float*)malloc((size_t)(ngroups > 0 ? ngroups : 1) * GROUP * sizeof(float));
+    /* Gather each 16-value block (and transform it) into a dense fp32
+     * buffer in output order. */
+    float* vbuf = (float*)malloc((size_t)(out_rows * out_k > 0 ? out_rows * out_k : 1) * sizeof(float));
     if (!vbuf) return -1;
     float amax = 0.0f;
     for (int64_t o = 0; o < out_rows; ++o) {
-        for (int64_t g = 0; g < gpr; ++g) {
+        for (int64_t b = 0; b < bpr; ++b) {
             float xg[GROUP];
             for (int j = 0; j < GROUP; ++j) {
-                int64_t k = g * GROUP + j;
+                int64_t k = b * GROUP + j;
                 int64_t r = strided ? k : o, c = strided ? o : k;
                 xg[j] = bf16_to_float(x[r * ld_x + c]);
                 if (!isfinite(xg[j])) {
@@ -577,7 +607,7 @@ int oracle_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int6
                     return -1;
                 }
             }
-            float* v = vbuf + (o * gpr + g) * GROUP;
+            float* v = vbuf + o * out_k + b * GROUP;
             if (flags & F_RHT)
                 oracle_rht16(xg, rht_signs, v);
             else
@@ -593,6 +623,8 @@ int oracle_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int6
     float alpha = (flags & F_SCALE_IN) ? *tensor_scale : oracle_tensor_scale(fmt, amax, flags);
     if (!(flags & F_SCALE_IN)) *tensor_scale = alpha;
 
+    /* Group gi (the index of its scale byte) draws its SR numbers from the
+     * Philox blocks of counter gi; a group of 8 uses the first 8. */
     for (int64_t o = 0; o < out_rows; ++o) {
         for (int64_t g = 0; g < gpr; ++g) {
             int64_t gi = o * gpr + g;
@@ -603,11 +635,12 @@ int oracle_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int6
                 memset(h, 0, sizeof(h));
             uint8_t cg[GROUP], sb;
             float ef, ei;
-            oracle_quantize_group(fmt, vbuf + gi * GROUP, alpha, flags, h, cg, &sb, &ef, &ei);
+            oracle_quantize_group(fmt, vbuf + o * out_k + g * n, alpha, flags, h, cg, &sb, &ef, &ei);
             scales[gi] = sb;
-            pack_group(f->bits, cg, codes + o * code_bytes_row + g * 2 * f->bits);
+            pack_group(f->bits, n, cg, codes + o * code_bytes_row + g * n * f->bits / 8);
         }
     }
+    (void)ngroups;
     free(vbuf);
     return 0;
 }
@@ -643,15 +676,16 @@ int oracle_dequantize(int fmt, const uint8_t* codes, const uint8_t* scales, floa
     ensure_init();
     if (fmt < 0 || fmt >= FMT_COUNT || cols % GROUP) return -1;
     const fmt_desc* f = &g_fmt[fmt];
-    const int64_t gpr = cols / GROUP;
+    const int n = f->gsize;
+    const int64_t gpr = cols / n;
     const int64_t code_bytes_row = cols * f->bits / 8;
     for (int64_t r = 0; r < rows; ++r) {
         for (int64_t g = 0; g < gpr; ++g) {
             uint8_t cg[GROUP];
-            unpack_group(f->bits, codes + r * code_bytes_row + g * 2 * f->bits, cg);
+            unpack_group(f->bits, n, codes + r * code_bytes_row + g * n * f->bits / 8, cg);
             uint8_t sb = scales[r * gpr + g];
-            for (int j = 0; j < GROUP; ++j)
-                out[r * cols + g * GROUP + j] = dequant_element(f, cg[j], sb, alpha);
+            for (int j = 0; j < n; ++j)
+                out[r * cols + g * n + j] = dequant_element(f, cg[j], sb, alpha);
         }
     }
     return 0;
@@ -666,17 +700,18 @@ int oracle_dequantize_f64(int fmt, const uint8_t* codes, const uint8_t* scales, 
     ensure_init();
     if (fmt < 0 || fmt >= FMT_COUNT || cols % GROUP) return -1;
     const fmt_desc* f = &g_fmt[fmt];
-    const int64_t gpr = cols / GROUP;
+    const int n = f->gsize;
+    const int64_t gpr = cols / n;
     const int64_t code_bytes_row = cols * f->bits / 8;
     const double kdn = f->kind == KIND_INT ? 1.0 : (double)f->fp_max / (double)f->int_max;
     for (int64_t r = 0; r < rows; ++r) {
         for (int64_t g = 0; g < gpr; ++g) {
             uint8_t cg[GROUP];
-            unpack_group(f->bits, codes + r * code_bytes_row + g * 2 * f->bits, cg);
+            unpack_group(f->bits, n, codes + r * code_bytes_row + g * n * f->bits / 8, cg);
             uint8_t sb = scales[r * gpr + g];
             double delta = oracle_e4m3_value(sb & 0x7F);
             int is_int = f->kind == KIND_INT || (f->adaptive && (sb & 0x80));
-            for (int j = 0; j < GROUP; ++j) {
+            for (int j = 0; j < n; ++j) {
                 double q;
                 if (is_int) {
                     int c = cg[j];
@@ -686,7 +721,7 @@ int oracle_dequantize_f64(int fmt, const uint8_t* codes, const uint8_t* scales, 
                     q = f->mag[cg[j] & (f->n_mag - 1)];
                     if (cg[j] & f->n_mag) q = -q;
                 }
-                out[r * cols + g * GROUP + j] = (double)alpha * delta * q;
+                out[r * cols + g * n + j] = (double)alpha * delta * q;
             }
         }
     }
