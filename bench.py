@@ -41,7 +41,7 @@ def parse():
                    help="read rocprofv3 FETCH_SIZE/WRITE_SIZE counter CSVs of a --mode step run "
                         "(DIR/pmc_FETCH_SIZE, DIR/pmc_WRITE_SIZE) and write profiles/hbm_traffic.json")
     p.add_argument("--format", choices=["if4", "nvfp4", "if3", "if6_e2m3", "if6_e3m2", "nvint4",
-                                        "nvfp4_46"], default="if4",
+                                        "nvfp4_46", "if4_bs8", "if3_bs8", "nvfp4_bs8"], default="if4",
                    help="format of the --mode step run")
     p.add_argument("--small", action="store_true", help="1/8-size shapes (quick checks)")
     p.add_argument("--mode", choices=["full", "step", "copy", "wgrad", "bitwidth", "dual"], default="full",
@@ -93,7 +93,7 @@ def main():
 
     def alloc(fmt, rows, cols):
         return ops.Packed(fmt, torch.empty((rows, cols * ops.BITS[fmt] // 8), dtype=torch.uint8, device=dev),
-                          torch.empty((rows, cols // 16), dtype=torch.uint8, device=dev),
+                          torch.empty((rows, cols // ops.GSIZE[fmt]), dtype=torch.uint8, device=dev),
                           torch.empty(1, dtype=torch.float32, device=dev), rows, cols)
 
     ws = torch.empty(4096, dtype=torch.uint8, device=dev)

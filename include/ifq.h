@@ -27,6 +27,12 @@
  *   IF6_E3M2    6     E3M2           28     INT6   31    (Sec. 5.1, Table 6)
  *   NVINT4      4     --             --     INT4   7     (INT only, Sec. 2)
  *   NVFP4_46    4     E2M1           6      --     --    (FP only, 4/6, Sec. 3)
+ *   IF4_BS8, IF3_BS8, NVFP4_BS8: IF4, IF3 and NVFP4 with one scale per 8
+ *                values instead of 16 (Sec. 6, Table 6: 5.0, 4.0, 5.0 bits per
+ *                parameter).  Scales are [R, K/8]; the two scale bytes of
+ *                values 16i .. 16i+15 are adjacent, and their codes fill the
+ *                same 2b bytes as one block-16 group.  SR draws of group g
+ *                (its scale byte index) are the first 8 of counter g.
  *
  * NVINT4 groups are scaled straight to M_I = 7 (Delta = max|X_g| / (alpha * 7),
  * alpha = max|X| / (7 * 448), Table 1), decode as q * Delta * alpha, and keep
@@ -83,7 +89,10 @@ typedef enum ifq_format {
     IFQ_FMT_IF6_E2M3 = 3,
     IFQ_FMT_IF6_E3M2 = 4,
     IFQ_FMT_NVINT4 = 5,
-    IFQ_FMT_NVFP4_46 = 6
+    IFQ_FMT_NVFP4_46 = 6,
+    IFQ_FMT_IF4_BS8 = 7,
+    IFQ_FMT_IF3_BS8 = 8,
+    IFQ_FMT_NVFP4_BS8 = 9
 } ifq_format;
 
 typedef enum ifq_dtype { IFQ_F32 = 0, IFQ_BF16 = 1 } ifq_dtype;
@@ -148,8 +157,8 @@ int nvfp4_quantize(const void* x, int64_t rows, int64_t cols, int64_t ld_x, uint
                    uint32_t rht_signs, uint64_t seed, uint8_t* codes, uint8_t* scales,
                    float* tensor_scale, void* workspace, size_t workspace_bytes, void* stream);
 
-/* Any format (IF3 and IF6 of Sec. 5.1, NVINT4 and NVFP4_46 included); same
- * arguments. */
+/* Any format (IF3 and IF6 of Sec. 5.1, NVINT4, NVFP4_46 and the block-size-8
+ * formats included); same arguments, scales [R, K / ifq_group_size()]. */
 int ifx_quantize(int format, const void* x, int64_t rows, int64_t cols, int64_t ld_x,
                  uint32_t flags, uint32_t rht_signs, uint64_t seed, uint8_t* codes,
                  uint8_t* scales, float* tensor_scale, void* workspace, size_t workspace_bytes,
@@ -249,6 +258,8 @@ int ifx_gemm(int format, const uint8_t* a_codes, const uint8_t* a_scales,
 /* ---------------------------------------------------------- host helpers */
 size_t ifq_codes_bytes(int format, int64_t rows, int64_t cols); /* rows * cols * bits / 8 */
 size_t ifq_scales_bytes(int64_t rows, int64_t cols);            /* rows * cols / 16 */
+int ifq_group_size(int format);  /* values per scale byte: 16, or 8 for the *_BS8 formats;
+                                    0 for an unknown format */
 const char* ifq_status_string(int status);
 int ifq_abi_version(void);
 

@@ -11,12 +11,13 @@ constexpr uint32_t kKnownFlags =
     IFQ_RHT | IFQ_SR | IFQ_MARGIN_16_17 | IFQ_SCALE_IN | IFQ_AXIS_STRIDED | IFQ_SR_RTN_TYPE;
 constexpr int64_t kMaxElems = int64_t(1) << 40;  // keeps every index product in int64
 
-bool valid_format(int f) { return f >= IFQ_FMT_IF4 && f <= IFQ_FMT_NVFP4_46; }
+bool valid_format(int f) { return f >= IFQ_FMT_IF4 && f <= IFQ_FMT_NVFP4_BS8; }
 
 int bits_of(int f)
 {
     switch (f) {
-        case IFQ_FMT_IF3: return 3;
+        case IFQ_FMT_IF3:
+        case IFQ_FMT_IF3_BS8: return 3;
         case IFQ_FMT_IF6_E2M3:
         case IFQ_FMT_IF6_E3M2: return 6;
         default: return 4;
@@ -261,6 +262,12 @@ int ifx_quantize_dual(int format, const void* x, int64_t rows, int64_t cols, int
     a.row = {row_flags, row_seed, row_codes, row_scales, row_tensor_scale, ws};
     a.col = {col_flags, col_seed, col_codes, col_scales, col_tensor_scale, ws ? ws + ifq::kMaxPartials : nullptr};
     return ifq::launch_quantize_dual(a, static_cast<hipStream_t>(stream)) == hipSuccess ? IFQ_OK : IFQ_EHIP;
+}
+
+int ifq_group_size(int format)
+{
+    if (!valid_format(format)) return 0;
+    return (format == IFQ_FMT_IF4_BS8 || format == IFQ_FMT_IF3_BS8 || format == IFQ_FMT_NVFP4_BS8) ? 8 : 16;
 }
 
 size_t ifq_codes_bytes(int format, int64_t rows, int64_t cols)

@@ -21,12 +21,15 @@ __global__ __launch_bounds__(kDqThreads) void dequantize_groups(const uint8_t* _
     for (int64_t g = (int64_t)blockIdx.x * kDqThreads + threadIdx.x; g < ngroups; g += stride) {
         uint32_t c[kGroup];
         load_unpack16<F::BITS>(codes + g * (2 * F::BITS), c);
-        const uint32_t sb = scales[g];
-        const float delta = e4m3_value(sb);
-        const bool is_int = F::KIND == kKindInt || (F::ADAPTIVE && (sb & 0x80u));
+        // block size 8: the second half of the 16 values has its own scale byte
+        const uint32_t sb0 = F::G == 8 ? scales[2 * g] : scales[g];
+        const uint32_t sb1 = F::G == 8 ? scales[2 * g + 1] : sb0;
         float o[kGroup];
 #pragma unroll
         for (int j = 0; j < kGroup; ++j) {
+            const uint32_t sb = j < 8 ? sb0 : sb1;
+            const float delta = e4m3_value(sb);
+            const bool is_int = F::KIND == kKindInt || (F::ADAPTIVE && (sb & 0x80u));
             float q;
             if (is_int) {
                 q = (float)((int)(c[j] << (32 - F::BITS)) >> (32 - F::BITS));
@@ -84,6 +87,9 @@ hipError_t launch_dequantize(int fmt, const uint8_t* codes, const uint8_t* scale
         case IFQ_FMT_NVINT4: return launch_dq<IFQ_FMT_NVINT4>(codes, scales, ts, ngroups, out, bf16, s);
         // 4/6 data decode exactly like NVFP4
         case IFQ_FMT_NVFP4_46: return launch_dq<IFQ_FMT_NVFP4>(codes, scales, ts, ngroups, out, bf16, s);
+        case IFQ_FMT_IF4_BS8: return launch_dq<IFQ_FMT_IF4_BS8>(codes, scales, ts, ngroups, out, bf16, s);
+        case IFQ_FMT_IF3_BS8: return launch_dq<IFQ_FMT_IF3_BS8>(codes, scales, ts, ngroups, out, bf16, s);
+        case IFQ_FMT_NVFP4_BS8: return launch_dq<IFQ_FMT_NVFP4_BS8>(codes, scales, ts, ngroups, out, bf16, s);
         default: return hipErrorInvalidValue;
     }
 }

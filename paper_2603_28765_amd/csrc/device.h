@@ -31,40 +31,54 @@ enum FmtKind { kKindFP = 0, kKindAdaptive = 1, kKindInt = 2, kKindFourSix = 3 };
 
 template <int FMT> struct Fmt;
 template <> struct Fmt<IFQ_FMT_IF4> {
-    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7, KIND = kKindAdaptive;
+    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7, KIND = kKindAdaptive, G = 16;
     static constexpr bool ADAPTIVE = true;
     static constexpr float FP_MAX = 6.0f, M = 6.0f, A8 = 448.0f;
 };
 template <> struct Fmt<IFQ_FMT_NVFP4> {
-    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7, KIND = kKindFP;
+    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7, KIND = kKindFP, G = 16;
     static constexpr bool ADAPTIVE = false;
     static constexpr float FP_MAX = 6.0f, M = 6.0f, A8 = 448.0f;
 };
 template <> struct Fmt<IFQ_FMT_IF3> {
-    static constexpr int BITS = 3, EB = 2, MB = 0, IMAX = 3, KIND = kKindAdaptive;
+    static constexpr int BITS = 3, EB = 2, MB = 0, IMAX = 3, KIND = kKindAdaptive, G = 16;
     static constexpr bool ADAPTIVE = true;
     static constexpr float FP_MAX = 4.0f, M = 4.0f, A8 = 448.0f;
 };
 template <> struct Fmt<IFQ_FMT_IF6_E2M3> {
-    static constexpr int BITS = 6, EB = 2, MB = 3, IMAX = 31, KIND = kKindAdaptive;
+    static constexpr int BITS = 6, EB = 2, MB = 3, IMAX = 31, KIND = kKindAdaptive, G = 16;
     static constexpr bool ADAPTIVE = true;
     static constexpr float FP_MAX = 7.5f, M = 7.5f, A8 = 448.0f;
 };
 template <> struct Fmt<IFQ_FMT_IF6_E3M2> {
-    static constexpr int BITS = 6, EB = 3, MB = 2, IMAX = 31, KIND = kKindAdaptive;
+    static constexpr int BITS = 6, EB = 3, MB = 2, IMAX = 31, KIND = kKindAdaptive, G = 16;
     static constexpr bool ADAPTIVE = true;
     static constexpr float FP_MAX = 28.0f, M = 28.0f, A8 = 448.0f;
 };
 template <> struct Fmt<IFQ_FMT_NVINT4> {
-    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7, KIND = kKindInt;
+    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7, KIND = kKindInt, G = 16;
     static constexpr bool ADAPTIVE = false;
     static constexpr float FP_MAX = 6.0f, M = 7.0f, A8 = 448.0f;
 };
 template <> struct Fmt<IFQ_FMT_NVFP4_46> {
-    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7, KIND = kKindFourSix;
+    static constexpr int BITS = 4, EB = 2, MB = 1, IMAX = 7, KIND = kKindFourSix, G = 16;
     static constexpr bool ADAPTIVE = false;
     static constexpr float FP_MAX = 6.0f, M = 6.0f, A8 = 256.0f;
 };
+
+// Block size 8 (Sec. 6, Table 6): the same elements with one scale per 8
+// values (G = 8).  A quantizer lane still owns 16 values -- two groups, two
+// adjacent scale bytes -- and the code bit stream of 16 values is unchanged.
+template <> struct Fmt<IFQ_FMT_IF4_BS8> : Fmt<IFQ_FMT_IF4> { static constexpr int G = 8; };
+template <> struct Fmt<IFQ_FMT_IF3_BS8> : Fmt<IFQ_FMT_IF3> { static constexpr int G = 8; };
+template <> struct Fmt<IFQ_FMT_NVFP4_BS8> : Fmt<IFQ_FMT_NVFP4> { static constexpr int G = 8; };
+
+// The 16-value format whose element arithmetic a format uses (itself, or
+// the block-16 counterpart of a block-8 format).
+template <int FMT> struct Base { static constexpr int F = FMT; };
+template <> struct Base<IFQ_FMT_IF4_BS8> { static constexpr int F = IFQ_FMT_IF4; };
+template <> struct Base<IFQ_FMT_IF3_BS8> { static constexpr int F = IFQ_FMT_IF3; };
+template <> struct Base<IFQ_FMT_NVFP4_BS8> { static constexpr int F = IFQ_FMT_NVFP4; };
 
 template <int FMT> struct FmtDerived {
     using F = Fmt<FMT>;
@@ -144,6 +158,15 @@ __device__ __forceinline__ void sr_words(uint64_t seed, uint64_t gi, uint32_t (&
     uint4 b = philox4x32_10(make_uint4((uint32_t)gi, (uint32_t)(gi >> 32), 1u, 0u), k0, k1);
     w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
     w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+}
+
+// The first Philox block of group gi's counter (8 draws: a group of 8).
+__device__ __forceinline__ void sr_words_first(uint64_t seed, uint64_t gi, uint32_t (&w)[8])
+{
+    uint4 a = philox4x32_10(make_uint4((uint32_t)gi, (uint32_t)(gi >> 32), 0u, 0u), (uint32_t)seed,
+                            (uint32_t)(seed >> 32));
+    w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
+    w[4] = 0u; w[5] = 0u; w[6] = 0u; w[7] = 0u;
 }
 
 __device__ __forceinline__ float sr_uniform(const uint32_t (&w)[8], int j)
@@ -235,30 +258,30 @@ template <int FMT> __device__ __forceinline__ uint32_t fp_sr_index(float m, floa
 // in element order with fused multiply-adds.  RTN_TYPE (with SR): the type is
 // decided on the round-to-nearest candidates' errors and the stored codes
 // are the stochastic candidate of that type (the App. B alternative).
-template <int FMT, bool SR, bool RTN_TYPE = false>
-__device__ __forceinline__ uint32_t quantize_group(const float (&v)[kGroup], float alpha,
+template <int FMT, bool SR, bool RTN_TYPE = false, int N = kGroup>
+__device__ __forceinline__ uint32_t quantize_group(const float (&v)[N], float alpha,
                                                    float denom, const uint32_t (&w)[8],
-                                                   uint32_t (&code)[kGroup])
+                                                   uint32_t (&code)[N])
 {
     using F = Fmt<FMT>;
     using D = FmtDerived<FMT>;
     float amax = 0.0f;
 #pragma unroll
-    for (int j = 0; j < kGroup; ++j) amax = fmaxf(amax, fabsf(v[j]));
+    for (int j = 0; j < N; ++j) amax = fmaxf(amax, fabsf(v[j]));
     uint32_t dcode = e4m3_encode(amax / denom);
     float s = alpha * e4m3_value(dcode);
     if (!(s >= 1.17549435e-38f)) {
 #pragma unroll
-        for (int j = 0; j < kGroup; ++j) code[j] = 0;
+        for (int j = 0; j < N; ++j) code[j] = 0;
         return 0;
     }
     float inv = 1.0f / s;
 
     float ef = 0.0f, ei = 0.0f;
     float rf = 0.0f, ri = 0.0f;  // RTN errors (RTN_TYPE only)
-    uint32_t cf[kGroup], ci[kGroup];
+    uint32_t cf[N], ci[N];
 #pragma unroll
-    for (int j = 0; j < kGroup; ++j) {
+    for (int j = 0; j < N; ++j) {
         float xb = v[j] * inv;
         if constexpr (SR && RTN_TYPE && F::ADAPTIVE) {
             const float m0 = fabsf(xb);
@@ -309,7 +332,7 @@ __device__ __forceinline__ uint32_t quantize_group(const float (&v)[kGroup], flo
     else
         use_int = F::ADAPTIVE && (ei < ef);
 #pragma unroll
-    for (int j = 0; j < kGroup; ++j) code[j] = use_int ? ci[j] : cf[j];
+    for (int j = 0; j < N; ++j) code[j] = use_int ? ci[j] : cf[j];
     return dcode | (use_int ? 0x80u : 0u);
 }
 
@@ -640,8 +663,9 @@ template <int BITS> __device__ __forceinline__ void load_unpack16(const uint8_t*
 }
 
 // ------------------------------------------------------ group dispatcher
-// Quantize one (already transformed) group of any format: returns the scale
-// byte and the packed codes.  denom = fp32(alpha * M) with M the format's
+// Quantize one (already transformed) block of 16 values of any format:
+// returns its scale byte (two, low byte first, for block size 8) and the
+// packed codes.  denom = fp32(alpha * M) with M the format's
 // group target (with the margin when it is on); gi is the group's index for
 // the SR draws.
 template <int FMT, bool SR>
@@ -651,9 +675,32 @@ __device__ __forceinline__ uint32_t quantize_any(const float (&v)[kGroup], float
 {
     using F = Fmt<FMT>;
     constexpr int BITS = F::BITS;
+    const bool rtn_type = (qflags & kQSrRtnType) != 0;
+    if constexpr (F::G == 8) {
+        // two groups of 8 (scale bytes 2 gi and 2 gi + 1, which are also their
+        // SR counters); returns both scale bytes, low byte first
+        constexpr int B = Base<FMT>::F;
+        uint32_t c[kGroup];
+        uint32_t sb = 0;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            float vh[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) vh[j] = v[8 * h + j];
+            uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+            if constexpr (SR) sr_words_first(seed, 2 * (uint64_t)gi + h, w);
+            uint32_t ch[8];
+            const uint32_t b = (SR && rtn_type) ? quantize_group<B, SR, true, 8>(vh, alpha, denom, w, ch)
+                                                : quantize_group<B, SR, false, 8>(vh, alpha, denom, w, ch);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) c[8 * h + j] = ch[j];
+            sb |= b << (8 * h);
+        }
+        out = pack16<BITS>(c);
+        return sb;
+    }
     uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if constexpr (SR) sr_words(seed, (uint64_t)gi, w);
-    const bool rtn_type = (qflags & kQSrRtnType) != 0;
     if constexpr (F::KIND == kKindFourSix) {
         const float denom4 = alpha * ((qflags & kQMargin) ? kFourTargetMargin : kFourTarget);
         if constexpr (SR) {

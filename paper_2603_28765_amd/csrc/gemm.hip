@@ -33,6 +33,8 @@
 // two K steps ahead.  LDS rows hold 64 halves padded to 144 bytes, so the 16
 // lanes of a 128-bit access phase touch disjoint banks and every address is a
 // per-lane base plus an immediate.
+#include <type_traits>
+
 #include "device.h"
 #include "launch.h"
 
@@ -71,6 +73,10 @@ template <> struct Fold<IFQ_FMT_IF6_E2M3> {
 template <> struct Fold<IFQ_FMT_IF6_E3M2> {
     static constexpr float FP = 31.0f / 8.0f, INT = 28.0f / 8.0f, EPI = 64.0f / 961.0f;
 };
+// block size 8: the block-16 format's folds, applied per 8 values
+template <> struct Fold<IFQ_FMT_IF4_BS8> : Fold<IFQ_FMT_IF4> {};
+template <> struct Fold<IFQ_FMT_IF3_BS8> : Fold<IFQ_FMT_IF3> {};
+template <> struct Fold<IFQ_FMT_NVFP4_BS8> : Fold<IFQ_FMT_NVFP4> {};
 
 __device__ __forceinline__ uint32_t h2_as_u32(half2v h) { return __builtin_bit_cast(uint32_t, h); }
 __device__ __forceinline__ half2v u32_as_h2(uint32_t u) { return __builtin_bit_cast(half2v, u); }
@@ -158,14 +164,16 @@ __device__ __forceinline__ void decode_word(uint32_t w, bool is_int, uint32_t k2
 }
 
 // Sixteen three-bit IF3 codes (48 bits) -> 8 FP16 operand pairs: 3 q (FP) or
-// 4 q (INT), times Delta (at most 6 significant bits, exact).
-__device__ __forceinline__ void decode_if3_group(uint64_t bitsv, bool is_int, uint32_t k2,
-                                                 uint32_t (&out)[8])
+// 4 q (INT), times Delta (at most 6 significant bits, exact).  Codes 0-7 use
+// (is_int0, k20), codes 8-15 (is_int1, k21): the same for block size 16.
+__device__ __forceinline__ void decode_if3_group(uint64_t bitsv, bool is_int0, uint32_t k20, bool is_int1,
+                                                 uint32_t k21, uint32_t (&out)[8])
 {
     using D = FmtDerived<IFQ_FMT_IF3>;
-    const half2v K = u32_as_h2(k2);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
+        const bool is_int = i < 4 ? is_int0 : is_int1;
+        const half2v K = u32_as_h2(i < 4 ? k20 : k21);
         half2v hv;
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
@@ -208,10 +216,14 @@ __device__ __forceinline__ void decode_if6_group(const uint32_t* w, uint32_t sby
 // ------------------------------------------------------------ raw chunks
 // A: one lane's 32 k-values of one row for one step (2 groups);
 // B: one thread's 64 k-values of one row (4 groups).  IF3 keeps 6-byte groups.
-template <int FMT> struct RawA { uint32_t w[4]; uint32_t sb; };
+// Scale bytes of a chunk: one per 16 values, two for block size 8.
+template <int FMT> using ScaleBits = typename std::conditional<Fmt<FMT>::G == 8, uint64_t, uint32_t>::type;
+template <int FMT> struct RawA { uint32_t w[4]; ScaleBits<FMT> sb; };
 template <> struct RawA<IFQ_FMT_IF3> { uint16_t h[6]; uint32_t sb; };
-template <int FMT> struct RawB { uint32_t w[8]; uint32_t sb; };
+template <> struct RawA<IFQ_FMT_IF3_BS8> { uint16_t h[6]; uint64_t sb; };
+template <int FMT> struct RawB { uint32_t w[8]; ScaleBits<FMT> sb; };
 template <> struct RawB<IFQ_FMT_IF3> { uint16_t h[12]; uint32_t sb; };
+template <> struct RawB<IFQ_FMT_IF3_BS8> { uint16_t h[12]; uint64_t sb; };
 template <> struct RawA<IFQ_FMT_IF6_E2M3> { uint32_t w[6]; uint32_t sb; };
 template <> struct RawA<IFQ_FMT_IF6_E3M2> { uint32_t w[6]; uint32_t sb; };
 template <> struct RawB<IFQ_FMT_IF6_E2M3> { uint32_t w[12]; uint32_t sb; };
@@ -223,17 +235,23 @@ template <int FMT, bool EDGE, int NG>
 __device__ __forceinline__ void load_groups(const uint8_t* __restrict__ codes,
                                             const uint8_t* __restrict__ scales, int64_t row,
                                             int64_t nrows, int64_t gpr, int64_t g0,
-                                            uint32_t* w, uint16_t* h, uint32_t& sb)
+                                            uint32_t* w, uint16_t* h, ScaleBits<FMT>& sb)
 {
     constexpr int BITS = Fmt<FMT>::BITS;
+    constexpr int SPG = Fmt<FMT>::G == 8 ? 2 : 1;  // scale bytes per 16 values
     const uint8_t* cp = codes + (row * gpr + g0) * (2 * BITS);
-    const uint8_t* sp = scales + row * gpr + g0;
+    const uint8_t* sp = scales + (row * gpr + g0) * SPG;
     if constexpr (BITS == 4 && !EDGE) {
         const uint4 a = *reinterpret_cast<const uint4*>(cp);
         w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
         if constexpr (NG == 4) {
             const uint4 b = *reinterpret_cast<const uint4*>(cp + 16);
             w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+        }
+        if constexpr (SPG == 2 && NG == 4) {
+            const uint32_t* sp4 = reinterpret_cast<const uint32_t*>(sp);  // 4-byte aligned
+            sb = (uint64_t)sp4[0] | ((uint64_t)sp4[1] << 32);
+        } else if constexpr (SPG == 2 || NG == 4) {
             sb = *reinterpret_cast<const uint32_t*>(sp);
         } else {
             sb = *reinterpret_cast<const uint16_t*>(sp);
@@ -259,7 +277,11 @@ __device__ __forceinline__ void load_groups(const uint8_t* __restrict__ codes,
                 h[3 * g + 1] = ok ? p[1] : (uint16_t)0;
                 h[3 * g + 2] = ok ? p[2] : (uint16_t)0;
             }
-            sb |= (ok ? (uint32_t)sp[g] : 0u) << (8 * g);
+            if constexpr (SPG == 2) {
+                sb |= (ok ? (ScaleBits<FMT>)sp[2 * g] | ((ScaleBits<FMT>)sp[2 * g + 1] << 8) : 0) << (16 * g);
+            } else {
+                sb |= (ok ? (uint32_t)sp[g] : 0u) << (8 * g);
+            }
         }
     }
 }
@@ -286,9 +308,32 @@ __device__ __forceinline__ void load_b(const uint8_t* __restrict__ codes, const 
 
 // Decode group g of a raw chunk (whose scale bytes are sb) into 8 operand pairs.
 template <int FMT>
-__device__ __forceinline__ void decode_group(const uint32_t* w, const uint16_t* h, uint32_t sb, int g,
+__device__ __forceinline__ void decode_group(const uint32_t* w, const uint16_t* h, ScaleBits<FMT> sb, int g,
                                              uint32_t (&out)[8])
 {
+    if constexpr (Fmt<FMT>::G == 8) {
+        // block size 8: the two scale bytes of these 16 values hold the
+        // constants of codes 0-7 (low byte) and 8-15 (high byte)
+        const uint32_t sw = (uint32_t)(sb >> (16 * g)) & 0xFFFFu;
+        uint32_t K, Cb;
+        pair_scales<FMT>(sw, K, Cb);
+        const bool i0 = Fmt<FMT>::ADAPTIVE && ((sw >> 7) & 1u), i1 = Fmt<FMT>::ADAPTIVE && ((sw >> 15) & 1u);
+        if constexpr (Fmt<FMT>::BITS == 4) {
+            uint32_t o0[4], o1[4];
+            decode_word<FMT>(w[2 * g], i0, bcast_lo(K), bcast_lo(Cb), o0);
+            decode_word<FMT>(w[2 * g + 1], i1, bcast_hi(K), bcast_hi(Cb), o1);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                out[i] = o0[i];
+                out[4 + i] = o1[i];
+            }
+        } else {
+            const uint64_t bitsv = (uint64_t)h[3 * g] | ((uint64_t)h[3 * g + 1] << 16) |
+                                   ((uint64_t)h[3 * g + 2] << 32);
+            decode_if3_group(bitsv, i0, bcast_lo(K), i1, bcast_hi(K), out);
+        }
+        return;
+    } else {
     const uint32_t sw = (sb >> (16 * (g >> 1))) & 0xFFFFu;
     uint32_t K, Cb;
     pair_scales<FMT>(sw, K, Cb);
@@ -309,7 +354,8 @@ __device__ __forceinline__ void decode_group(const uint32_t* w, const uint16_t* 
     } else {
         const uint64_t bitsv = (uint64_t)h[3 * g] | ((uint64_t)h[3 * g + 1] << 16) |
                                ((uint64_t)h[3 * g + 2] << 32);
-        decode_if3_group(bitsv, is_int, k2, out);
+        decode_if3_group(bitsv, is_int, k2, is_int, k2, out);
+    }
     }
 }
 
@@ -1103,19 +1149,23 @@ static hipError_t launch_g(const GemmArgs& a, hipStream_t s)
     const int64_t full_n = interior_ok ? a.N / kBN : 0;
     if constexpr (Fmt<FMT>::BITS == 4) {
       if (full_m * full_n > 0) {
-        const bool fast_ok = (a.K % 512) == 0 && ((uintptr_t)a.a_codes % 16) == 0 &&
+        const bool fast_ok = Fmt<FMT>::G == 16 && (a.K % 512) == 0 && ((uintptr_t)a.a_codes % 16) == 0 &&
                              ((uintptr_t)a.b_codes % 16) == 0 && ((uintptr_t)a.a_scales % 16) == 0 &&
                              ((uintptr_t)a.b_scales % 16) == 0;
         const dim3 grid((unsigned)(full_m * full_n)), block(kGemmThreads);
 #define IFQ_GEMM_ARGS a.a_codes, a.a_scales, a.a_ts, a.b_codes, a.b_scales, a.b_ts, a.M, a.N, a.K, a.c, a.ldc, \
                       (int)full_m, (int)full_n
-        if (fast_ok && a.out_bf16)
-            hipLaunchKernelGGL((gemm_tn_fast<FMT, true>), grid, block, 0, s, IFQ_GEMM_ARGS);
-        else if (fast_ok)
-            hipLaunchKernelGGL((gemm_tn_fast<FMT, false>), grid, block, 0, s, IFQ_GEMM_ARGS);
-        else if (a.out_bf16)
+        bool done = false;
+        if constexpr (Fmt<FMT>::G == 16) {  // the fast path stages one scale byte per 16 values
+            if (fast_ok && a.out_bf16)
+                hipLaunchKernelGGL((gemm_tn_fast<FMT, true>), grid, block, 0, s, IFQ_GEMM_ARGS);
+            else if (fast_ok)
+                hipLaunchKernelGGL((gemm_tn_fast<FMT, false>), grid, block, 0, s, IFQ_GEMM_ARGS);
+            done = fast_ok;
+        }
+        if (!done && a.out_bf16)
             hipLaunchKernelGGL((gemm_tn_interior<FMT, true>), grid, block, 0, s, IFQ_GEMM_ARGS);
-        else
+        else if (!done)
             hipLaunchKernelGGL((gemm_tn_interior<FMT, false>), grid, block, 0, s, IFQ_GEMM_ARGS);
 #undef IFQ_GEMM_ARGS
         hipError_t e = hipGetLastError();
@@ -1152,6 +1202,9 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s)
         case IFQ_FMT_NVINT4: return launch_g<IFQ_FMT_NVINT4>(a, s);
         // 4/6 operands are NVFP4 data (E2M1 codes, E4M3 scales, bit 7 clear)
         case IFQ_FMT_NVFP4_46: return launch_g<IFQ_FMT_NVFP4>(a, s);
+        case IFQ_FMT_IF4_BS8: return launch_g<IFQ_FMT_IF4_BS8>(a, s);
+        case IFQ_FMT_IF3_BS8: return launch_g<IFQ_FMT_IF3_BS8>(a, s);
+        case IFQ_FMT_NVFP4_BS8: return launch_g<IFQ_FMT_NVFP4_BS8>(a, s);
         default: return hipErrorNotSupported;
     }
 }

@@ -74,7 +74,12 @@ __device__ __forceinline__ void quantize_store(const float (&v)[kGroup], float a
     Packed<BITS> p;
     const uint32_t sb = quantize_any<FMT, SR>(v, alpha, denom, qflags, seed, gi, p);
     store_packed<BITS>(codes + gi * (2 * BITS), p);
-    scales[gi] = (uint8_t)sb;
+    if constexpr (Fmt<FMT>::G == 8) {
+        scales[2 * gi] = (uint8_t)sb;
+        scales[2 * gi + 1] = (uint8_t)(sb >> 8);
+    } else {
+        scales[gi] = (uint8_t)sb;
+    }
 }
 
 // --------------------------------------------------------------- row-wise
@@ -511,7 +516,7 @@ static inline bool strided_load_ok(const QuantArgs& a)
 template <int FMT>
 static inline bool strided_cols_ok(const QuantArgs& a)
 {
-    return Fmt<FMT>::BITS == 4 && strided_load_ok(a) && (a.rows / kGroup) % 16 == 0 &&
+    return Fmt<FMT>::BITS == 4 && Fmt<FMT>::G == 16 && strided_load_ok(a) && (a.rows / kGroup) % 16 == 0 &&
            a.rows / kGroup / kGrpTile < 65536 && reinterpret_cast<uintptr_t>(a.codes) % 16 == 0 &&
            reinterpret_cast<uintptr_t>(a.scales) % 16 == 0;
 }
@@ -523,7 +528,7 @@ static hipError_t launch_q(const QuantArgs& a, hipStream_t s, int npartials, flo
     const int scale_in = (a.flags & IFQ_SCALE_IN) ? 1 : 0;
     const int qflags = ((a.flags & IFQ_SR_RTN_TYPE) ? kQSrRtnType : 0) |
                        ((a.flags & IFQ_MARGIN_16_17) ? kQMargin : 0);
-    if constexpr (Fmt<FMT>::BITS == 4) {
+    if constexpr (Fmt<FMT>::BITS == 4 && Fmt<FMT>::G == 16) {
         if ((a.flags & IFQ_AXIS_STRIDED) && strided_cols_ok<FMT>(a)) {
             dim3 grid((unsigned)cdiv(a.cols, kColTile), (unsigned)cdiv(a.rows / kGroup, kGrpTile));
             hipLaunchKernelGGL((quantize_cols<FMT, RHT, SR>), grid, dim3(kThreads), 0, s, a.x, a.rows,
@@ -610,6 +615,9 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t s)
         case IFQ_FMT_IF6_E3M2: targets<IFQ_FMT_IF6_E3M2>(scale_max, a8); break;
         case IFQ_FMT_NVINT4: targets<IFQ_FMT_NVINT4>(scale_max, a8); break;
         case IFQ_FMT_NVFP4_46: targets<IFQ_FMT_NVFP4_46>(scale_max, a8); break;
+        case IFQ_FMT_IF4_BS8: targets<IFQ_FMT_IF4_BS8>(scale_max, a8); break;
+        case IFQ_FMT_IF3_BS8: targets<IFQ_FMT_IF3_BS8>(scale_max, a8); break;
+        case IFQ_FMT_NVFP4_BS8: targets<IFQ_FMT_NVFP4_BS8>(scale_max, a8); break;
         default: return hipErrorInvalidValue;
     }
     if (a.flags & IFQ_MARGIN_16_17) scale_max = (float)((double)scale_max * 16.0 / 17.0);
@@ -633,7 +641,10 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t s)
         case IFQ_FMT_IF6_E2M3: return dispatch_fmt<IFQ_FMT_IF6_E2M3>(a, s, npartials, scale_max, denom_alpha);
         case IFQ_FMT_IF6_E3M2: return dispatch_fmt<IFQ_FMT_IF6_E3M2>(a, s, npartials, scale_max, denom_alpha);
         case IFQ_FMT_NVINT4: return dispatch_fmt<IFQ_FMT_NVINT4>(a, s, npartials, scale_max, denom_alpha);
-        default: return dispatch_fmt<IFQ_FMT_NVFP4_46>(a, s, npartials, scale_max, denom_alpha);
+        case IFQ_FMT_NVFP4_46: return dispatch_fmt<IFQ_FMT_NVFP4_46>(a, s, npartials, scale_max, denom_alpha);
+        case IFQ_FMT_IF4_BS8: return dispatch_fmt<IFQ_FMT_IF4_BS8>(a, s, npartials, scale_max, denom_alpha);
+        case IFQ_FMT_IF3_BS8: return dispatch_fmt<IFQ_FMT_IF3_BS8>(a, s, npartials, scale_max, denom_alpha);
+        default: return dispatch_fmt<IFQ_FMT_NVFP4_BS8>(a, s, npartials, scale_max, denom_alpha);
     }
 }
 

@@ -18,10 +18,14 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libifq.so")
 
-IF4, NVFP4, IF3, IF6_E2M3, IF6_E3M2, NVINT4, NVFP4_46 = range(7)
+IF4, NVFP4, IF3, IF6_E2M3, IF6_E3M2, NVINT4, NVFP4_46, IF4_BS8, IF3_BS8, NVFP4_BS8 = range(10)
 FORMAT_NAMES = {IF4: "if4", NVFP4: "nvfp4", IF3: "if3", IF6_E2M3: "if6_e2m3", IF6_E3M2: "if6_e3m2",
-                NVINT4: "nvint4", NVFP4_46: "nvfp4_46"}
-BITS = {IF4: 4, NVFP4: 4, IF3: 3, IF6_E2M3: 6, IF6_E3M2: 6, NVINT4: 4, NVFP4_46: 4}
+                NVINT4: "nvint4", NVFP4_46: "nvfp4_46", IF4_BS8: "if4_bs8", IF3_BS8: "if3_bs8",
+                NVFP4_BS8: "nvfp4_bs8"}
+BITS = {IF4: 4, NVFP4: 4, IF3: 3, IF6_E2M3: 6, IF6_E3M2: 6, NVINT4: 4, NVFP4_46: 4, IF4_BS8: 4,
+        IF3_BS8: 3, NVFP4_BS8: 4}
+# values per scale byte
+GSIZE = {f: (8 if f in (IF4_BS8, IF3_BS8, NVFP4_BS8) else 16) for f in BITS}
 
 RHT, SR, MARGIN_16_17, SCALE_IN, AXIS_STRIDED, SR_RTN_TYPE = 1, 2, 4, 8, 16, 32
 F32, BF16 = 0, 1
@@ -76,6 +80,8 @@ def lib() -> C.CDLL:
         L.ifq_quantize_dual_workspace_bytes.argtypes = [C.c_int, C.c_int64, C.c_int64, C.c_uint32,
                                                         C.c_uint32]
         L.ifq_quantize_dual_workspace_bytes.restype = C.c_size_t
+        L.ifq_group_size.argtypes = [C.c_int]
+        L.ifq_group_size.restype = C.c_int
         L.ifq_status_string.argtypes = [C.c_int]
         L.ifq_status_string.restype = C.c_char_p
         L.ifq_abi_version.restype = C.c_int
@@ -121,7 +127,7 @@ def _quantize(fn: str, fmt: int, x: torch.Tensor, flags: int = 0, rht_signs: int
     dev = x.device
     if out is None:
         codes = torch.empty((R, K * BITS[fmt] // 8), dtype=torch.uint8, device=dev)
-        scales = torch.empty((R, K // 16), dtype=torch.uint8, device=dev)
+        scales = torch.empty((R, K // GSIZE[fmt]), dtype=torch.uint8, device=dev)
         ts = torch.empty(1, dtype=torch.float32, device=dev) if tensor_scale is None else tensor_scale
         out = Packed(fmt, codes, scales, ts, R, K)
     elif tensor_scale is not None:
@@ -159,7 +165,7 @@ def ifx_quantize(fmt, x, flags=0, rht_signs=0, seed=0, tensor_scale=None, out=No
 
 def _packed_for(fmt: int, R: int, K: int, dev, tensor_scale=None) -> Packed:
     codes = torch.empty((R, K * BITS[fmt] // 8), dtype=torch.uint8, device=dev)
-    scales = torch.empty((R, K // 16), dtype=torch.uint8, device=dev)
+    scales = torch.empty((R, K // GSIZE[fmt]), dtype=torch.uint8, device=dev)
     ts = torch.empty(1, dtype=torch.float32, device=dev) if tensor_scale is None else tensor_scale
     return Packed(fmt, codes, scales, ts, R, K)
 

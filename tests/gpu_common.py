@@ -7,7 +7,8 @@ import torch
 import oracle as O
 from paper_2603_28765_amd import ops
 
-FORMATS = [ops.IF4, ops.NVFP4, ops.IF3, ops.IF6_E2M3, ops.IF6_E3M2, ops.NVINT4, ops.NVFP4_46]
+FORMATS = [ops.IF4, ops.NVFP4, ops.IF3, ops.IF6_E2M3, ops.IF6_E3M2, ops.NVINT4, ops.NVFP4_46,
+           ops.IF4_BS8, ops.IF3_BS8, ops.NVFP4_BS8]
 GEMM_FORMATS = FORMATS
 
 

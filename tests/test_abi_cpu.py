@@ -53,6 +53,8 @@ def test_version_and_strings(L):
     assert L.ifq_quantize_dual_workspace_bytes(0, 8192, 8192, 0, 8) >= 8
     assert L.ifq_quantize_dual_workspace_bytes(0, 8192, 8192, 8, 8) == 0
     assert "ifx_quantize_dual" in declared_functions()
+    assert [L.ifq_group_size(f) for f in range(11)] == [16] * 7 + [8] * 3 + [0]
+    assert L.ifq_codes_bytes(7, 16, 64) == 16 * 64 // 2 and L.ifq_codes_bytes(8, 16, 64) == 16 * 64 * 3 // 8
 
 
 # fake, never dereferenced device addresses: validation fails first
@@ -74,9 +76,9 @@ def test_quantize_validation(L):
     assert q(L, codes=None) == EINVAL
     assert q(L, flags=1 << 7) == EINVAL
     assert q(L, signs=1 << 16) == EINVAL
-    assert q(L, fmt=9) == EINVAL
-    assert q(L, fmt=7) == EINVAL
+    assert q(L, fmt=10) == EINVAL
     assert q(L, fmt=6, cols=40) == ESHAPE
+    assert q(L, fmt=7, cols=40, ld=40) == ESHAPE   # block size 8: K still a multiple of 16
     assert q(L, rows=-1) == ESHAPE
     assert q(L, cols=40, ld=40) == ESHAPE                  # K % 16
     assert q(L, rows=40, flags=16) == ESHAPE               # strided: rows % 16
@@ -108,7 +110,8 @@ def test_gemm_validation(L):
     assert g(L, fmt=4, ldc=32) == ESHAPE
     assert g(L, fmt=5, K=40) == ESHAPE    # NVINT4 and NVFP4 with 4/6 likewise
     assert g(L, fmt=6, ldc=32) == ESHAPE
-    assert g(L, fmt=7) == EINVAL
+    assert g(L, fmt=8, K=40) == ESHAPE    # block size 8 likewise
+    assert g(L, fmt=10) == EINVAL
     assert g(L, fmt=-1) == EINVAL
 
 
@@ -123,11 +126,12 @@ def test_dual_quantize_validation(L):
     assert qd(L, cf=16) == EINVAL
     assert qd(L, cf=1 << 7) == EINVAL
     assert qd(L, signs=1 << 16) == EINVAL
-    assert qd(L, fmt=7) == EINVAL
+    assert qd(L, fmt=10) == EINVAL
     assert qd(L, rts=None) == EINVAL
     assert qd(L, cts=None) == EINVAL
     assert qd(L, fmt=2) == EUNSUPPORTED        # IF3 / IF6: not training formats
     assert qd(L, fmt=3) == EUNSUPPORTED
+    assert qd(L, fmt=7) == EUNSUPPORTED        # block size 8
     assert qd(L, rows=40) == ESHAPE            # both axes are grouped
     assert qd(L, cols=40, ld=40) == ESHAPE
     assert qd(L, ld=48) == ESHAPE

@@ -26,7 +26,8 @@ def _quantized_pair(fmt, a_cpu, b_cpu, flags=0, signs=0, seeds=(0, 0)):
 
 
 # IF6 operands are rounded to FP16; the others are exact
-EXACT_OPERANDS = (ops.IF4, ops.NVFP4, ops.IF3, ops.NVINT4, ops.NVFP4_46)
+EXACT_OPERANDS = (ops.IF4, ops.NVFP4, ops.IF3, ops.NVINT4, ops.NVFP4_46, ops.IF4_BS8, ops.IF3_BS8,
+                  ops.NVFP4_BS8)
 
 
 def _check(fmt, pa, oa, pb, ob, dtype=ops.F32, tag=""):
