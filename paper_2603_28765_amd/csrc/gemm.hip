@@ -166,35 +166,53 @@ __device__ __forceinline__ void decode_word(uint32_t w, bool is_int, uint32_t k2
 // Sixteen three-bit IF3 codes (48 bits) -> 8 FP16 operand pairs: 3 q (FP) or
 // 4 q (INT), times Delta (at most 6 significant bits, exact).  Codes 0-7 use
 // (is_int0, k20), codes 8-15 (is_int1, k21): the same for block size 16.
+// Each run of 4 codes is spread to bytes, one v_perm looks up the E4M3 byte
+// of its folded value (3 x E2M0 sign-magnitude, or 4 x INT3 two's
+// complement -- small integers, exact in E4M3), the FP8 converter turns
+// it into FP16 and one FP16 multiply applies Delta (k2 = Delta in both
+// halves; the product has at most 6 significant bits).
 __device__ __forceinline__ void decode_if3_group(uint64_t bitsv, bool is_int0, uint32_t k20, bool is_int1,
                                                  uint32_t k21, uint32_t (&out)[8])
 {
-    using D = FmtDerived<IFQ_FMT_IF3>;
+    // bytes 0..7 = code 0..7: FP {0, 3, 6, 12, -0, -3, -6, -12}; INT {0, 4, 8, 12, -16, -12, -8, -4}
+    constexpr uint32_t kFpLo = 0x544C4400u, kFpHi = 0xD4CCC480u;
+    constexpr uint32_t kIntLo = 0x54504800u, kIntHi = 0xC8D0D4D8u;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const bool is_int = i < 4 ? is_int0 : is_int1;
-        const half2v K = u32_as_h2(i < 4 ? k20 : k21);
-        half2v hv;
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            const uint32_t c = (uint32_t)(bitsv >> (3 * (2 * i + e))) & 7u;
-            const float qi = (float)((int)(c << 29) >> 29);
-            const float mag = fp_magnitude<IFQ_FMT_IF3>(c & 3u);
-            const float qf = (c & D::SIGN_BIT) ? -mag : mag;
-            hv[e] = (_Float16)(is_int ? qi * Fold<IFQ_FMT_IF3>::INT : qf * Fold<IFQ_FMT_IF3>::FP);
-        }
-        out[i] = h2_as_u32(hv * K);
+    for (int q = 0; q < 4; ++q) {
+        const bool is_int = q < 2 ? is_int0 : is_int1;
+        const half2v K = u32_as_h2(q < 2 ? k20 : k21);
+        const uint32_t t = (uint32_t)(bitsv >> (12 * q)) & 0xFFFu;
+        const uint32_t sel = (t & 7u) | ((t << 5) & 0x700u) | ((t << 10) & 0x70000u) | ((t << 15) & 0x7000000u);
+        const uint32_t e = __builtin_amdgcn_perm(is_int ? kIntHi : kFpHi, is_int ? kIntLo : kFpLo, sel);
+        out[2 * q] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(e, 1.0f, false) * K);
+        out[2 * q + 1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(e, 1.0f, true) * K);
     }
 }
 
 // Sixteen six-bit IF6 codes (96 bits in w[0..2], code j at bits 6j) -> 8
 // FP16 operand pairs: Fold::FP * q (FP, sign-magnitude ExMy) or Fold::INT * q
-// (INT6 two's complement), times Delta, rounded once to FP16.
+// (INT6 two's complement), times Delta, rounded once to FP16.  FP codes go
+// through the gfx950 FP6 converter (E2M3: fp6, E3M2: bf6; 32 codes per
+// instruction, the upper 16 unused) to exact FP16 values; INT codes are
+// sign-extended and converted exactly; one FP16 multiply by the exact fold
+// constant (Fold * Delta has at most 9 significant bits) rounds the product
+// once, as the FP32 product rounded to FP16 would.
+typedef int v6i32 __attribute__((ext_vector_type(6)));
+typedef _Float16 v32f16 __attribute__((ext_vector_type(32)));
+
 template <int FMT>
 __device__ __forceinline__ void decode_if6_group(const uint32_t* w, uint32_t sbyte, uint32_t (&out)[8])
 {
     const bool is_int = (sbyte >> 7) & 1u;
     const float delta = e4m3_value(sbyte & 0x7Fu);
+    const _Float16 kf = (_Float16)(Fold<FMT>::FP * delta), ki = (_Float16)(Fold<FMT>::INT * delta);
+    const half2v KF = {kf, kf}, KI = {ki, ki};
+    const v6i32 src = {(int)w[0], (int)w[1], (int)w[2], 0, 0, 0};
+    v32f16 f;
+    if constexpr (Fmt<FMT>::EB == 2)
+        f = __builtin_amdgcn_cvt_scalef32_pk32_f16_fp6(src, 1.0f);
+    else
+        f = __builtin_amdgcn_cvt_scalef32_pk32_f16_bf6(src, 1.0f);
     const uint64_t lo = (uint64_t)w[0] | ((uint64_t)w[1] << 32);
     const uint64_t hi = (uint64_t)w[1] | ((uint64_t)w[2] << 32);  // bits 32 .. 95
 #pragma unroll
@@ -204,12 +222,10 @@ __device__ __forceinline__ void decode_if6_group(const uint32_t* w, uint32_t sby
         for (int e = 0; e < 2; ++e) {
             const int bit = 6 * (2 * i + e);
             const uint32_t c = (uint32_t)((bit <= 58 ? (lo >> bit) : (hi >> (bit - 32))) & 63u);
-            const float qi = (float)((int)(c << 26) >> 26);
-            const float mag = fp_magnitude<FMT>(c & 31u);
-            const float qf = (c & 32u) ? -mag : mag;
-            hv[e] = (_Float16)((is_int ? qi * Fold<FMT>::INT : qf * Fold<FMT>::FP) * delta);
+            hv[e] = (_Float16)((int)(c << 26) >> 26);
         }
-        out[i] = h2_as_u32(hv);
+        const half2v fv = {f[2 * i], f[2 * i + 1]};
+        out[i] = h2_as_u32(is_int ? hv * KI : fv * KF);
     }
 }
 
@@ -254,6 +270,42 @@ __device__ __forceinline__ void load_groups(const uint8_t* __restrict__ codes,
         } else if constexpr (SPG == 2 || NG == 4) {
             sb = *reinterpret_cast<const uint32_t*>(sp);
         } else {
+            sb = *reinterpret_cast<const uint16_t*>(sp);
+        }
+    } else if constexpr (BITS == 6 && !EDGE) {
+        // interior tiles (K % 128 == 0, 16-byte aligned codes): a row's NG
+        // groups are 12 NG contiguous bytes, 16-byte aligned for NG = 4 and
+        // 8-byte aligned for NG = 2
+        if constexpr (NG == 4) {
+#pragma unroll
+            for (int i = 0; i < 3; ++i) {
+                const uint4 v = reinterpret_cast<const uint4*>(cp)[i];
+                w[4 * i] = v.x; w[4 * i + 1] = v.y; w[4 * i + 2] = v.z; w[4 * i + 3] = v.w;
+            }
+            sb = *reinterpret_cast<const uint32_t*>(sp);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 3; ++i) {
+                const uint2 v = reinterpret_cast<const uint2*>(cp)[i];
+                w[2 * i] = v.x; w[2 * i + 1] = v.y;
+            }
+            sb = *reinterpret_cast<const uint16_t*>(sp);
+        }
+    } else if constexpr (BITS == 3 && !EDGE && SPG == 1) {
+        // interior tiles: 6 NG contiguous bytes, 8-byte aligned for NG = 4
+        // and 4-byte aligned for NG = 2 (8-byte pieces, then dwords)
+        if constexpr (NG == 4) {
+#pragma unroll
+            for (int i = 0; i < 3; ++i) {
+                const uint2 v = reinterpret_cast<const uint2*>(cp)[i];
+                h[4 * i] = (uint16_t)v.x; h[4 * i + 1] = (uint16_t)(v.x >> 16);
+                h[4 * i + 2] = (uint16_t)v.y; h[4 * i + 3] = (uint16_t)(v.y >> 16);
+            }
+            sb = *reinterpret_cast<const uint32_t*>(sp);
+        } else {
+            const uint32_t* c4 = reinterpret_cast<const uint32_t*>(cp);
+#pragma unroll
+            for (int i = 0; i < 3; ++i) { h[2 * i] = (uint16_t)c4[i]; h[2 * i + 1] = (uint16_t)(c4[i] >> 16); }
             sb = *reinterpret_cast<const uint16_t*>(sp);
         }
     } else {
@@ -1143,20 +1195,23 @@ static hipError_t launch_g(const GemmArgs& a, hipStream_t s)
     const int64_t tiles_m = (a.M + kBM - 1) / kBM, tiles_n = (a.N + kBN - 1) / kBN;
     if (tiles_m == 0 || tiles_n == 0) return hipSuccess;
     if (tiles_m * tiles_n > (int64_t)1 << 30) return hipErrorInvalidValue;
+    // interior tiles load whole row chunks: K % 128 == 0, 4-byte aligned scale
+    // rows, 16-byte aligned codes (as the API requires)
     const bool interior_ok = (a.K % (2 * kBK)) == 0 && ((uintptr_t)a.a_scales % 4) == 0 &&
-                             ((uintptr_t)a.b_scales % 4) == 0 && Fmt<FMT>::BITS == 4;
+                             ((uintptr_t)a.b_scales % 4) == 0 && ((uintptr_t)a.a_codes % 16) == 0 &&
+                             ((uintptr_t)a.b_codes % 16) == 0;
     const int64_t full_m = interior_ok ? a.M / kBM : 0;
     const int64_t full_n = interior_ok ? a.N / kBN : 0;
-    if constexpr (Fmt<FMT>::BITS == 4) {
+    {
       if (full_m * full_n > 0) {
-        const bool fast_ok = Fmt<FMT>::G == 16 && (a.K % 512) == 0 && ((uintptr_t)a.a_codes % 16) == 0 &&
+        const bool fast_ok = Fmt<FMT>::BITS == 4 && Fmt<FMT>::G == 16 && (a.K % 512) == 0 && ((uintptr_t)a.a_codes % 16) == 0 &&
                              ((uintptr_t)a.b_codes % 16) == 0 && ((uintptr_t)a.a_scales % 16) == 0 &&
                              ((uintptr_t)a.b_scales % 16) == 0;
         const dim3 grid((unsigned)(full_m * full_n)), block(kGemmThreads);
 #define IFQ_GEMM_ARGS a.a_codes, a.a_scales, a.a_ts, a.b_codes, a.b_scales, a.b_ts, a.M, a.N, a.K, a.c, a.ldc, \
                       (int)full_m, (int)full_n
         bool done = false;
-        if constexpr (Fmt<FMT>::G == 16) {  // the fast path stages one scale byte per 16 values
+        if constexpr (Fmt<FMT>::BITS == 4 && Fmt<FMT>::G == 16) {  // fast path: 4-bit codes, one scale per 16
             if (fast_ok && a.out_bf16)
                 hipLaunchKernelGGL((gemm_tn_fast<FMT, true>), grid, block, 0, s, IFQ_GEMM_ARGS);
             else if (fast_ok)
