@@ -194,38 +194,52 @@ __device__ __forceinline__ void decode_if3_group(uint64_t bitsv, bool is_int0, u
 // (INT6 two's complement), times Delta, rounded once to FP16.  FP codes go
 // through the gfx950 FP6 converter (E2M3: fp6, E3M2: bf6; 32 codes per
 // instruction, the upper 16 unused) to exact FP16 values; INT codes are
-// sign-extended and converted exactly; one FP16 multiply by the exact fold
-// constant (Fold * Delta has at most 9 significant bits) rounds the product
-// once, as the FP32 product rounded to FP16 would.
+// sign-extended and turned into FP16 exactly through the bits of 1536 + q;
+// one FP16 multiply by the exact fold constant (Fold * Delta has at most 9
+// significant bits) rounds the product once, as the FP32 product rounded to
+// FP16 would.
 typedef int v6i32 __attribute__((ext_vector_type(6)));
 typedef _Float16 v32f16 __attribute__((ext_vector_type(32)));
 
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
 template <int FMT>
-__device__ __forceinline__ void decode_if6_group(const uint32_t* w, uint32_t sbyte, uint32_t (&out)[8])
+__device__ __forceinline__ void decode_if6_group(const uint32_t* w, bool is_int, uint32_t k2, uint32_t (&out)[8])
 {
-    const bool is_int = (sbyte >> 7) & 1u;
-    const float delta = e4m3_value(sbyte & 0x7Fu);
-    const _Float16 kf = (_Float16)(Fold<FMT>::FP * delta), ki = (_Float16)(Fold<FMT>::INT * delta);
-    const half2v KF = {kf, kf}, KI = {ki, ki};
+    // k2 = Delta in both halves (exact FP16); the folds are exact FP16 too
+    const half2v D = u32_as_h2(k2);
+    const half2v KF = D * half2v{(_Float16)Fold<FMT>::FP, (_Float16)Fold<FMT>::FP};
+    const half2v KI = D * half2v{(_Float16)Fold<FMT>::INT, (_Float16)Fold<FMT>::INT};
+    const uint32_t im = 0u - (uint32_t)is_int;  // all-ones in an INT group: branch-free select
     const v6i32 src = {(int)w[0], (int)w[1], (int)w[2], 0, 0, 0};
     v32f16 f;
     if constexpr (Fmt<FMT>::EB == 2)
         f = __builtin_amdgcn_cvt_scalef32_pk32_f16_fp6(src, 1.0f);
     else
         f = __builtin_amdgcn_cvt_scalef32_pk32_f16_bf6(src, 1.0f);
-    const uint64_t lo = (uint64_t)w[0] | ((uint64_t)w[1] << 32);
-    const uint64_t hi = (uint64_t)w[1] | ((uint64_t)w[2] << 32);  // bits 32 .. 95
+    // code j at bits 6j: codes 5 (bits 30-35) and 10 (bits 60-65) straddle words
+    const uint32_t x5 = __builtin_amdgcn_alignbit(w[1], w[0], 30);
+    const uint32_t x10 = __builtin_amdgcn_alignbit(w[2], w[1], 28);
+    const u16x2 bias = {0x6600, 0x6600};          // 1536 in FP16: ulp 1 on [1024, 2048)
+    const half2v off = {(_Float16)1536.0f, (_Float16)1536.0f};
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        half2v hv;
+        int q[2];
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
-            const int bit = 6 * (2 * i + e);
-            const uint32_t c = (uint32_t)((bit <= 58 ? (lo >> bit) : (hi >> (bit - 32))) & 63u);
-            hv[e] = (_Float16)((int)(c << 26) >> 26);
+            const int j = 2 * i + e;
+            if (j < 5) q[e] = __builtin_amdgcn_sbfe((int)w[0], 6 * j, 6);
+            else if (j == 5) q[e] = __builtin_amdgcn_sbfe((int)x5, 0, 6);
+            else if (j < 10) q[e] = __builtin_amdgcn_sbfe((int)w[1], 6 * j - 32, 6);
+            else if (j == 10) q[e] = __builtin_amdgcn_sbfe((int)x10, 0, 6);
+            else q[e] = __builtin_amdgcn_sbfe((int)w[2], 6 * j - 64, 6);
         }
+        // the INT6 pair as FP16: bits of 1536 + q (exact), minus 1536
+        const u16x2 qq = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm((uint32_t)q[1], (uint32_t)q[0], 0x05040100u));
+        const half2v hv = __builtin_bit_cast(half2v, qq + bias) - off;
         const half2v fv = {f[2 * i], f[2 * i + 1]};
-        out[i] = h2_as_u32(is_int ? hv * KI : fv * KF);
+        const uint32_t ri = h2_as_u32(hv * KI), rf = h2_as_u32(fv * KF);
+        out[i] = (ri & im) | (rf & ~im);
     }
 }
 
@@ -291,7 +305,7 @@ __device__ __forceinline__ void load_groups(const uint8_t* __restrict__ codes,
             }
             sb = *reinterpret_cast<const uint16_t*>(sp);
         }
-    } else if constexpr (BITS == 3 && !EDGE && SPG == 1) {
+    } else if constexpr (BITS == 3 && !EDGE) {
         // interior tiles: 6 NG contiguous bytes, 8-byte aligned for NG = 4
         // and 4-byte aligned for NG = 2 (8-byte pieces, then dwords)
         if constexpr (NG == 4) {
@@ -301,11 +315,18 @@ __device__ __forceinline__ void load_groups(const uint8_t* __restrict__ codes,
                 h[4 * i] = (uint16_t)v.x; h[4 * i + 1] = (uint16_t)(v.x >> 16);
                 h[4 * i + 2] = (uint16_t)v.y; h[4 * i + 3] = (uint16_t)(v.y >> 16);
             }
-            sb = *reinterpret_cast<const uint32_t*>(sp);
         } else {
             const uint32_t* c4 = reinterpret_cast<const uint32_t*>(cp);
 #pragma unroll
             for (int i = 0; i < 3; ++i) { h[2 * i] = (uint16_t)c4[i]; h[2 * i + 1] = (uint16_t)(c4[i] >> 16); }
+        }
+        // scale bytes as for 4-bit codes (two per 16 values with block size 8)
+        if constexpr (SPG == 2 && NG == 4) {
+            const uint32_t* sp4 = reinterpret_cast<const uint32_t*>(sp);
+            sb = (uint64_t)sp4[0] | ((uint64_t)sp4[1] << 32);
+        } else if constexpr (SPG == 2 || NG == 4) {
+            sb = *reinterpret_cast<const uint32_t*>(sp);
+        } else {
             sb = *reinterpret_cast<const uint16_t*>(sp);
         }
     } else {
@@ -402,7 +423,7 @@ __device__ __forceinline__ void decode_group(const uint32_t* w, const uint16_t* 
             out[4 + i] = o1[i];
         }
     } else if constexpr (Fmt<FMT>::BITS == 6) {
-        decode_if6_group<FMT>(w + 3 * g, (sb >> (8 * g)) & 0xFFu, out);
+        decode_if6_group<FMT>(w + 3 * g, is_int, k2, out);
     } else {
         const uint64_t bitsv = (uint64_t)h[3 * g] | ((uint64_t)h[3 * g + 1] << 16) |
                                ((uint64_t)h[3 * g + 2] << 32);
