@@ -76,11 +76,15 @@ def test_shapes(fmt, dtype):
 @pytest.mark.parametrize("fmt", GEMM_FORMATS)
 @pytest.mark.parametrize("dtype", [ops.F32, ops.BF16])
 def test_shapes_k_multiple_of_512(fmt, dtype):
-    """Shapes whose full 256 x 256 tiles take the interior kernel with
-    line-sized operand copies (4-bit formats, K % 512 == 0), alone and next
-    to boundary tiles."""
+    """Shapes whose full 256 x 256 tiles take the interior kernels: the fast
+    kernel with line-sized operand copies (4-bit formats, K % 512 == 0), the
+    general kernel with whole row-chunk loads otherwise (K % 128 == 0; IF3,
+    IF6 and block size 8), alone and next to boundary tiles."""
     rng = np.random.default_rng(60 + fmt)
-    for (M, N, K) in [(256, 256, 512), (512, 768, 1024), (600, 520, 1536), (1024, 256, 4096)]:
+    # K % 128 == 0 but not 512: the general kernel's interior tiles (whole
+    # row-chunk loads) next to boundary tiles
+    for (M, N, K) in [(256, 256, 512), (512, 768, 1024), (600, 520, 1536), (1024, 256, 4096),
+                      (512, 256, 384), (256, 520, 640)]:
         a = workloads.to_bf16(rng.standard_t(3, (M, K)))
         b = workloads.to_bf16(rng.standard_normal((N, K)) * 0.02)
         pa, oa, pb, ob = _quantized_pair(fmt, a, b)
