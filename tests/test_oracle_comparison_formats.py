@@ -140,25 +140,28 @@ def test_bruteforce_nvint4(oracle):
             assert q == best or abs(abs(q - xq) - abs(best - xq)) < Fraction(1, 10 ** 5)
 
 
-def test_bruteforce_four_six(oracle):
-    """Three live values with alpha = 1: for each target t in {6, 4}, Delta_t
-    is the nearest E4M3 value to max|v| / t and every code the nearest E2M1
-    point of v / Delta_t; the kept scaling has the smaller exact squared
-    error of the dequantized group."""
+@pytest.mark.parametrize("margin", [False, True])
+def test_bruteforce_four_six(oracle, margin):
+    """Three live values with alpha = 1: for each target t in {6, 4} (each
+    times 16/17 with the margin of Sec. 4.1), Delta_t is the nearest E4M3
+    value to max|v| / t and every code the nearest E2M1 point of
+    v / Delta_t; the kept scaling has the smaller exact squared error of the
+    dequantized group."""
     grid = _e4m3_grid(oracle)
-    rng = np.random.default_rng(46)
+    rng = np.random.default_rng(46 + margin)
+    targets = [np.float32(t * 16.0 / 17.0) if margin else np.float32(t) for t in (6, 4)]
     seen = {0: 0, 1: 0}
     for trial in range(150):
         v = _group((rng.uniform(-1, 1, 3) * 2.0 ** rng.integers(-4, 6)).astype(np.float32))
         if trial % 3 == 0:  # lattice values make exact candidates likely
             v[:3] = np.round(v[:3] * 2) / 2
             v[0] = v[0] or 1.0
-        codes, sb, e6, e4 = oracle.quantize_group(v, 1.0, 6)
+        codes, sb, e6, e4 = oracle.quantize_group(v, 1.0, 6, oracle.MARGIN if margin else 0)
         xs = [Fraction(float(t)) for t in v[:3]]
         amax = max(abs(t) for t in xs)
         cand = {}
-        for ti, t in enumerate((6, 4)):
-            quot = Fraction(float(np.float32(np.float32(amax) / np.float32(t))))
+        for ti, t in enumerate(targets):
+            quot = Fraction(float(np.float32(np.float32(amax) / t)))
             dc = _nearest_e4m3_code(grid, quot)
             d = grid[dc]
             qs = [min(range(16), key=lambda c: (abs(_signed_e2m1(c) - x / d), c & 1)) for x in xs]
