@@ -756,12 +756,12 @@ __device__ __forceinline__ void vm_drain(u32x4 (&a)[2][2][2])
 
 // Fold constants of the two groups whose scale bytes are the low and high
 // byte of sw, one half each: the operand is K x + C, x the converted code.
-//   IF4 FP group : K = 7 Delta / 32, C = 0
+//   IF4 FP group : K = 14 Delta, C = 0 (x = E2M1 value times 2^-6)
 //   IF4 INT group: K = 96 Delta, C = -1.5 Delta (x = (q + 8) 2^-9)
-//   NVFP4        : K = Delta, C = 0
+//   NVFP4        : K = Delta, C = 0 (x = E2M1 value)
 //   NVINT4       : K = 128 Delta, C = -2 Delta (every group INT)
 // For IF4 the E4M3 conversion keeps the indicator bit as the sign (d = -Delta
-// for INT groups), so max(7 d / 32, -96 d) and min(1.5 d, 0) select the
+// for INT groups), so max(14 d, -96 d) and min(1.5 d, 0) select the
 // constants without masks; C != 0 marks an INT group (an INT group with
 // Delta = 0 decodes to zeros either way).
 struct KC {
@@ -779,7 +779,8 @@ __device__ __forceinline__ KC pair_kc(uint32_t sw)
         r.C = d * cn;
     } else if constexpr (Fmt<FMT>::ADAPTIVE) {
         const half2v d = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw, 1.0f, false);
-        const half2v f = {(_Float16)Fold<FMT>::FP, (_Float16)Fold<FMT>::FP};
+        constexpr float kf = Fold<FMT>::FP * 64.0f;
+        const half2v f = {(_Float16)kf, (_Float16)kf};
         const half2v fi = {(_Float16)-96.0f, (_Float16)-96.0f};
         const half2v c = {(_Float16)1.5f, (_Float16)1.5f};
         const half2v z = {(_Float16)0.0f, (_Float16)0.0f};
@@ -793,59 +794,137 @@ __device__ __forceinline__ KC pair_kc(uint32_t sw)
     return r;
 }
 
-// Four operand pairs from one dword of 4-bit codes (elements 2i, 2i + 1 in
-// byte i).  INT codes: u = n ^ 8 per nibble, spread to bytes (u0 u1 u2 u3),
-// (u4 u5 u6 u7), and converted as E4M3 (exact u 2^-9).
-template <int FMT>
-__device__ __forceinline__ void decode_word_kc(uint32_t w, bool is_int, half2v K2, half2v C2,
-                                               uint32_t (&out)[4])
+// Per-group selector of the IF4 byte mapping: X = 0x08080808, P = 0 for an
+// INT group, X = 0, P = 2 for an FP group (unused by the other formats).
+struct TypeSel {
+    uint32_t X, P;
+};
+
+template <int FMT, int HS>
+__device__ __forceinline__ TypeSel type_sel(const KC& kc)
 {
-    uint32_t x[4];
-    if constexpr (Fmt<FMT>::KIND == kKindInt) {
-        (void)is_int;
-        const uint32_t w4 = w >> 4;
-        const uint32_t d0 = (__builtin_amdgcn_perm(w4, w, 0x05010400u) & 0x0F0F0F0Fu) ^ 0x08080808u;
-        const uint32_t d1 = (__builtin_amdgcn_perm(w4, w, 0x07030602u) & 0x0F0F0F0Fu) ^ 0x08080808u;
-        x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d0, 1.0f, false));
-        x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d0, 1.0f, true));
-        x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d1, 1.0f, false));
-        x[3] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d1, 1.0f, true));
-#pragma unroll
-        for (int i = 0; i < 4; ++i) out[i] = h2_as_u32(__builtin_elementwise_fma(u32_as_h2(x[i]), K2, C2));
-        return;
-    }
-    x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 0));
-    x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 1));
-    x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 2));
-    x[3] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 3));
     if constexpr (Fmt<FMT>::ADAPTIVE) {
-        const uint32_t w4 = w >> 4;
-        const uint32_t d0 = (__builtin_amdgcn_perm(w4, w, 0x05010400u) & 0x0F0F0F0Fu) ^ 0x08080808u;
-        const uint32_t d1 = (__builtin_amdgcn_perm(w4, w, 0x07030602u) & 0x0F0F0F0Fu) ^ 0x08080808u;
-        const uint32_t y0 = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d0, 1.0f, false));
-        const uint32_t y1 = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d0, 1.0f, true));
-        const uint32_t y2 = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d1, 1.0f, false));
-        const uint32_t y3 = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(d1, 1.0f, true));
-        x[0] = is_int ? y0 : x[0];
-        x[1] = is_int ? y1 : x[1];
-        x[2] = is_int ? y2 : x[2];
-        x[3] = is_int ? y3 : x[3];
+        const uint32_t cb = h2_as_u32(kc.C);
+        const bool is_int = HS ? (cb > 0xFFFFu) : ((cb & 0xFFFFu) != 0u);
+        return TypeSel{is_int ? 0x08080808u : 0u, is_int ? 0u : 2u};
+    } else {
+        return TypeSel{0u, 0u};
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) out[i] = h2_as_u32(__builtin_elementwise_fma(u32_as_h2(x[i]), K2, C2));
 }
 
-// One group (two dwords w[0], w[1]) with the constants of half HS of kc.
-template <int FMT, int HS>
-__device__ __forceinline__ void decode_group_kc(const uint32_t* w, const KC& kc, uint32_t (&out)[8])
+// IF4 codes as E4M3 bytes, one code per byte (d holds a code in the low
+// nibble of each byte).  FP group: the sign goes to bit 7 and the three
+// magnitude bits to bits 2..4, which is the E4M3 pattern of the E2M1 value
+// times 2^-6 (subnormal 0.5 included).  INT group: n ^ 8, the E4M3 pattern
+// of (q + 8) 2^-9.  Both types thus share one conversion per two codes.
+__device__ __forceinline__ uint32_t if4_bytes(uint32_t d, const TypeSel& ts)
+{
+    const uint32_t a = d & 0x07070707u;
+    const uint32_t sg = (d & 0x08080808u) ^ ts.X;
+    return ((sg << ts.P) | a) << ts.P;
+}
+
+// Empty asm statements that pin a value to a program point: the slice
+// schedule below places each decode stage between two MFMAs, and without
+// them instruction selection would sink every stage to its last use.
+template <bool ON> __device__ __forceinline__ void pin(uint32_t& a)
+{
+    if constexpr (ON) asm volatile("" : "+v"(a));
+}
+template <bool ON> __device__ __forceinline__ void pin4(uint32_t (&a)[4])
+{
+    if constexpr (ON) asm volatile("" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]));
+}
+
+// Decode of one dword w of eight 4-bit codes (code 2i in the low nibble of
+// byte i) into four FP16 operand pairs, in four stages of a few VALU
+// operations each.  The E4M3 paths (IF4, NVINT4) convert the even codes
+// (low nibbles) and the odd codes (high nibbles) as two byte vectors, so the
+// pairs come out as (0, 2), (4, 6), (1, 3), (5, 7); NVFP4 converts nibble
+// pairs in place: (0, 1), (2, 3), (4, 5), (6, 7).  Both operands of a GEMM
+// are decoded alike, so either order is the same contraction over K.
+//   s1: even codes to bytes (IF4, NVINT4) or the E2M1 conversions (NVFP4)
+//   s2: odd codes to bytes
+//   s3: E4M3 conversions
+//   s4: K x + C
+struct WordDec {
+    uint32_t d0, d1;
+    uint32_t x[4];
+};
+
+template <int FMT, bool PIN>
+__device__ __forceinline__ void wd_s1(uint32_t w, const TypeSel& ts, WordDec& s)
+{
+    pin<PIN>(w);
+    if constexpr (Fmt<FMT>::KIND == kKindInt) {
+        s.d0 = (w & 0x0F0F0F0Fu) ^ 0x08080808u;
+        pin<PIN>(s.d0);
+    } else if constexpr (Fmt<FMT>::ADAPTIVE) {
+        s.d0 = if4_bytes(w, ts);
+        pin<PIN>(s.d0);
+    } else {
+        s.x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 0));
+        s.x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 1));
+        s.x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 2));
+        s.x[3] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 3));
+        pin4<PIN>(s.x);
+    }
+}
+
+template <int FMT, bool PIN>
+__device__ __forceinline__ void wd_s2(uint32_t w, const TypeSel& ts, WordDec& s)
+{
+    if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
+        pin<PIN>(w);
+        const uint32_t w4 = w >> 4;
+        if constexpr (Fmt<FMT>::KIND == kKindInt) s.d1 = (w4 & 0x0F0F0F0Fu) ^ 0x08080808u;
+        else s.d1 = if4_bytes(w4, ts);
+        pin<PIN>(s.d1);
+    }
+}
+
+template <int FMT, bool PIN>
+__device__ __forceinline__ void wd_s3(WordDec& s)
+{
+    if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
+        pin<PIN>(s.d0);
+        pin<PIN>(s.d1);
+        s.x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d0, 1.0f, false));
+        s.x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d0, 1.0f, true));
+        s.x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d1, 1.0f, false));
+        s.x[3] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d1, 1.0f, true));
+        pin4<PIN>(s.x);
+    }
+}
+
+template <int FMT, int HS, bool PIN>
+__device__ __forceinline__ void wd_s4(const WordDec& s, const KC& kc, uint32_t (&out)[4])
 {
     const half2v K2 = {kc.K[HS], kc.K[HS]};
     const half2v C2 = {kc.C[HS], kc.C[HS]};
-    const uint32_t cb = h2_as_u32(kc.C);
-    const bool is_int = Fmt<FMT>::ADAPTIVE && (HS ? (cb > 0xFFFFu) : ((cb & 0xFFFFu) != 0u));
+    uint32_t x[4] = {s.x[0], s.x[1], s.x[2], s.x[3]};
+    pin4<PIN>(x);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[i] = h2_as_u32(__builtin_elementwise_fma(u32_as_h2(x[i]), K2, C2));
+    pin4<PIN>(out);
+}
+
+// One group (two dwords w[0], w[1]) with the constants of half HS of kc,
+// all stages in a row.
+template <int FMT, int HS>
+__device__ __forceinline__ void decode_group_kc(const uint32_t* w, const KC& kc, uint32_t (&out)[8])
+{
+    const TypeSel ts = type_sel<FMT, HS>(kc);
+    WordDec a, b;
     uint32_t o0[4], o1[4];
-    decode_word_kc<FMT>(w[0], is_int, K2, C2, o0);
-    decode_word_kc<FMT>(w[1], is_int, K2, C2, o1);
+    wd_s1<FMT, false>(w[0], ts, a);
+    wd_s2<FMT, false>(w[0], ts, a);
+    wd_s3<FMT, false>(a);
+    wd_s4<FMT, HS, false>(a, kc, o0);
+    wd_s1<FMT, false>(w[1], ts, b);
+    wd_s2<FMT, false>(w[1], ts, b);
+    wd_s3<FMT, false>(b);
+    wd_s4<FMT, HS, false>(b, kc, o1);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         out[i] = o0[i];
@@ -992,16 +1071,37 @@ __device__ __forceinline__ void read_bfrags_fast(const uint8_t* stg, int kk, int
     for (int j = 0; j < 8; ++j) bf[j] = *reinterpret_cast<const half8*>(base + j * 32 * 128);
 }
 
+// B fragments j0, j0 + 1 of slice kk of a decoded stage.
+__device__ __forceinline__ void read_bfrag2(const uint8_t* stg, int kk, int lane, half8 (&bf)[8], int j0)
+{
+    const int h = lane >> 5;
+    const uint8_t* base = stg + (lane & 31) * 128 + 16 * ((4 * h + kk) ^ swz8(lane & 31));
+    bf[j0] = *reinterpret_cast<const half8*>(base + j0 * 32 * 128);
+    bf[j0 + 1] = *reinterpret_cast<const half8*>(base + (j0 + 1) * 32 * 128);
+}
+
 // One K step s = 4 u + Q of the four-step loop body.  c = s / 2 is the A
 // chunk of this step (slot CS = Q / 2), j = Q % 2 the step within it.
+// Each slice kk issues its 16 MFMAs one per slot and places, after each,
+// one piece of the slice's other work, fenced with sched_barrier so that
+// the matrix core never waits behind a long run of VALU work:
+//   slots 0..3 : the next slice's B fragments (two LDS reads per slot)
+//   slots 1..8 : decode of one B group (stages of its two words), stored
+//                to the stage of step s + 2 at slot 8
+//   slots 9..15: decode of one A group into the fragments of a later slice
+//                (this step's second group at kk = 0, 1; the next step's
+//                first group at kk = 2, 3)
+// Every MFMA operand was produced at least one slice earlier.
 template <int FMT, int Q>
 __device__ __forceinline__ void step(const Ctx& x, State& st, int s, int64_t arow0, int arow_local,
                                      uint8_t* Bs, uint8_t* Bn, uint8_t* Bd, floatx16 (&acc)[2][8])
 {
     constexpr int j = Q & 1, CS = Q >> 1;
-    const int lane = threadIdx.x & 63;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
     const int h = lane >> 5;
     const int c = s >> 1;
+    const int swb = swz8(t);
     if constexpr (j == 1) {
         copy_b_chunk(x, min(c + 3, x.nch - 1), x.raw + (CS ^ 1) * kRawBytes);
         if constexpr (Q == 1) {
@@ -1017,56 +1117,116 @@ __device__ __forceinline__ void step(const Ctx& x, State& st, int s, int64_t aro
     KC bkc;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-        const int f = kk & 1;
-        if (kk < 3)
-            read_bfrags_fast(Bs, kk + 1, lane, st.bf[f ^ 1]);
-        else
-            read_bfrags_fast(Bn, 0, lane, st.bf[f ^ 1]);
+        const int f = kk & 1, gg = kk >> 1, par = kk & 1;
+        const uint8_t* nstg = kk < 3 ? Bs : Bn;
+        const int nkk = kk < 3 ? kk + 1 : 0;
+        WordDec b0, b1, a0, a1;
+#define IFQ_MFMA(m) \
+    acc[(m) >> 3][(m) & 7] = __builtin_amdgcn_mfma_f32_32x32x16_f16(st.af[gg][(m) >> 3][par], st.bf[f][(m) & 7], \
+                                                                      acc[(m) >> 3][(m) & 7], 0, 0, 0)
+#define IFQ_SLOT_END() __builtin_amdgcn_sched_barrier(0)
+        IFQ_MFMA(0);
+        read_bfrag2(nstg, nkk, lane, st.bf[f ^ 1], 0);
         if (kk == 0) bkc = pair_kc<FMT>(st.bs & 0xFFFFu);
         if (kk == 2) bkc = pair_kc<FMT>(st.bs >> 16);
-        if (kk == 0) decode_b_fast<FMT, 0>(st, bkc, Bd);
-        if (kk == 1) decode_b_fast<FMT, 1>(st, bkc, Bd);
-        if (kk == 2) decode_b_fast<FMT, 2>(st, bkc, Bd);
-        if (kk == 3) decode_b_fast<FMT, 3>(st, bkc, Bd);
-        if (kk == 3) read_b_raw(x, s + 3, st);
+        const TypeSel bts = (kk & 1) ? type_sel<FMT, 1>(bkc) : type_sel<FMT, 0>(bkc);
+        IFQ_SLOT_END();
+        IFQ_MFMA(1);
+        read_bfrag2(nstg, nkk, lane, st.bf[f ^ 1], 2);
+        wd_s1<FMT, true>(st.bw[2 * kk], bts, b0);
+        IFQ_SLOT_END();
+        IFQ_MFMA(2);
+        read_bfrag2(nstg, nkk, lane, st.bf[f ^ 1], 4);
+        wd_s2<FMT, true>(st.bw[2 * kk], bts, b0);
+        IFQ_SLOT_END();
+        IFQ_MFMA(3);
+        read_bfrag2(nstg, nkk, lane, st.bf[f ^ 1], 6);
+        wd_s3<FMT, true>(b0);
+        IFQ_SLOT_END();
+        IFQ_MFMA(4);
+        uint32_t v0[4], v1[4];
+        if (kk & 1) wd_s4<FMT, 1, true>(b0, bkc, v0); else wd_s4<FMT, 0, true>(b0, bkc, v0);
+        IFQ_SLOT_END();
+        IFQ_MFMA(5);
+        wd_s1<FMT, true>(st.bw[2 * kk + 1], bts, b1);
+        IFQ_SLOT_END();
+        IFQ_MFMA(6);
+        wd_s2<FMT, true>(st.bw[2 * kk + 1], bts, b1);
+        IFQ_SLOT_END();
+        IFQ_MFMA(7);
+        wd_s3<FMT, true>(b1);
+        IFQ_SLOT_END();
+        IFQ_MFMA(8);
+        if (kk & 1) wd_s4<FMT, 1, true>(b1, bkc, v1); else wd_s4<FMT, 0, true>(b1, bkc, v1);
+        {
+            // B group kk of row t: pieces 2 kk and 2 kk + 1 of the stage row
+            uint8_t* row = Bd + t * 128;
+            *reinterpret_cast<u32x4*>(row + 16 * ((2 * kk) ^ swb)) = u32x4{v0[0], v0[1], v0[2], v0[3]};
+            *reinterpret_cast<u32x4*>(row + 16 * ((2 * kk + 1) ^ swb)) = u32x4{v1[0], v1[1], v1[2], v1[3]};
+        }
+        IFQ_SLOT_END();
+        IFQ_MFMA(9);
+        // the A group of this slice: kk < 2: local group 2 j + 1 of chunk c,
+        // row block kk (constants computed with group 2 j); kk >= 2: the
+        // first group of the next step, row block kk - 2 -- local group 0 of
+        // chunk c + 1 (j = 1, loaded two steps ago; then slot CS, whose last
+        // group was decoded at kk = 1, is refilled) or local group 2 of chunk
+        // c (j = 0)
+        uint32_t aw0, aw1;
+        KC akc;
         if (kk < 2) {
-            // group 1 of this step: local group 2 j + 1 of chunk c, whose pair
-            // constants were computed with group 2 j
-            decode_a_fast<FMT, 2 * j + 1>(st.a[CS][kk], st.akc[kk], st.af[1][kk][0], st.af[1][kk][1]);
+            aw0 = st.a[CS][kk][j][2];
+            aw1 = st.a[CS][kk][j][3];
+            akc = st.akc[kk];
         } else {
             if constexpr (j == 1) {
                 if (kk == 2) {
-                    // chunk c + 1 (loaded two steps ago) must have landed; then
-                    // refill slot CS, whose last group was decoded above
                     vm_wait<Q == 1 ? 6 : 4>(st.a[CS ^ 1][0][0], st.a[CS ^ 1][0][1], st.a[CS ^ 1][1][0],
                                             st.a[CS ^ 1][1][1]);
                     load_a_chunk(x, arow0, h, min(c + 2, x.nch - 1), st.a[CS]);
                 }
-                // group 0 of the next step: local group 0 of chunk c + 1
                 st.akc[kk - 2] = pair_kc<FMT>(st.as[CS ^ 1][kk - 2] & 0xFFFFu);
-                decode_a_fast<FMT, 0>(st.a[CS ^ 1][kk - 2], st.akc[kk - 2], st.af[0][kk - 2][0],
-                                      st.af[0][kk - 2][1]);
+                aw0 = st.a[CS ^ 1][kk - 2][0][0];
+                aw1 = st.a[CS ^ 1][kk - 2][0][1];
             } else {
-                // group 0 of the next step: local group 2 of chunk c
                 st.akc[kk - 2] = pair_kc<FMT>(st.as[CS][kk - 2] >> 16);
-                decode_a_fast<FMT, 2>(st.a[CS][kk - 2], st.akc[kk - 2], st.af[0][kk - 2][0],
-                                      st.af[0][kk - 2][1]);
+                aw0 = st.a[CS][kk - 2][1][0];
+                aw1 = st.a[CS][kk - 2][1][1];
             }
+            akc = st.akc[kk - 2];
         }
-        const int gg = kk >> 1, par = kk & 1;
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int jb = 0; jb < 8; ++jb)
-                acc[i][jb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(st.af[gg][i][par], st.bf[f][jb], acc[i][jb], 0, 0, 0);
-#pragma unroll
-        for (int m = 0; m < 16; ++m) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
-            if (m < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            if (m == 3 || m == 7) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+        const TypeSel ats = (kk < 2) ? type_sel<FMT, 1>(akc) : type_sel<FMT, 0>(akc);
+        wd_s1<FMT, true>(aw0, ats, a0);
+        IFQ_SLOT_END();
+        IFQ_MFMA(10);
+        wd_s2<FMT, true>(aw0, ats, a0);
+        IFQ_SLOT_END();
+        IFQ_MFMA(11);
+        wd_s3<FMT, true>(a0);
+        IFQ_SLOT_END();
+        IFQ_MFMA(12);
+        uint32_t o0[4], o1[4];
+        if (kk < 2) wd_s4<FMT, 1, true>(a0, akc, o0); else wd_s4<FMT, 0, true>(a0, akc, o0);
+        wd_s1<FMT, true>(aw1, ats, a1);
+        IFQ_SLOT_END();
+        IFQ_MFMA(13);
+        wd_s2<FMT, true>(aw1, ats, a1);
+        IFQ_SLOT_END();
+        IFQ_MFMA(14);
+        wd_s3<FMT, true>(a1);
+        IFQ_SLOT_END();
+        IFQ_MFMA(15);
+        if (kk < 2) wd_s4<FMT, 1, true>(a1, akc, o1); else wd_s4<FMT, 0, true>(a1, akc, o1);
+        {
+            const half8 f0 = __builtin_bit_cast(half8, u32x4{o0[0], o0[1], o0[2], o0[3]});
+            const half8 f1 = __builtin_bit_cast(half8, u32x4{o1[0], o1[1], o1[2], o1[3]});
+            st.af[kk < 2 ? 1 : 0][kk & 1][0] = f0;
+            st.af[kk < 2 ? 1 : 0][kk & 1][1] = f1;
         }
-        __builtin_amdgcn_sched_barrier(0);
+        if (kk == 3) read_b_raw(x, s + 3, st);
+        IFQ_SLOT_END();
+#undef IFQ_MFMA
+#undef IFQ_SLOT_END
     }
     // even steps: the copies of the last odd step (B codes, scales) must have
     // landed before the barrier makes them visible
