@@ -824,9 +824,10 @@ __device__ __forceinline__ uint32_t if4_bytes(uint32_t d, const TypeSel& ts)
     return ((sg << ts.P) | a) << ts.P;
 }
 
-// Empty asm statements that pin a value to a program point: the slice
-// schedule below places each decode stage between two MFMAs, and without
-// them instruction selection would sink every stage to its last use.
+// Empty asm statements that pin a stage's results to a program point: the
+// slice schedule below places each decode stage between two MFMAs, and
+// without them instruction selection would sink every stage to the last
+// use of its results.
 template <bool ON> __device__ __forceinline__ void pin(uint32_t& a)
 {
     if constexpr (ON) asm volatile("" : "+v"(a));
@@ -855,7 +856,6 @@ struct WordDec {
 template <int FMT, bool PIN>
 __device__ __forceinline__ void wd_s1(uint32_t w, const TypeSel& ts, WordDec& s)
 {
-    pin<PIN>(w);
     if constexpr (Fmt<FMT>::KIND == kKindInt) {
         s.d0 = (w & 0x0F0F0F0Fu) ^ 0x08080808u;
         pin<PIN>(s.d0);
@@ -875,7 +875,6 @@ template <int FMT, bool PIN>
 __device__ __forceinline__ void wd_s2(uint32_t w, const TypeSel& ts, WordDec& s)
 {
     if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
-        pin<PIN>(w);
         const uint32_t w4 = w >> 4;
         if constexpr (Fmt<FMT>::KIND == kKindInt) s.d1 = (w4 & 0x0F0F0F0Fu) ^ 0x08080808u;
         else s.d1 = if4_bytes(w4, ts);
@@ -887,8 +886,6 @@ template <int FMT, bool PIN>
 __device__ __forceinline__ void wd_s3(WordDec& s)
 {
     if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
-        pin<PIN>(s.d0);
-        pin<PIN>(s.d1);
         s.x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d0, 1.0f, false));
         s.x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d0, 1.0f, true));
         s.x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d1, 1.0f, false));
@@ -902,10 +899,8 @@ __device__ __forceinline__ void wd_s4(const WordDec& s, const KC& kc, uint32_t (
 {
     const half2v K2 = {kc.K[HS], kc.K[HS]};
     const half2v C2 = {kc.C[HS], kc.C[HS]};
-    uint32_t x[4] = {s.x[0], s.x[1], s.x[2], s.x[3]};
-    pin4<PIN>(x);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) out[i] = h2_as_u32(__builtin_elementwise_fma(u32_as_h2(x[i]), K2, C2));
+    for (int i = 0; i < 4; ++i) out[i] = h2_as_u32(__builtin_elementwise_fma(u32_as_h2(s.x[i]), K2, C2));
     pin4<PIN>(out);
 }
 
