@@ -91,6 +91,48 @@ def test_shapes_k_multiple_of_512(fmt, dtype):
         _check(fmt, pa, oa, pb, ob, dtype, tag=f"{fmt} {M}x{N}x{K}")
 
 
+def _packed_from_arrays(fmt, codes, scales, alpha=1.0):
+    R, K = codes.shape[0], scales.shape[1] * ops.GSIZE[fmt]
+    ts = torch.tensor([alpha], dtype=torch.float32, device="cuda")
+    return ops.Packed(fmt, torch.from_numpy(codes).cuda(), torch.from_numpy(scales).cuda(), ts, R, K)
+
+
+@pytest.mark.parametrize("fmt", [ops.IF4, ops.NVFP4, ops.NVINT4])
+def test_every_code_and_scale_byte(fmt):
+    """Packed operands written directly: every 4-bit code, every finite E4M3
+    scale byte and, for IF4, both values of the indicator bit (both group
+    types), at shapes whose interior tiles take the fast kernel.  Case 1:
+    each row has one scale byte for all its groups (rows cycle through the
+    bytes), so every output is a sum of terms of one magnitude and a wrong
+    decode at any scale, down to the E4M3 subnormals, shows against the
+    elementwise bound; the folded FP16 operands are exact, so the fp32
+    result differs from the fp64 product of the oracle-dequantized operands
+    only by accumulation rounding.  Case 2: random scale bytes per group
+    (types mixed along K), relative Frobenius error."""
+    rng = np.random.default_rng(70 + fmt)
+    top = 256 if fmt == ops.IF4 else 128
+    byte_vals = np.array([b for b in range(top) if (b & 0x7F) != 0x7F], dtype=np.uint8)
+    for (M, N, K) in [(256, 256, 512), (512, 288, 1024)]:
+        ca = rng.integers(0, 256, (M, K // 2), dtype=np.uint8)
+        cb = rng.integers(0, 256, (N, K // 2), dtype=np.uint8)
+        sa = np.repeat(byte_vals[np.arange(M) % len(byte_vals)][:, None], K // 16, axis=1)
+        sb = np.repeat(byte_vals[(7 * np.arange(N) + 3) % len(byte_vals)][:, None], K // 16, axis=1)
+        c = ops.ifx_gemm(_packed_from_arrays(fmt, ca, sa), _packed_from_arrays(fmt, cb, sb),
+                         ops.F32).cpu().numpy().astype(np.float64)
+        A = O.dequantize(ca, sa, 1.0, fmt, np.float64)
+        B = O.dequantize(cb, sb, 1.0, fmt, np.float64)
+        ref = A @ B.T
+        bound = 3e-5 * (np.abs(A) @ np.abs(B).T)
+        bad = np.abs(c - ref) > bound
+        assert not bad.any(), (fmt, M, N, K, np.argwhere(bad)[:3], sa[np.argwhere(bad)[0][0], 0])
+        sa = rng.choice(byte_vals, (M, K // 16)).astype(np.uint8)
+        sb = rng.choice(byte_vals, (N, K // 16)).astype(np.uint8)
+        c = ops.ifx_gemm(_packed_from_arrays(fmt, ca, sa), _packed_from_arrays(fmt, cb, sb),
+                         ops.F32).cpu().numpy()
+        ref = O.gemm_ref(ca, sa, 1.0, cb, sb, 1.0, fmt)
+        assert rel_fro(c, ref) <= 1e-6, (fmt, M, N, K)
+
+
 def test_unaligned_scales_take_the_general_path():
     """Scale buffers that start 4 bytes past a 16-byte boundary cannot use the
     line-sized operand copies (codes must be 16-byte aligned by contract);
