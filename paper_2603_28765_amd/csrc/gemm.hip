@@ -794,19 +794,21 @@ __device__ __forceinline__ KC pair_kc(uint32_t sw)
     return r;
 }
 
-// Per-group selector of the IF4 byte mapping: X = 0x08080808, P = 0 for an
-// INT group, X = 0, P = 2 for an FP group (unused by the other formats).
+// Per-group selector of the IF4 byte mapping: M = all ones, P = 0 for an INT
+// group, M = 0, P = 2 for an FP group (unused by the other formats).  M is
+// the sign of the group's C (negative exactly for INT groups; a zero INT
+// scale gives C = -0 or +0, and K = 0 makes the group zero either way).
 struct TypeSel {
-    uint32_t X, P;
+    uint32_t M, P;
 };
 
 template <int FMT, int HS>
 __device__ __forceinline__ TypeSel type_sel(const KC& kc)
 {
     if constexpr (Fmt<FMT>::ADAPTIVE) {
-        const uint32_t cb = h2_as_u32(kc.C);
-        const bool is_int = HS ? (cb > 0xFFFFu) : ((cb & 0xFFFFu) != 0u);
-        return TypeSel{is_int ? 0x08080808u : 0u, is_int ? 0u : 2u};
+        const int32_t cb = (int32_t)h2_as_u32(kc.C);
+        const uint32_t m = (uint32_t)(HS ? (cb >> 31) : ((cb << 16) >> 31));
+        return TypeSel{m, ~m & 2u};
     } else {
         return TypeSel{0u, 0u};
     }
@@ -820,7 +822,7 @@ __device__ __forceinline__ TypeSel type_sel(const KC& kc)
 __device__ __forceinline__ uint32_t if4_bytes(uint32_t d, const TypeSel& ts)
 {
     const uint32_t a = d & 0x07070707u;
-    const uint32_t sg = (d & 0x08080808u) ^ ts.X;
+    const uint32_t sg = (d ^ ts.M) & 0x08080808u;
     return ((sg << ts.P) | a) << ts.P;
 }
 
