@@ -117,7 +117,7 @@ enum {
  * Follows Eq. 1 and 2 and Fig. 3a of the paper: alpha from the tensor
  * maximum, Delta per group rounded to E4M3, then for IF formats both an FP
  * and a scaled-INT candidate with the INT one kept only if its squared
- * error is strictly smaller (Fig. 3a line 10).
+ * error is strictly smaller (Fig. 3a (selection)).
  *
  *   x             (device) bf16 [rows, ld_x], ld_x >= cols; row-wise: 16-byte
  *                 aligned with ld_x % 8 == 0; strided axis: any alignment
@@ -152,7 +152,7 @@ int if4_quantize(const void* x, int64_t rows, int64_t cols, int64_t ld_x, uint32
                  uint32_t rht_signs, uint64_t seed, uint8_t* codes, uint8_t* scales,
                  float* tensor_scale, void* workspace, size_t workspace_bytes, void* stream);
 
-/* NVFP4 (Fig. 3a lines 1-4 only): same arguments, bit 7 of every scale is 0. */
+/* NVFP4 (Fig. 3a up to the FP candidate): same arguments, bit 7 of every scale is 0. */
 int nvfp4_quantize(const void* x, int64_t rows, int64_t cols, int64_t ld_x, uint32_t flags,
                    uint32_t rht_signs, uint64_t seed, uint8_t* codes, uint8_t* scales,
                    float* tensor_scale, void* workspace, size_t workspace_bytes, void* stream);
@@ -207,7 +207,7 @@ size_t ifq_quantize_dual_workspace_bytes(int format, int64_t rows, int64_t cols,
 
 /* ---------------------------------------------------------- dequantize --
  * out[r, k] = q * Delta * (M_FP/M_I if INT) * alpha (the factor is 1 for
- * NVINT4), evaluated as three fp32 multiplies in that order (Fig. 3a lines 5 and 8 with alpha restored); the
+ * NVINT4), evaluated as three fp32 multiplies in that order (the dequantized values of Fig. 3a with alpha restored); the
  * bf16 output is the round-to-nearest-even of that fp32 value.
  *   codes, scales  (device) packed [R, K] as written by the quantizer
  *   tensor_scale   (device) alpha

@@ -136,7 +136,7 @@ static void ensure_init(void)
 {
     if (g_init) return;
     init_fmt(&g_fmt[FMT_IF4], 4, 2, 1, KIND_ADAPTIVE);       /* E2M1 / INT4, Sec. 3 */
-    init_fmt(&g_fmt[FMT_NVFP4], 4, 2, 1, KIND_FP);           /* E2M1 only, Fig. 3a lines 1-4 */
+    init_fmt(&g_fmt[FMT_NVFP4], 4, 2, 1, KIND_FP);           /* E2M1 only: Fig. 3a up to the FP candidate */
     init_fmt(&g_fmt[FMT_IF3], 3, 2, 0, KIND_ADAPTIVE);       /* E2M0 / INT3, Sec. 5.1 */
     init_fmt(&g_fmt[FMT_IF6_E2M3], 6, 2, 3, KIND_ADAPTIVE);  /* E2M3 / INT6, Table 6 */
     init_fmt(&g_fmt[FMT_IF6_E3M2], 6, 3, 2, KIND_ADAPTIVE);  /* E3M2 / INT6, Table 6 */
@@ -319,7 +319,7 @@ float oracle_tensor_scale(int fmt, float amax, uint32_t flags)
 
 /* ------------------------------------------------------ one group -- */
 
-/* The two candidates of one group (Fig. 3a lines 4-9) for scaled values
+/* The two candidates of one group (Fig. 3a) for scaled values
  * xb: codes cf (FP) and ci (INT) and their squared errors, with
  * round-to-nearest-even or, with sr, stochastic rounding by h. */
 static void candidates(const fmt_desc* f, const float xb[GROUP], int sr, const uint16_t h[GROUP],
@@ -328,7 +328,7 @@ static void candidates(const fmt_desc* f, const float xb[GROUP], int sr, const u
     const int n = f->gsize;
     const int sign_bit = 1 << (f->bits - 1);
     const int code_mask = (1 << f->bits) - 1;
-    /* FP candidate (Fig. 3a lines 4-6). */
+    /* FP candidate (Fig. 3a). */
     float ef = 0.0f;
     for (int j = 0; j < n; ++j) {
         double m = fabs((double)xb[j]);
@@ -355,7 +355,7 @@ static void candidates(const fmt_desc* f, const float xb[GROUP], int sr, const u
         ef = fmaf(d, d, ef);
     }
 
-    /* INT candidate (Fig. 3a lines 7-9): int(x-bar * M_I/M_FP), clamped to
+    /* INT candidate (Fig. 3a): int(x-bar * M_I/M_FP), clamped to
      * +-M_I, reconstructed as code * M_FP/M_I. */
     float ei = 0.0f;
     for (int j = 0; j < n; ++j) {
@@ -384,7 +384,7 @@ static void candidates(const fmt_desc* f, const float xb[GROUP], int sr, const u
 }
 
 /* Quantize one group of 16 values v (already transformed when the RHT is
- * on) under tensor scale alpha; Fig. 3a lines 1-10 with alpha restored
+ * on) under tensor scale alpha; Fig. 3a with alpha restored
  * (Eq. 2 divides by alpha * M_FP).
  *   h      16-bit uniforms for stochastic rounding (ignored without F_SR)
  *   codes  out: 16 element codes (low `bits` bits used)
@@ -466,7 +466,7 @@ void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t 
         return;
     }
 
-    /* Fig. 3a line 1 / Eq. (2): Delta = max|X_g| / (alpha * M). */
+    /* Fig. 3a, Eq. (2): Delta = max|X_g| / (alpha * M). */
     float amax_g = 0.0f;
     for (int j = 0; j < n; ++j) {
         float a = fabsf(v[j]);
@@ -474,11 +474,11 @@ void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t 
     }
     float denom = alpha * scale_max(f, flags);
     float delta_raw = amax_g / denom;
-    /* Fig. 3a line 2: cast to E4M3 (round to nearest even, saturating). */
+    /* Fig. 3a: cast to E4M3 (round to nearest even, saturating). */
     int dcode = (denom > 0.0f) ? oracle_e4m3_encode(delta_raw) : 0;
     float delta = (float)oracle_e4m3_value(dcode);
 
-    /* Scaled values x-bar = X / (alpha * Delta) (Fig. 3a line 3, alpha from
+    /* Scaled values x-bar = X / (alpha * Delta) (Fig. 3a, alpha from
      * Eq. 1), as a multiply by the rounded reciprocal.  A group whose
      * combined scale is zero or below the smallest normal fp32 stores zeros. */
     float s = alpha * delta;
@@ -505,7 +505,7 @@ void oracle_quantize_group(int fmt, const float v[GROUP], float alpha, uint32_t 
         candidates(f, xb, 0, h, rf, ri, &sel_f, &sel_i);
     }
 
-    /* Fig. 3a line 10: INT only if strictly better; Sec. 3: the choice is
+    /* Fig. 3a (selection): INT only if strictly better; Sec. 3: the choice is
      * recorded in the scale's sign bit.  NVINT4 always stores INT codes and
      * its scale is a plain E4M3 value (bit 7 clear). */
     int use_int = f->adaptive && (sel_i < sel_f);
@@ -645,7 +645,7 @@ int oracle_quantize(int fmt, const uint16_t* x, int64_t rows, int64_t cols, int6
     return 0;
 }
 
-/* Dequantized value of one element (Fig. 3a lines 5 and 8 with alpha):
+/* Dequantized value of one element (Fig. 3a's dequantized values with alpha):
  * q * Delta, times M_FP/M_I for INT groups of the IF formats (1 for
  * NVINT4), times alpha, each step an fp32
  * multiply in that order (q * Delta is exact). */

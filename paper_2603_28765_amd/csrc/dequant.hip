@@ -1,5 +1,5 @@
 // dequant.hip -- standalone dequantization: q * Delta [* M_FP/M_I] * alpha
-// (Fig. 3a lines 5 and 8 with the tensor scale of Eq. 1), one group of 16 per
+// (the dequantized values of Fig. 3a with the tensor scale of Eq. 1), one group of 16 per
 // lane, written as fp32 or bf16.
 #include "device.h"
 #include "launch.h"

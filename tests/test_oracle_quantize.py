@@ -3,7 +3,7 @@
 - Fig. 3a worked example (tests/golden/fig3a_worked_example.json), exact.
 - Brute force over every code vector of tiny groups: the FP and INT
   candidates are the least-squares code vectors and the selection takes the
-  type with the smaller error (Fig. 3a line 10), checked in exact rationals.
+  type with the smaller error (Fig. 3a (selection)), checked in exact rationals.
 - IF4's error never exceeds NVFP4's on the same group, and an IF4 group that
   keeps FP is bit-identical to the NVFP4 encoding (Sec. 3).
 - Exact round trips of values already on the FP or scaled-INT grid (Eq. 1-2).
@@ -38,20 +38,20 @@ def test_fig3a_worked_example_alpha_one(oracle):
     codes, sb, e_fp, e_int = oracle.quantize_group(v, 1.0, oracle.FMT_IF4, oracle.SCALE_IN)
     delta = oracle.e4m3_value(sb & 0x7F)
     assert delta == ex["line2_delta_e4m3"] == ex["line1_delta_before_cast"]
-    # INT selected: sign bit of the scale set (Sec. 3), codes = line 7 / line 10
+    # INT selected: sign bit of the scale set (Sec. 3), codes of the INT candidate
     assert sb & 0x80
     assert [int(c) for c in codes[:4]] == ex["line10_selected"] == ex["line7_int4_values"]
     assert all(c == 0 for c in codes[4:])
-    # errors are kept in x-bar units; times Delta^2 they are line 6 and line 9.
+    # errors are kept in x-bar units; times Delta^2 they are the errors of Fig. 3a.
     # The printed 46.0 is the sum of squares (1 + 9 + 36 + 0), not the mean.
     assert e_fp * delta ** 2 == pytest.approx(ex["line6_fp_error_printed"], rel=1e-6)
     assert e_int * delta ** 2 == pytest.approx(ex["line9_int_error_printed"], abs=1e-9)
-    # the FP candidate itself (NVFP4 ends at line 4)
+    # the FP candidate itself (NVFP4 stops at the FP candidate)
     nv_codes, nv_sb, _, _ = oracle.quantize_group(v, 1.0, oracle.FMT_NVFP4, oracle.SCALE_IN)
     fp_vals = [oracle.fp_magnitude(oracle.FMT_NVFP4, c & 7) for c in nv_codes[:4]]
     assert fp_vals == ex["line4_fp4_values"]
     assert nv_sb == sb & 0x7F
-    # dequantized values: line 5 (FP) and line 8 (INT)
+    # dequantized values of both candidates
     packed = oracle.pack_group(oracle.FMT_IF4, codes)[None, :]
     deq = oracle.dequantize(packed, np.array([[sb]], np.uint8), 1.0)[0, :4]
     assert list(deq) == ex["line8_int_dequant"]
@@ -125,7 +125,7 @@ def test_bruteforce_tiny_groups(oracle, fmt):
         assert all(q == 0 for q in codes[3:])
         tol = Fraction(1, 10 ** 5) * max(best_fp, best_int, Fraction(1, 10 ** 30))
         assert chosen <= min(best_fp, best_int) + tol
-        # selection: strict "<" in favour of INT (Fig. 3a line 10)
+        # selection: strict "<" in favour of INT (Fig. 3a (selection))
         if abs(best_int - best_fp) > tol:
             assert is_int == (best_int < best_fp)
         # the fp32 errors track the exact ones
@@ -239,7 +239,7 @@ def test_table1_max_min_values(oracle):
 
 
 def test_selection_tie_goes_to_fp(oracle):
-    """Fig. 3a line 10 takes INT only when its error is strictly smaller.
+    """Fig. 3a (selection) takes INT only when its error is strictly smaller.
     An outlier group whose small values round to zero in both candidates
     gives bit-identical fp32 errors (the max is exact in both, and the INT
     max's 7*fp32(6/7) - 6 residue is absorbed by the larger sum), so the
