@@ -44,7 +44,7 @@ def parse():
                                         "nvfp4_46", "if4_bs8", "if3_bs8", "nvfp4_bs8"], default="if4",
                    help="format of the --mode step run")
     p.add_argument("--small", action="store_true", help="1/8-size shapes (quick checks)")
-    p.add_argument("--mode", choices=["full", "step", "copy", "wgrad", "bitwidth", "dual"], default="full",
+    p.add_argument("--mode", choices=["full", "step", "copy", "wgrad", "bitwidth", "dual", "dequant"], default="full",
                    help="step: only the timed IF4 step (for counter runs); copy: a plain 1 GiB "
                         "device copy, the reference for scaling the HBM byte counters")
     return p.parse_args()
@@ -83,6 +83,9 @@ def main():
         return
     if args.mode == "dual":
         print(json.dumps({"mode": "dual", **dual_times(ops, workloads, torch)}))
+        return
+    if args.mode == "dequant":
+        print(json.dumps({"mode": "dequant", **dequant_times(ops, workloads, torch)}))
         return
     div = 8 if args.small else 1
     M, N, K = 8192 // div, 14336 // div, 4096 // div
@@ -323,6 +326,31 @@ def dual_times(ops, workloads, torch):
     t_g = _event_time(torch, lambda: ops.if4_gemm(pdy, pw, ops.BF16, out), 20, 5)
     res["dgrad"] = {"workload": f"dgrad_{M}x{N}x{K}", "gemm_us": round(t_g * 1e6, 1),
                     "gemm_TFLOPs": round(2.0 * M * N * K / t_g / 1e12, 1)}
+    return res
+
+
+def dequant_times(ops, workloads, torch):
+    """Standalone dequantizer on the weights W 14336 x 4096 in every format,
+    bf16 and fp32 out, cache flushed before every launch.  Algorithmic bytes
+    per element: codes b/8 + scales 1/G read, 2 or 4 written."""
+    W = workloads.fwd_mlp().tensors["W"].cuda()
+    n = W.numel()
+    ws = torch.empty(4096, dtype=torch.uint8, device="cuda")
+    flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device="cuda")
+    res = {"workload": f"dequant_{W.shape[0]}x{W.shape[1]}"}
+    for fmt, name in ops.FORMAT_NAMES.items():
+        p = ops.ifx_quantize(fmt, W, workspace=ws)
+        read = ops.BITS[fmt] / 8 + 1 / ops.GSIZE[fmt]
+        r = {}
+        for dt, tag, wb in ((ops.BF16, "bf16", 2), (ops.F32, "fp32", 4)):
+            out = ops.ifx_dequantize(p, dt)
+            t = _event_time(torch, lambda: ops.ifx_dequantize(p, dt, out), 10, 2, flush)
+            r[tag + "_us"] = round(t * 1e6, 1)
+            r[tag + "_GBps"] = round(n * (read + wb) / t / 1e9, 1)
+            del out
+        res[name] = r
+        del p
+    del flush
     return res
 
 

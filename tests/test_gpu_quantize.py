@@ -181,6 +181,32 @@ def test_dequantize_bit_exact(fmt, dtype):
             np.testing.assert_array_equal(got, O.bf16_bits(ref))
 
 
+ADAPTIVE_FORMATS = (ops.IF4, ops.IF3, ops.IF6_E2M3, ops.IF6_E3M2, ops.IF4_BS8, ops.IF3_BS8)
+
+
+@pytest.mark.parametrize("fmt", FORMATS)
+def test_dequantize_every_code_and_scale_byte(fmt):
+    """Packed data written directly: random code bits (every code value),
+    every finite scale byte (with the indicator bit for the adaptive
+    formats), and tensor scales that push the products into fp32 subnormals
+    and near the top of the range; fp32 and bf16 outputs bit for bit."""
+    rng = np.random.default_rng(120 + fmt)
+    rows, cols = 96, 1024
+    g = ops.GSIZE[fmt]
+    codes = rng.integers(0, 256, (rows, cols * ops.BITS[fmt] // 8), dtype=np.uint8)
+    top = 256 if fmt in ADAPTIVE_FORMATS else 128
+    vals = np.array([b for b in range(top) if (b & 0x7F) != 0x7F], dtype=np.uint8)
+    scales = vals[np.arange(rows * cols // g) % len(vals)].reshape(rows, cols // g)
+    for alpha in (1.0, 2.0 ** -120, 3.7e5):
+        ts = torch.tensor([alpha], dtype=torch.float32, device="cuda")
+        p = ops.Packed(fmt, torch.from_numpy(codes).cuda(), torch.from_numpy(scales).cuda(), ts, rows, cols)
+        ref = O.dequantize(codes, scales, np.float32(alpha), fmt)
+        got = ops.ifx_dequantize(p, ops.F32).cpu().numpy()
+        np.testing.assert_array_equal(got.view(np.uint32), ref.view(np.uint32), err_msg=f"fp32 alpha {alpha}")
+        got16 = ops.ifx_dequantize(p, ops.BF16).cpu().view(torch.int16).numpy().view(np.uint16)
+        np.testing.assert_array_equal(got16, O.bf16_bits(ref), err_msg=f"bf16 alpha {alpha}")
+
+
 def test_full_size_quant_sweep():
     """8192x8192 t(3) with outlier columns: IF4 and NVFP4, with and without
     the RHT, bit-exact over the whole tensor."""
