@@ -197,14 +197,16 @@ __device__ __forceinline__ void rht16(float (&v)[kGroup], uint32_t signs)
 }
 
 // ---------------------------------------------------- FP element rounding
-// Magnitude of non-negative FP code `idx`.
+// Magnitude of non-negative FP code `idx` (both forms computed and selected:
+// a branch here diverges per element).
 template <int FMT> __device__ __forceinline__ float fp_magnitude(uint32_t idx)
 {
     using F = Fmt<FMT>;
     constexpr int BIAS = FmtDerived<FMT>::BIAS;
-    uint32_t E = idx >> F::MB, M = idx & ((1u << F::MB) - 1u);
-    if (E == 0) return (float)M * __uint_as_float((uint32_t)(127 + 1 - BIAS - F::MB) << 23);
-    return __uint_as_float(((E - BIAS + 127u) << 23) | (M << (23 - F::MB)));
+    const uint32_t E = idx >> F::MB, M = idx & ((1u << F::MB) - 1u);
+    const float sub = (float)M * __uint_as_float((uint32_t)(127 + 1 - BIAS - F::MB) << 23);
+    const float nor = __uint_as_float(((E - BIAS + 127u) << 23) | (M << (23 - F::MB)));
+    return E ? nor : sub;
 }
 
 // Nearest FP code index to m >= 0 (ties to the even code), saturating.
