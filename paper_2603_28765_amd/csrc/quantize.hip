@@ -38,16 +38,58 @@ __device__ __forceinline__ float block_max(float m, float* red)
     return r;
 }
 
-__device__ __forceinline__ void load_group_rowwise(const uint16_t* p, float (&v)[kGroup])
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// 16 bf16 values (two 16-byte pieces, low piece first) as floats
+__device__ __forceinline__ void unpack_group(u32x4 a, u32x4 b, float (&v)[kGroup])
 {
-    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-    const u32x4* q = reinterpret_cast<const u32x4*>(p);
-    u32x4 a = __builtin_nontemporal_load(q);
-    u32x4 b = __builtin_nontemporal_load(q + 1);
     v[0] = bf16lo(a.x);  v[1] = bf16hi(a.x);  v[2] = bf16lo(a.y);  v[3] = bf16hi(a.y);
     v[4] = bf16lo(a.z);  v[5] = bf16hi(a.z);  v[6] = bf16lo(a.w);  v[7] = bf16hi(a.w);
     v[8] = bf16lo(b.x);  v[9] = bf16hi(b.x);  v[10] = bf16lo(b.y); v[11] = bf16hi(b.y);
     v[12] = bf16lo(b.z); v[13] = bf16hi(b.z); v[14] = bf16lo(b.w); v[15] = bf16hi(b.w);
+}
+
+__device__ __forceinline__ void load_group_rowwise(const uint16_t* p, float (&v)[kGroup])
+{
+    const u32x4* q = reinterpret_cast<const u32x4*>(p);
+    unpack_group(__builtin_nontemporal_load(q), __builtin_nontemporal_load(q + 1), v);
+}
+
+// 64 consecutive groups (2 KiB at p, 16-byte aligned) read by one wavefront
+// with two loads that each cover 1 KiB contiguously (a lane's two 16-byte
+// pieces of one group would otherwise sit 32 bytes apart in every load, and
+// each load would touch twice the cache lines): lane l reads pieces
+// 2(l mod 32) + l/32 and 64 + 2(l mod 32) + l/32.  Lane l < 32 then holds the
+// first half of group l and of group 32 + l, lane l + 32 their second halves;
+// one swap across the wavefront's halves per dword leaves group l whole in
+// lane l.  Every lane of the wavefront must be active.
+__device__ __forceinline__ void load_wave_raw(const uint16_t* p, u32x4& a, u32x4& b)
+{
+    const int lane = threadIdx.x & 63;
+    const int piece = 2 * (lane & 31) + (lane >> 5);
+    const u32x4* q = reinterpret_cast<const u32x4*>(p);
+    a = __builtin_nontemporal_load(q + piece);
+    b = __builtin_nontemporal_load(q + 64 + piece);
+}
+
+__device__ __forceinline__ void wave_groups(u32x4 a, u32x4 b, float (&v)[kGroup])
+{
+    u32x4 lo, hi;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        const auto r = __builtin_amdgcn_permlane32_swap(a[d], b[d], false, false);
+        lo[d] = r[0];
+        hi[d] = r[1];
+    }
+    unpack_group(lo, hi, v);
+}
+
+__device__ __forceinline__ void load_wave_group(const uint16_t* p, float (&v)[kGroup])
+{
+    u32x4 a, b;
+    load_wave_raw(p, a, b);
+    wave_groups(a, b, v);
 }
 
 // alpha for this launch: the caller's, or Eq. 1 from the pass-1 partials.
@@ -64,8 +106,28 @@ __device__ __forceinline__ float resolve_alpha(bool scale_in, float* tensor_scal
     return alpha;
 }
 
+// Non-temporal stores: the outputs are written once and not read back by
+// this launch, and streaming them past the caches keeps the write path at
+// full rate (a wavefront's stores still cover whole lines).
+template <int BITS> __device__ __forceinline__ void store_packed_nt(uint8_t* dst, const Packed<BITS>& p)
+{
+    if constexpr (BITS == 4) {
+        __builtin_nontemporal_store(u32x2{p.w[0], p.w[1]}, reinterpret_cast<u32x2*>(dst));
+    } else if constexpr (BITS == 6) {
+        uint32_t* d = reinterpret_cast<uint32_t*>(dst);
+        __builtin_nontemporal_store(p.w[0], d);
+        __builtin_nontemporal_store(p.w[1], d + 1);
+        __builtin_nontemporal_store(p.w[2], d + 2);
+    } else {
+        uint16_t* d = reinterpret_cast<uint16_t*>(dst);
+        __builtin_nontemporal_store((uint16_t)p.w[0], d);
+        __builtin_nontemporal_store((uint16_t)(p.w[0] >> 16), d + 1);
+        __builtin_nontemporal_store((uint16_t)p.w[1], d + 2);
+    }
+}
+
 // Quantize one (transformed) group and store its codes and scale byte.
-template <int FMT, bool SR>
+template <int FMT, bool SR, bool NTS = false>
 __device__ __forceinline__ void quantize_store(const float (&v)[kGroup], float alpha, float denom,
                                                uint64_t seed, int64_t gi, uint8_t* __restrict__ codes,
                                                uint8_t* __restrict__ scales, int qflags)
@@ -73,12 +135,21 @@ __device__ __forceinline__ void quantize_store(const float (&v)[kGroup], float a
     constexpr int BITS = Fmt<FMT>::BITS;
     Packed<BITS> p;
     const uint32_t sb = quantize_any<FMT, SR>(v, alpha, denom, qflags, seed, gi, p);
-    store_packed<BITS>(codes + gi * (2 * BITS), p);
-    if constexpr (Fmt<FMT>::G == 8) {
-        scales[2 * gi] = (uint8_t)sb;
-        scales[2 * gi + 1] = (uint8_t)(sb >> 8);
+    if constexpr (NTS) {
+        store_packed_nt<BITS>(codes + gi * (2 * BITS), p);
+        if constexpr (Fmt<FMT>::G == 8) {
+            __builtin_nontemporal_store((uint16_t)sb, reinterpret_cast<uint16_t*>(scales + 2 * gi));
+        } else {
+            __builtin_nontemporal_store((uint8_t)sb, scales + gi);
+        }
     } else {
-        scales[gi] = (uint8_t)sb;
+        store_packed<BITS>(codes + gi * (2 * BITS), p);
+        if constexpr (Fmt<FMT>::G == 8) {
+            scales[2 * gi] = (uint8_t)sb;
+            scales[2 * gi + 1] = (uint8_t)(sb >> 8);
+        } else {
+            scales[gi] = (uint8_t)sb;
+        }
     }
 }
 
@@ -95,17 +166,25 @@ __global__ __launch_bounds__(kThreads) void tensor_max_rows(const uint16_t* __re
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     for (int64_t r = blockIdx.y; r < nrows; r += gridDim.y) {
         int64_t gc = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-        // four groups' loads in flight per lane: the grid is small (at most
-        // kMaxPartials blocks), so bytes in flight come from unrolling
-        for (; gc + 3 * stride < gpr; gc += 4 * stride) {
-            float v[4][kGroup];
+        const int64_t gc0 = gc - (threadIdx.x & 63);  // the wavefront's first group
+        // four chunks of 64 groups in flight per wavefront: the grid is small
+        // (at most kMaxPartials blocks), so bytes in flight come from unrolling.
+        // The condition is the same in every lane of a wavefront.
+        for (int64_t w0 = gc0; w0 + 3 * stride + 64 <= gpr; w0 += 4 * stride, gc += 4 * stride) {
+            u32x4 a[4], b[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) load_group_rowwise(x + r * ld + (gc + u * stride) * kGroup, v[u]);
+            for (int u = 0; u < 4; ++u) load_wave_raw(x + r * ld + (w0 + u * stride) * kGroup, a[u], b[u]);
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                if constexpr (RHT) rht16(v[u], signs);
+                float v[kGroup];
+                if constexpr (RHT) {
+                    wave_groups(a[u], b[u], v);
+                    rht16(v, signs);
+                } else {
+                    unpack_group(a[u], b[u], v);  // which group a value is in does not matter
+                }
 #pragma unroll
-                for (int j = 0; j < kGroup; ++j) m = fmaxf(m, fabsf(v[u][j]));
+                for (int j = 0; j < kGroup; ++j) m = fmaxf(m, fabsf(v[j]));
             }
         }
         for (; gc < gpr; gc += stride) {
@@ -135,10 +214,14 @@ __global__ __launch_bounds__(kThreads) void quantize_rows(
     for (int64_t r = blockIdx.y; r < nrows; r += gridDim.y) {
         for (int64_t gc = (int64_t)blockIdx.x * kThreads + threadIdx.x; gc < gpr; gc += stride) {
             float v[kGroup];
-            load_group_rowwise(x + r * ld + gc * kGroup, v);
+            const int64_t gc0 = gc - (threadIdx.x & 63);  // the wavefront's first group
+            if (gc0 + 64 <= gpr)  // the whole wavefront is in this row
+                load_wave_group(x + r * ld + gc0 * kGroup, v);
+            else
+                load_group_rowwise(x + r * ld + gc * kGroup, v);
             if constexpr (RHT) rht16(v, signs);
             const int64_t gi = r * gpr + gc;
-            quantize_store<FMT, SR>(v, alpha, denom, seed, gi, codes, scales, qflags);
+            quantize_store<FMT, SR, true>(v, alpha, denom, seed, gi, codes, scales, qflags);
         }
     }
 }

@@ -109,6 +109,45 @@ def test_ties_and_signed_zero():
         assert_quant_equal(fmt, x, 0, tag=f"ties auto fmt {fmt}")
 
 
+def _bf16_neighbours(v):
+    """The bf16 values one step below and above each positive bf16 value v."""
+    b = O.bf16_bits(np.asarray(v, dtype=np.float32)).astype(np.int64)
+    return (O.bf16_to_f32((b - 1).astype(np.uint16)).astype(np.float64),
+            O.bf16_to_f32((b + 1).astype(np.uint16)).astype(np.float64))
+
+
+def test_every_scale_code_and_tie():
+    """With alpha supplied as fp32(1/M), fp32(alpha * M) is exactly 1, so the
+    scale quotient of Eq. 2 equals the group maximum.  Group maxima at every
+    E4M3 value, at every midpoint between neighbouring codes (a tie, which
+    goes to the even code), one bf16 step either side of each midpoint, at
+    2^-10 (rounds to the zero scale) and above 448 (saturates) exercise every
+    scale code and every rounding boundary between codes."""
+    vals = np.array([O.e4m3_value(c) for c in range(127)], dtype=np.float64)
+    mids = (vals[:-1] + vals[1:]) / 2
+    lo, hi = _bf16_neighbours(mids)
+    maxima = np.concatenate([vals[1:], mids, lo, hi, [2.0 ** -10, 448.0, 460.0, 464.0, 500.0, 3.0e4]])
+    ng = 16 * int(np.ceil(len(maxima) / 16))
+    maxima = np.concatenate([maxima, np.full(ng - len(maxima), 1.0)])
+    rng = np.random.default_rng(77)
+    g = maxima[:, None] * rng.uniform(-1, 1, (ng, 16))
+    g[:, 0] = maxima
+    g = g[rng.permutation(ng)]
+    for j in range(ng):  # the maximum in a different place in every group
+        g[j] = np.roll(g[j], j % 16)
+    x = workloads.to_bf16(g.reshape(ng // 16, 256))
+    assert np.all(np.abs(bits(x).view(np.uint16) & 0x7FFF) <= 0x7F80)
+    targets = {ops.IF3: 4.0, ops.IF6_E2M3: 7.5, ops.IF6_E3M2: 28.0, ops.NVINT4: 7.0, ops.IF3_BS8: 4.0}
+    for fmt in FORMATS:
+        m = targets.get(fmt, 6.0)
+        alpha = float(np.float32(1.0) / np.float32(m))
+        assert np.float32(alpha) * np.float32(m) == np.float32(1.0)
+        _, (_, osc, _) = assert_quant_equal(fmt, x, ops.SCALE_IN, alpha=alpha, tag=f"scale codes fmt {fmt}")
+        if fmt in (ops.IF4, ops.NVFP4):
+            assert len(np.unique(osc & 0x7F)) == 127  # every code, 0 included
+        assert_quant_equal(fmt, x, ops.SCALE_IN | ops.SR, alpha=alpha, seed=3, tag=f"scale codes sr fmt {fmt}")
+
+
 def test_nvint4_and_four_six_boundaries():
     """NVINT4 with alpha = 1 and group maximum 7 (Delta = 1): half-integers
     are exact rounding ties.  4/6: a group exact only when scaled to 4, a
