@@ -85,11 +85,21 @@ __device__ __forceinline__ void wave_groups(u32x4 a, u32x4 b, float (&v)[kGroup]
     unpack_group(lo, hi, v);
 }
 
-__device__ __forceinline__ void load_wave_group(const uint16_t* p, float (&v)[kGroup])
+// Raw bytes of group gc of row r: whole-wavefront loads when the wavefront's
+// 64 groups lie in the row (returns true; wave_groups then assembles lane
+// l's group), else the group's own two 16-byte pieces (returns false).
+__device__ __forceinline__ bool load_row_group(const uint16_t* x, int64_t r, int64_t ld, int64_t gc,
+                                               int64_t gpr, u32x4& a, u32x4& b)
 {
-    u32x4 a, b;
-    load_wave_raw(p, a, b);
-    wave_groups(a, b, v);
+    const int64_t gc0 = gc - (threadIdx.x & 63);  // the wavefront's first group
+    if (gc0 + 64 <= gpr) {
+        load_wave_raw(x + r * ld + gc0 * kGroup, a, b);
+        return true;
+    }
+    const u32x4* q = reinterpret_cast<const u32x4*>(x + r * ld + gc * kGroup);
+    a = __builtin_nontemporal_load(q);
+    b = __builtin_nontemporal_load(q + 1);
+    return false;
 }
 
 // alpha for this launch: the caller's, or Eq. 1 from the pass-1 partials.
@@ -208,17 +218,49 @@ __global__ __launch_bounds__(kThreads) void quantize_rows(
 {
     constexpr int BITS = Fmt<FMT>::BITS;
     __shared__ float red[kThreads / 64];
-    const float alpha = resolve_alpha(scale_in, tensor_scale, partials, npartials, denom_alpha, red);
-    const float denom = alpha * scale_max;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
+    const int64_t gc_first = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    // One value per thread -- its pass-1 partial maximum, or alpha itself when
+    // it is supplied -- then the block's first group are loaded before alpha
+    // is reduced: loads complete in order, so the reduction waits only for
+    // the first and the group's HBM latency overlaps it.  Both loads are
+    // unconditional (a lane without a group reads group 0 and drops it), so
+    // the wait for the first one stays partial.
+    static_assert(kMaxPartials <= kThreads, "one partial per thread");
+    const float* one = scale_in ? tensor_scale : partials + min((int)threadIdx.x, npartials - 1);
+    const float first = *one;
+    u32x4 pa, pb;
+    bool pwave;
+    {
+        const int64_t w0 = gc_first - (threadIdx.x & 63);  // the wavefront's first group
+        const bool row_ok = blockIdx.y < nrows;
+        pwave = row_ok && w0 + 64 <= gpr;                  // the same in every lane
+        if (pwave) {
+            load_wave_raw(x + (int64_t)blockIdx.y * ld + w0 * kGroup, pa, pb);
+        } else {
+            const bool mine = row_ok && gc_first < gpr;
+            const u32x4* q = reinterpret_cast<const u32x4*>(
+                x + (mine ? (int64_t)blockIdx.y * ld + gc_first * kGroup : 0));
+            pa = __builtin_nontemporal_load(q);
+            pb = __builtin_nontemporal_load(q + 1);
+        }
+    }
+    float alpha = first;
+    if (!scale_in) {
+        alpha = block_max((int)threadIdx.x < npartials ? first : 0.0f, red) / denom_alpha;
+        if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *tensor_scale = alpha;
+    }
+    const float denom = alpha * scale_max;
     for (int64_t r = blockIdx.y; r < nrows; r += gridDim.y) {
-        for (int64_t gc = (int64_t)blockIdx.x * kThreads + threadIdx.x; gc < gpr; gc += stride) {
+        for (int64_t gc = gc_first; gc < gpr; gc += stride) {
+            u32x4 a = pa, b = pb;
+            bool wave = pwave;
+            if (r != blockIdx.y || gc != gc_first) wave = load_row_group(x, r, ld, gc, gpr, a, b);
             float v[kGroup];
-            const int64_t gc0 = gc - (threadIdx.x & 63);  // the wavefront's first group
-            if (gc0 + 64 <= gpr)  // the whole wavefront is in this row
-                load_wave_group(x + r * ld + gc0 * kGroup, v);
+            if (wave)
+                wave_groups(a, b, v);
             else
-                load_group_rowwise(x + r * ld + gc * kGroup, v);
+                unpack_group(a, b, v);
             if constexpr (RHT) rht16(v, signs);
             const int64_t gi = r * gpr + gc;
             quantize_store<FMT, SR, true>(v, alpha, denom, seed, gi, codes, scales, qflags);
