@@ -91,15 +91,64 @@ __global__ __launch_bounds__(kDqThreads) void dequantize_groups(const uint8_t* _
 #pragma unroll
             for (int i = 0; i < 8; ++i)
                 p[i] = (uint32_t)f32_to_bf16_rne(o[2 * i]) | ((uint32_t)f32_to_bf16_rne(o[2 * i + 1]) << 16);
-            // ordinary stores: non-temporal ones were faster only for the
-            // decode-heavy formats and up to 30 % slower for NVFP4 and NVINT4
-            dq_u32x4* dst = reinterpret_cast<dq_u32x4*>(static_cast<uint16_t*>(out) + g * kGroup);
-            dst[0] = dq_u32x4{p[0], p[1], p[2], p[3]};
-            dst[1] = dq_u32x4{p[4], p[5], p[6], p[7]};
-        } else {
-            float4* dst = reinterpret_cast<float4*>(static_cast<float*>(out) + g * kGroup);
+            dq_u32x4 lo{p[0], p[1], p[2], p[3]}, hi{p[4], p[5], p[6], p[7]};
+            const int64_t g0 = g - (threadIdx.x & 63);  // the wavefront's first group
+            if (g0 + 64 <= ngroups) {
+                // The wavefront's 64 groups are 2 KiB of output: swap halves
+                // across the wavefront so that each store covers 1 KiB
+                // contiguously (lane l writes pieces 2(l mod 32) + l/32 and
+                // 64 + 2(l mod 32) + l/32), the inverse of the quantizer's
+                // load.
 #pragma unroll
-            for (int i = 0; i < 4; ++i) dst[i] = make_float4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
+                for (int d = 0; d < 4; ++d) {
+                    const auto r = __builtin_amdgcn_permlane32_swap(lo[d], hi[d], false, false);
+                    lo[d] = r[0];
+                    hi[d] = r[1];
+                }
+                const int lane = threadIdx.x & 63;
+                const int piece = 2 * (lane & 31) + (lane >> 5);
+                dq_u32x4* dst = reinterpret_cast<dq_u32x4*>(static_cast<uint16_t*>(out) + g0 * kGroup);
+                dst[piece] = lo;
+                dst[64 + piece] = hi;
+            } else {
+                dq_u32x4* dst = reinterpret_cast<dq_u32x4*>(static_cast<uint16_t*>(out) + g * kGroup);
+                dst[0] = lo;
+                dst[1] = hi;
+            }
+        } else {
+            dq_u32x4 P[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                P[i] = dq_u32x4{__float_as_uint(o[4 * i]), __float_as_uint(o[4 * i + 1]),
+                                __float_as_uint(o[4 * i + 2]), __float_as_uint(o[4 * i + 3])};
+            const int64_t g0 = g - (threadIdx.x & 63);  // the wavefront's first group
+            if (g0 + 64 <= ngroups) {
+                // 4 KiB of output per wavefront: a 4 x 4 transpose of the
+                // 16-byte pieces across the wavefront's four 16-lane rows
+                // (swap 2 x 2 blocks across the halves, then rows within
+                // each half) leaves in lane (row r, column c) piece r of the
+                // group of lane (k, c) in P[k], so store k covers 1 KiB
+                // contiguously: groups 16k .. 16k + 15.
+#pragma unroll
+                for (int d = 0; d < 4; ++d) {
+                    auto a = __builtin_amdgcn_permlane32_swap(P[0][d], P[2][d], false, false);
+                    auto b = __builtin_amdgcn_permlane32_swap(P[1][d], P[3][d], false, false);
+                    auto c0 = __builtin_amdgcn_permlane16_swap(a[0], b[0], false, false);
+                    auto c1 = __builtin_amdgcn_permlane16_swap(a[1], b[1], false, false);
+                    P[0][d] = c0[0];
+                    P[1][d] = c0[1];
+                    P[2][d] = c1[0];
+                    P[3][d] = c1[1];
+                }
+                const int lane = threadIdx.x & 63;
+                dq_u32x4* dst = reinterpret_cast<dq_u32x4*>(static_cast<float*>(out) + g0 * kGroup);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) dst[64 * k + 4 * (lane & 15) + (lane >> 4)] = P[k];
+            } else {
+                dq_u32x4* dst = reinterpret_cast<dq_u32x4*>(static_cast<float*>(out) + g * kGroup);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) dst[i] = P[i];
+            }
         }
     }
 }
