@@ -108,8 +108,9 @@ __global__ __launch_bounds__(kDqThreads) void dequantize_groups(const uint8_t* _
                 const int lane = threadIdx.x & 63;
                 const int piece = 2 * (lane & 31) + (lane >> 5);
                 dq_u32x4* dst = reinterpret_cast<dq_u32x4*>(static_cast<uint16_t*>(out) + g0 * kGroup);
-                dst[piece] = lo;
-                dst[64 + piece] = hi;
+                // non-temporal: 1-2 us faster here (no gain for fp32 output)
+                __builtin_nontemporal_store(lo, dst + piece);
+                __builtin_nontemporal_store(hi, dst + 64 + piece);
             } else {
                 dq_u32x4* dst = reinterpret_cast<dq_u32x4*>(static_cast<uint16_t*>(out) + g * kGroup);
                 dst[0] = lo;
