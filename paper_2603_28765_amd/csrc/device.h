@@ -658,6 +658,93 @@ template <int BITS> __device__ __forceinline__ void load_unpack16(const uint8_t*
     }
 }
 
+// IF4 / NVFP4 with stochastic rounding: the arithmetic of quantize_group
+// with SR (FP: grid neighbours lo <= m < lo + q of the clamped magnitude m,
+// up iff u q < m - lo; INT: y = x c_up, up iff u < |y| - floor|y|, clamped to
+// 7), with fewer steps: the grid step q of m's binade (0.5 below 2, 1 below
+// 4, 2 above) comes from m's exponent bits, the candidate is the chosen grid
+// value itself (lo or lo + q, exact) with x's sign instead of a rebuild from
+// its code, and the codes come from the converters -- the E2M1 code of an
+// exact grid value (round to nearest even leaves it in place, the sign and a
+// signed zero kept) and, for INT, the low nibble of r + 1.5 * 2^23.  RTN_TYPE
+// decides the type on the round-to-nearest candidates' errors (App. B).
+template <bool ADAPTIVE, bool RTN_TYPE>
+__device__ __forceinline__ uint32_t quantize_group_e2m1_sr(const float (&v)[kGroup], float alpha, float denom,
+                                                           const uint32_t (&w)[8], uint2& packed)
+{
+    constexpr float C_UP = 7.0f / 6.0f, K_DN = 6.0f / 7.0f;
+    const float amax = group_amax(v);
+    const uint32_t dcode = e4m3_encode(amax / denom);
+    const float s = alpha * e4m3_value(dcode);
+    if (!(s >= 1.17549435e-38f)) {
+        packed = make_uint2(0, 0);
+        return 0;
+    }
+    const float inv = 1.0f / s;
+    float xb[kGroup], qf[kGroup];
+    uint32_t tb[kGroup];
+    float ef = 0.0f, ei = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+        xb[j] = v[j] * inv;
+        const float u = sr_uniform(w, j);
+        const float m = fminf(fabsf(xb[j]), 6.0f);
+        // 2^floor(log2 m) (0 for m below 2^-126), the step q and 1/q (powers of two)
+        const float p2 = __uint_as_float(__float_as_uint(m) & 0x7F800000u);
+        const float q = fmaxf(p2 * 0.5f, 0.5f);
+        const float inv_q = __uint_as_float((254u << 23) - __float_as_uint(q));
+        const float lo = __builtin_floorf(m * inv_q) * q;
+        const float mag = (u * q < m - lo) ? lo + q : lo;
+        qf[j] = __uint_as_float(__float_as_uint(mag) | (__float_as_uint(xb[j]) & 0x80000000u));
+        const float d = qf[j] - xb[j];
+        ef = __builtin_fmaf(d, d, ef);
+        if constexpr (ADAPTIVE) {
+            const float y = xb[j] * C_UP;
+            const float a = fabsf(y);
+            const float il = __builtin_floorf(a);
+            const float rr = fminf((u < a - il) ? il + 1.0f : il, 7.0f);
+            const float r = (y < 0.0f) ? -rr : rr;
+            tb[j] = __float_as_uint(r + 12582912.0f);
+            const float di = __builtin_fmaf(r, K_DN, -xb[j]);
+            ei = __builtin_fmaf(di, di, ei);
+        }
+    }
+    uint32_t f0 = 0, f1 = 0;
+    f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, qf[0], qf[1], 1.0f, 0);
+    f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, qf[2], qf[3], 1.0f, 1);
+    f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, qf[4], qf[5], 1.0f, 2);
+    f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, qf[6], qf[7], 1.0f, 3);
+    f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, qf[8], qf[9], 1.0f, 0);
+    f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, qf[10], qf[11], 1.0f, 1);
+    f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, qf[12], qf[13], 1.0f, 2);
+    f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, qf[14], qf[15], 1.0f, 3);
+    if constexpr (!ADAPTIVE) {
+        packed = make_uint2(f0, f1);
+        return dcode;
+    }
+    bool use_int;
+    if constexpr (RTN_TYPE) {
+        // the round-to-nearest candidates' errors decide the type
+        uint32_t g0, g1;
+        const float rf = e2m1_candidate(xb, g0, g1);
+        float ri = 0.0f;
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) {
+            const float xc = __builtin_amdgcn_fmed3f(xb[j], -6.0f, 6.0f);
+            const float r0 = __builtin_fmaf(xc, C_UP, 12582912.0f) - 12582912.0f;
+            const float e0 = __builtin_fmaf(r0, K_DN, -xb[j]);
+            ri = __builtin_fmaf(e0, e0, ri);
+        }
+        use_int = ri < rf;
+    } else {
+        use_int = ei < ef;
+    }
+    uint32_t i0, i1;
+    pack_int4_biased(tb, i0, i1);
+    packed = use_int ? make_uint2(i0, i1) : make_uint2(f0, f1);
+    return dcode | (use_int ? 0x80u : 0u);
+}
+
 // ------------------------------------------------------ group dispatcher
 // Quantize one (already transformed) block of 16 values of any format:
 // returns its scale byte (two, low byte first, for block size 8) and the
@@ -721,6 +808,13 @@ __device__ __forceinline__ uint32_t quantize_any(const float (&v)[kGroup], float
     } else if constexpr (BITS == 4 && !SR) {
         uint2 pk;
         const uint32_t sb = quantize_group_e2m1<F::ADAPTIVE>(v, alpha, denom, pk);
+        out.w[0] = pk.x;
+        out.w[1] = pk.y;
+        return sb;
+    } else if constexpr (BITS == 4) {
+        uint2 pk;
+        const uint32_t sb = rtn_type ? quantize_group_e2m1_sr<F::ADAPTIVE, true>(v, alpha, denom, w, pk)
+                                     : quantize_group_e2m1_sr<F::ADAPTIVE, false>(v, alpha, denom, w, pk);
         out.w[0] = pk.x;
         out.w[1] = pk.y;
         return sb;

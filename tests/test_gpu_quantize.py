@@ -78,6 +78,14 @@ def test_non_contiguous_rows():
     for fmt in (ops.IF4, ops.IF3, ops.IF6_E2M3):
         assert_quant_equal(fmt, x, 0, ld_pad=24, tag="ld padded")
         assert_quant_equal(fmt, x, ops.RHT | ops.SR, signs=0x1234, seed=5, ld_pad=8, tag="ld padded rht sr")
+    # rows of 65 groups with padding: the first 64 groups of a row are read by
+    # whole-wavefront loads, the 65th per lane
+    xw = rand_bf16((33, 1040), 13, "outliers")
+    for fmt in (ops.IF4, ops.NVFP4, ops.IF3, ops.IF6_E3M2, ops.IF4_BS8):
+        assert_quant_equal(fmt, xw, 0, ld_pad=8, tag=f"ld padded 65 groups fmt {fmt}")
+        assert_quant_equal(fmt, xw, ops.RHT | ops.SR, signs=0x1234, seed=5, ld_pad=56,
+                           tag=f"ld padded 65 groups rht sr fmt {fmt}")
+        assert_quant_equal(fmt, xw, ops.RHT, signs=0x0FF0, tag=f"ld contiguous 65 groups rht fmt {fmt}")
     # strided axis: ld % 8 == 0 keeps the register path, ld % 8 != 0 the LDS path
     xs = rand_bf16((256, 328), 12, "outliers")
     for fmt in (ops.IF4, ops.NVFP4, ops.IF3):
