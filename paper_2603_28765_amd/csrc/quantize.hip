@@ -420,8 +420,9 @@ __global__ __launch_bounds__(kThreads) void tensor_max_cols(const uint16_t* __re
 // Pass 2 of the register path.  A block owns a tile of 64 columns x 1024
 // rows (64 groups per output row) and stages its output in LDS (36 KiB) so
 // that every output row segment -- 512 bytes of codes, 64 of scales -- is
-// written as whole cache lines (measured against 2048-row tiles: more
-// workgroups in flight, 20 % faster with round to nearest).  Lane l of wavefront w handles column chunk
+// written as whole cache lines, with non-temporal stores (measured against
+// 2048-row tiles: more workgroups in flight, 20 % faster with round to
+// nearest).  Lane l of wavefront w handles column chunk
 // l / 8 (8 columns) and group l % 8 of the wavefront's 8 groups per round;
 // one load instruction reads 16 B from each of 8 rows' 128-byte column
 // segments.  LDS rows are XOR-swizzled by 8 (col / 8) slots, which keeps the
@@ -477,7 +478,8 @@ __global__ __launch_bounds__(kThreads) void quantize_cols(
         const int row = idx / ppr, pc = idx % ppr;
         const int s = 8 * (row >> 3);
         const uint4 v = *reinterpret_cast<const uint4*>(lcodes + row * kCodeRowBytes + ((2 * pc) ^ s) * 8);
-        *reinterpret_cast<uint4*>(codes + ((c0 + row) * ngroups + g0 + 2 * pc) * 8) = v;
+        __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w},
+                                    reinterpret_cast<u32x4*>(codes + ((c0 + row) * ngroups + g0 + 2 * pc) * 8));
     }
     // scales: ncol rows x ntg bytes, 16-byte pieces (bytes keep the swizzle of 8-slot blocks)
     const int spr = ntg / 16;
@@ -493,7 +495,8 @@ __global__ __launch_bounds__(kThreads) void quantize_cols(
                 wv |= (uint32_t)lscales[row * kGrpTile + ((16 * pc + 4 * k + b) ^ s)] << (8 * b);
             w4[k] = wv;
         }
-        *reinterpret_cast<uint4*>(scales + (c0 + row) * ngroups + g0 + 16 * pc) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+        __builtin_nontemporal_store(u32x4{w4[0], w4[1], w4[2], w4[3]},
+                                    reinterpret_cast<u32x4*>(scales + (c0 + row) * ngroups + g0 + 16 * pc));
     }
 }
 
@@ -913,7 +916,8 @@ __global__ __launch_bounds__(kThreads) void quantize_cols_dual(DualK a)
         const int row = idx / ppr, pc = idx % ppr;
         const int s = 8 * (row >> 3);
         const uint4 v = *reinterpret_cast<const uint4*>(lcodes + row * kCodeRowBytes + ((2 * pc) ^ s) * 8);
-        *reinterpret_cast<uint4*>(codes + ((c0 + row) * ngroups + g0 + 2 * pc) * 8) = v;
+        __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w},
+                                    reinterpret_cast<u32x4*>(codes + ((c0 + row) * ngroups + g0 + 2 * pc) * 8));
     }
     const int spr = ntg / 16;
     for (int idx = t; idx < ncol * spr; idx += kThreads) {
@@ -928,7 +932,8 @@ __global__ __launch_bounds__(kThreads) void quantize_cols_dual(DualK a)
                 wv |= (uint32_t)lscales[row * kGrpTile + ((16 * pc + 4 * k + b) ^ s)] << (8 * b);
             w4[k] = wv;
         }
-        *reinterpret_cast<uint4*>(scales + (c0 + row) * ngroups + g0 + 16 * pc) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+        __builtin_nontemporal_store(u32x4{w4[0], w4[1], w4[2], w4[3]},
+                                    reinterpret_cast<u32x4*>(scales + (c0 + row) * ngroups + g0 + 16 * pc));
     }
 }
 
