@@ -253,6 +253,22 @@ def _event_time(torch, fn, steps, warmup, flush=None):
     return float(sum(times) / len(times))
 
 
+def _steady_time(torch, fn, steps=10, warmup=20):
+    """Mean time of fn() in seconds under sustained load, as in the timed
+    step: `warmup` launches back to back (the GEMM's power-management
+    transient settles within them), then `steps` launches back to back, each
+    between two HIP events, with one synchronisation at the end."""
+    for _ in range(warmup):
+        fn()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for e0, e1 in evs:
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    return float(sum(e0.elapsed_time(e1) for e0, e1 in evs) / steps * 1e-3)
+
+
 def wgrad_times(ops, workloads, torch):
     """Weight gradient dW = dY^T X (dY 8192 x 14336, X 8192 x 4096, both
     quantized along the token axis with RHT, SR and the 16/17 margin; fp32
@@ -274,7 +290,7 @@ def wgrad_times(ops, workloads, torch):
     del flush
     M, N, K = w.info["M"], w.info["N"], w.info["K"]
     out = torch.empty((M, N), dtype=torch.float32, device="cuda")
-    t_g = _event_time(torch, lambda: ops.if4_gemm(pdy, px, ops.F32, out), 20, 5)
+    t_g = _steady_time(torch, lambda: ops.if4_gemm(pdy, px, ops.F32, out), 20)
     n_dy = dy.numel()
     return {"workload": f"wgrad_{M}x{N}x{K}", "quant_dY_us": round(t_dy * 1e6, 1),
             "quant_dY_1pass_us": round(t_dy1 * 1e6, 1),
@@ -285,17 +301,19 @@ def wgrad_times(ops, workloads, torch):
 
 def bitwidth_times(ops, workloads, torch):
     """Bit-width study: A, B 8192 x 8192 (N(0,1), 0.05 % of elements x100)
-    quantized along K in every format, then the 8192^3 GEMM with bf16 out."""
+    quantized along K in every format (both passes, cache flushed), then the
+    8192^3 GEMM with bf16 out under sustained load."""
     w = workloads.bitwidth()
     a, b = w.tensors["A"].cuda(), w.tensors["B"].cuda()
     n = a.shape[0]
     ws = torch.empty(4096, dtype=torch.uint8, device="cuda")
     out = torch.empty((n, n), dtype=torch.bfloat16, device="cuda")
     res = {"workload": f"bitwidth_{n}^3"}
+    flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device="cuda")
     for fmt, name in ops.FORMAT_NAMES.items():
         pa, pb = ops.ifx_quantize(fmt, a, workspace=ws), ops.ifx_quantize(fmt, b, workspace=ws)
-        t_q = _event_time(torch, lambda: ops.ifx_quantize(fmt, a, out=pa, workspace=ws), 5, 2)
-        t_g = _event_time(torch, lambda: ops.ifx_gemm(pa, pb, ops.BF16, out), 5, 2)
+        t_q = _event_time(torch, lambda: ops.ifx_quantize(fmt, a, out=pa, workspace=ws), 5, 2, flush)
+        t_g = _steady_time(torch, lambda: ops.ifx_gemm(pa, pb, ops.BF16, out), 10)
         res[name] = {"quant_us": round(t_q * 1e6, 1), "gemm_us": round(t_g * 1e6, 1),
                      "gemm_TFLOPs": round(2.0 * n ** 3 / t_g / 1e12, 1)}
         del pa, pb
@@ -330,7 +348,7 @@ def dual_times(ops, workloads, torch):
     _, pw = ops.ifx_quantize_dual(ops.IF4, W)
     M, N, K = dy.shape[0], W.shape[1], dy.shape[1]
     out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-    t_g = _event_time(torch, lambda: ops.if4_gemm(pdy, pw, ops.BF16, out), 20, 5)
+    t_g = _steady_time(torch, lambda: ops.if4_gemm(pdy, pw, ops.BF16, out), 20)
     res["dgrad"] = {"workload": f"dgrad_{M}x{N}x{K}", "gemm_us": round(t_g * 1e6, 1),
                     "gemm_TFLOPs": round(2.0 * M * N * K / t_g / 1e12, 1)}
     return res
