@@ -745,6 +745,76 @@ __device__ __forceinline__ uint32_t quantize_group_e2m1_sr(const float (&v)[kGro
     return dcode | (use_int ? 0x80u : 0u);
 }
 
+// IF6 (E2M3 / E3M2) with round-to-nearest: the arithmetic of quantize_group
+// with the FP candidate from gfx950's 32-value FP6 converters: fp32 -> FP6
+// rounds to nearest even and saturates, keeping the sign (signed zero
+// included), and writes 32 codes at bits 6j .. 6j + 5, code 2i from element
+// i of its first source and 2i + 1 from element i of its second.  With the
+// group's even elements in the first source and its odd ones in the second
+// (zeros after them), the first three dwords are the group's FP codes in the
+// packed layout of the format; FP6 -> fp32 reads them back in code order.
+// An exhaustive comparison over every finite fp32 of both signs found the
+// conversion equal to the nearest-even encoder of quantize_group, and the
+// decode exact for all 64 codes of either format.
+template <int FMT>
+__device__ __forceinline__ uint32_t quantize_group_fp6(const float (&v)[kGroup], float alpha, float denom,
+                                                       Packed<6>& out)
+{
+    using F = Fmt<FMT>;
+    using D = FmtDerived<FMT>;
+    typedef float f16v __attribute__((ext_vector_type(16)));
+    typedef float f32v __attribute__((ext_vector_type(32)));
+    typedef uint32_t u6v __attribute__((ext_vector_type(6)));
+    const float amax = group_amax(v);
+    const uint32_t dcode = e4m3_encode(amax / denom);
+    const float s = alpha * e4m3_value(dcode);
+    if (!(s >= 1.17549435e-38f)) {
+        out.w[0] = out.w[1] = out.w[2] = 0;
+        return 0;
+    }
+    const float inv = 1.0f / s;
+    float xa[kGroup];
+    f16v ev, od;
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) xa[j] = v[j] * inv;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        ev[i] = xa[2 * i];
+        od[i] = xa[2 * i + 1];
+        ev[8 + i] = 0.0f;
+        od[8 + i] = 0.0f;
+    }
+    u6v fc;
+    f32v q;
+    if constexpr (F::EB == 2) {
+        fc = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(ev, od, 1.0f);
+        q = __builtin_amdgcn_cvt_scalef32_pk32_f32_fp6(fc, 1.0f);
+    } else {
+        fc = __builtin_amdgcn_cvt_scalef32_2xpk16_bf6_f32(ev, od, 1.0f);
+        q = __builtin_amdgcn_cvt_scalef32_pk32_f32_bf6(fc, 1.0f);
+    }
+    float ef = 0.0f, ei = 0.0f;
+    uint32_t ci[kGroup];
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+        const float d = q[j] - xa[j];
+        ef = __builtin_fmaf(d, d, ef);
+        const float xc = __builtin_amdgcn_fmed3f(xa[j], -F::FP_MAX, F::FP_MAX);
+        const float t = __builtin_fmaf(xc, D::C_UP, 12582912.0f);  // rint(xc*c_up) + 1.5*2^23
+        ci[j] = __float_as_uint(t) & D::CODE_MASK;                   // two's complement, 6 bits
+        const float di = __builtin_fmaf(t - 12582912.0f, D::K_DN, -xa[j]);
+        ei = __builtin_fmaf(di, di, ei);
+    }
+    if (ei < ef) {
+        out = pack16<6>(ci);
+        return dcode | 0x80u;
+    }
+    out.w[0] = fc[0];
+    out.w[1] = fc[1];
+    out.w[2] = fc[2];
+    return dcode;
+}
+
 // ------------------------------------------------------ group dispatcher
 // Quantize one (already transformed) block of 16 values of any format:
 // returns its scale byte (two, low byte first, for block size 8) and the
@@ -818,6 +888,8 @@ __device__ __forceinline__ uint32_t quantize_any(const float (&v)[kGroup], float
         out.w[0] = pk.x;
         out.w[1] = pk.y;
         return sb;
+    } else if constexpr (BITS == 6 && !SR) {
+        return quantize_group_fp6<FMT>(v, alpha, denom, out);
     } else {
         uint32_t c[kGroup];
         const uint32_t sb = (SR && rtn_type) ? quantize_group<FMT, SR, true>(v, alpha, denom, w, c)
