@@ -56,8 +56,8 @@ def main():
         record_traffic(args.traffic_from)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the multi-GPU layout "
-              "is described in DESIGN.md, not run.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the kernels run on one "
+              "GPU's share of the work; no path across several GPUs is built.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
