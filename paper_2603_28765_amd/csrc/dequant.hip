@@ -55,6 +55,19 @@ __global__ __launch_bounds__(kDqThreads) void dequantize_groups(const uint8_t* _
             fp4_pair<0>(t.y, qf, 8); fp4_pair<1>(t.y, qf, 10); fp4_pair<2>(t.y, qf, 12); fp4_pair<3>(t.y, qf, 14);
 #pragma unroll
             for (int j = 0; j < kGroup; ++j) c[j] = ((j < 8 ? t.x : t.y) >> (4 * (j & 7))) & 15u;
+        } else if constexpr (F::BITS == 6) {
+            // FP6 codes through the 32-value hardware decode (exact for every
+            // code; the stream's codes 0..15 are this group's, 16..31 zeros)
+            typedef uint32_t u6v __attribute__((ext_vector_type(6)));
+            typedef float f32v __attribute__((ext_vector_type(32)));
+            const uint32_t* src = reinterpret_cast<const uint32_t*>(codes + g * 12);
+            const u6v r = {src[0], src[1], src[2], 0u, 0u, 0u};
+            f32v q;
+            if constexpr (F::EB == 2) q = __builtin_amdgcn_cvt_scalef32_pk32_f32_fp6(r, 1.0f);
+            else q = __builtin_amdgcn_cvt_scalef32_pk32_f32_bf6(r, 1.0f);
+#pragma unroll
+            for (int j = 0; j < kGroup; ++j) qf[j] = q[j];
+            load_unpack16<6>(codes + g * 12, c);  // the INT codes
         } else {
             load_unpack16<F::BITS>(codes + g * (2 * F::BITS), c);
             if constexpr (F::KIND != kKindInt) {
