@@ -156,6 +156,28 @@ def test_every_scale_code_and_tie():
         assert_quant_equal(fmt, x, ops.SCALE_IN | ops.SR, alpha=alpha, seed=3, tag=f"scale codes sr fmt {fmt}")
 
 
+@pytest.mark.parametrize("fmt", [ops.IF6_E2M3, ops.IF6_E3M2, ops.IF4, ops.NVFP4, ops.IF3])
+def test_fp_grid_midpoints(fmt):
+    """alpha = 1 and a group maximum of M_FP make the scale 1, so x-bar is the
+    input itself: every midpoint between neighbouring FP grid values (a tie,
+    to the even code), one bf16 step either side of it, the grid values and
+    values beyond the maximum, in both signs, at every position of a group."""
+    grid = O.fp_grid(fmt).astype(np.float64)
+    fmax = float(grid.max())
+    mids = (grid[:-1] + grid[1:]) / 2
+    lo, hi = _bf16_neighbours(mids[mids > 0])
+    vals = np.concatenate([grid, mids, lo, hi, [fmax * 1.01, fmax * 1.5]])
+    vals = np.concatenate([vals, -vals])
+    n = 15 * int(np.ceil(len(vals) / 15))
+    vals = np.concatenate([vals, np.zeros(n - len(vals))])
+    rows = []
+    for k, chunk in enumerate(vals.reshape(-1, 15)):
+        g = np.insert(chunk, k % 16, fmax)   # the group maximum M_FP, anywhere in the group
+        rows.append(g)
+    x = workloads.to_bf16(np.array(rows))  # one group per row
+    assert_quant_equal(fmt, x, ops.SCALE_IN, alpha=1.0, tag=f"fp grid midpoints fmt {fmt}")
+
+
 def test_nvint4_and_four_six_boundaries():
     """NVINT4 with alpha = 1 and group maximum 7 (Delta = 1): half-integers
     are exact rounding ties.  4/6: a group exact only when scaled to 4, a
