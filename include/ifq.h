@@ -28,7 +28,7 @@
  *   NVINT4      4     --             --     INT4   7     (INT only, Sec. 2)
  *   NVFP4_46    4     E2M1           6      --     --    (FP only, 4/6, Sec. 3)
  *   IF4_BS8, IF3_BS8, NVFP4_BS8: IF4, IF3 and NVFP4 with one scale per 8
- *                values instead of 16 (Sec. 6, Table 6: 5.0, 4.0, 5.0 bits per
+ *                values instead of 16 (Sec. 5.1; Table 6 in App. D: 5.0, 4.0, 5.0 bits per
  *                parameter).  Scales are [R, K/8]; the two scale bytes of
  *                values 16i .. 16i+15 are adjacent, and their codes fill the
  *                same 2b bytes as one block-16 group.  SR draws of group g
@@ -43,7 +43,8 @@
  * data then decode exactly like NVFP4.
  *
  * Layouts (row-major, no padding):
- *   codes   uint8 [R, K * bits / 8]      scales  uint8 [R, K / 16]
+ *   codes   uint8 [R, K * bits / 8]      scales  uint8 [R, K / G]
+ * with G = 16 values per scale byte (8 for the *_BS8 formats)
  * where R is the number of logical rows and K (a multiple of 16) is the
  * grouped axis.
  *
@@ -70,7 +71,7 @@
 extern "C" {
 #endif
 
-#define IFQ_ABI_VERSION 1
+#define IFQ_ABI_VERSION 2
 
 typedef enum ifq_status {
     IFQ_OK = 0,
@@ -133,7 +134,7 @@ enum {
  *   rht_signs     16-bit sign mask (upper bits must be zero)
  *   seed          Philox key for IFQ_SR
  *   codes         (device) uint8 [R, K*bits/8], 16-byte aligned
- *   scales        (device) uint8 [R, K/16]
+ *   scales        (device) uint8 [R, K/G] (G = ifq_group_size(format))
  *                 Row-wise: R = rows, K = cols (cols % 16 == 0).
  *                 IFQ_AXIS_STRIDED: R = cols, K = rows (rows % 16 == 0): the
  *                 output is the packed form of X^T, K-major as the GEMM
@@ -256,8 +257,10 @@ int ifx_gemm(int format, const uint8_t* a_codes, const uint8_t* a_scales,
              int64_t ldc, int out_dtype, void* stream);
 
 /* ---------------------------------------------------------- host helpers */
-size_t ifq_codes_bytes(int format, int64_t rows, int64_t cols); /* rows * cols * bits / 8 */
-size_t ifq_scales_bytes(int64_t rows, int64_t cols);            /* rows * cols / 16 */
+/* Buffer sizes of a packed [rows, cols] tensor (cols = the grouped axis K);
+ * 0 for an unknown format or a negative size. */
+size_t ifq_codes_bytes(int format, int64_t rows, int64_t cols);  /* rows * cols * bits / 8 */
+size_t ifq_scales_bytes(int format, int64_t rows, int64_t cols); /* rows * (cols / group size) */
 int ifq_group_size(int format);  /* values per scale byte: 16, or 8 for the *_BS8 formats;
                                     0 for an unknown format */
 const char* ifq_status_string(int status);

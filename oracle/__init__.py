@@ -28,7 +28,7 @@ FORMATS = {"if4": FMT_IF4, "nvfp4": FMT_NVFP4, "if3": FMT_IF3,
            "nvfp4_bs8": FMT_NVFP4_BS8}
 BITS = {FMT_IF4: 4, FMT_NVFP4: 4, FMT_IF3: 3, FMT_IF6_E2M3: 6, FMT_IF6_E3M2: 6,
         FMT_NVINT4: 4, FMT_NVFP4_46: 4, FMT_IF4_BS8: 4, FMT_IF3_BS8: 3, FMT_NVFP4_BS8: 4}
-# values per group (one scale byte each): block size 8 for the *_BS8 formats (Sec. 6)
+# values per group (one scale byte each): block size 8 for the *_BS8 formats (Sec. 5.1, Table 6 in App. D)
 GSIZE = {f: (8 if f in (FMT_IF4_BS8, FMT_IF3_BS8, FMT_NVFP4_BS8) else 16) for f in BITS}
 
 RHT, SR, MARGIN, SCALE_IN, STRIDED, SR_RTN_TYPE = 1, 2, 4, 8, 16, 32

@@ -74,7 +74,7 @@ typedef struct {
     int bits;          /* bits per stored code */
     int ebits, mbits;  /* FP element: exponent and mantissa field widths */
     int kind;          /* KIND_* */
-    int gsize;         /* values per group (one scale each): 16, or 8 (Sec. 6) */
+    int gsize;         /* values per group (one scale each): 16, or 8 (Sec. 5.1) */
     int adaptive;      /* kind == KIND_ADAPTIVE */
     float m_scale;     /* M of Eq. 1-2: the element maximum a group is scaled to */
     float alpha_fp8;   /* the E4M3 factor of Eq. 1: 448, or 256 for 4/6 */
@@ -142,7 +142,7 @@ static void ensure_init(void)
     init_fmt(&g_fmt[FMT_IF6_E3M2], 6, 3, 2, KIND_ADAPTIVE);  /* E3M2 / INT6, Table 6 */
     init_fmt(&g_fmt[FMT_NVINT4], 4, 2, 1, KIND_INT);         /* INT4 only, Sec. 2 */
     init_fmt(&g_fmt[FMT_NVFP4_46], 4, 2, 1, KIND_FOUR_SIX);  /* E2M1, max 6 or 4, Sec. 3 */
-    /* block size 8: one scale per 8 values (Sec. 6, Table 6) */
+    /* block size 8: one scale per 8 values (Sec. 5.1; Table 6, App. D) */
     init_fmt(&g_fmt[FMT_IF4_BS8], 4, 2, 1, KIND_ADAPTIVE);
     init_fmt(&g_fmt[FMT_IF3_BS8], 3, 2, 0, KIND_ADAPTIVE);
     init_fmt(&g_fmt[FMT_NVFP4_BS8], 4, 2, 1, KIND_FP);

@@ -276,10 +276,11 @@ size_t ifq_codes_bytes(int format, int64_t rows, int64_t cols)
     return (size_t)(rows * cols * bits_of(format) / 8);
 }
 
-size_t ifq_scales_bytes(int64_t rows, int64_t cols)
+size_t ifq_scales_bytes(int format, int64_t rows, int64_t cols)
 {
-    if (rows < 0 || cols < 0) return 0;
-    return (size_t)(rows * (cols / 16));
+    const int g = ifq_group_size(format);
+    if (g == 0 || rows < 0 || cols < 0) return 0;
+    return (size_t)(rows * (cols / g));
 }
 
 const char* ifq_status_string(int status)

@@ -66,7 +66,7 @@ template <> struct Fmt<IFQ_FMT_NVFP4_46> {
     static constexpr float FP_MAX = 6.0f, M = 6.0f, A8 = 256.0f;
 };
 
-// Block size 8 (Sec. 6, Table 6): the same elements with one scale per 8
+// Block size 8 (Sec. 5.1; Table 6, App. D): the same elements with one scale per 8
 // values (G = 8).  A quantizer lane still owns 16 values -- two groups, two
 // adjacent scale bytes -- and the code bit stream of 16 values is unchanged.
 template <> struct Fmt<IFQ_FMT_IF4_BS8> : Fmt<IFQ_FMT_IF4> { static constexpr int G = 8; };

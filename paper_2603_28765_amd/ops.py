@@ -71,7 +71,7 @@ def lib() -> C.CDLL:
         L.ifq_quantize_workspace_bytes.restype = C.c_size_t
         L.ifq_codes_bytes.argtypes = [C.c_int, C.c_int64, C.c_int64]
         L.ifq_codes_bytes.restype = C.c_size_t
-        L.ifq_scales_bytes.argtypes = [C.c_int64, C.c_int64]
+        L.ifq_scales_bytes.argtypes = [C.c_int, C.c_int64, C.c_int64]
         L.ifq_scales_bytes.restype = C.c_size_t
         L.ifx_quantize_dual.argtypes = [C.c_int, C.c_void_p, C.c_int64, C.c_int64, C.c_int64,
                                          C.c_uint32, C.c_uint32, C.c_uint32, C.c_uint64, C.c_uint64,
@@ -104,6 +104,36 @@ def _require_gpu(*ts: torch.Tensor):
             raise ValueError("libifq operates on GPU tensors only")
 
 
+def _require_buffer(name: str, t: torch.Tensor, shape, dtype, device):
+    """The C ABI receives bare pointers, so every buffer's shape, dtype,
+    device and layout is checked here before a launch: a short or strided
+    buffer would otherwise be written past its end."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a tensor")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _require_packed(name: str, p: "Packed", device=None):
+    """A Packed operand must hold exactly the buffers its format and logical
+    shape [rows, cols] imply."""
+    if p.fmt not in BITS:
+        raise ValueError(f"{name}: unknown format {p.fmt}")
+    if p.cols % 16:
+        raise ValueError(f"{name}: K = {p.cols} is not a multiple of 16")
+    dev = p.codes.device if device is None else device
+    _require_gpu(p.codes)
+    _require_buffer(f"{name}.codes", p.codes, (p.rows, p.cols * BITS[p.fmt] // 8), torch.uint8, dev)
+    _require_buffer(f"{name}.scales", p.scales, (p.rows, p.cols // GSIZE[p.fmt]), torch.uint8, dev)
+    _require_buffer(f"{name}.tensor_scale", p.tensor_scale, (1,), torch.float32, dev)
+
+
 @dataclass
 class Packed:
     """A quantized tensor: codes [R, K*bits/8], scales [R, K/16] (uint8),
@@ -125,15 +155,23 @@ def _quantize(fn: str, fmt: int, x: torch.Tensor, flags: int = 0, rht_signs: int
     rows, cols = x.shape
     R, K = (cols, rows) if flags & AXIS_STRIDED else (rows, cols)
     dev = x.device
+    if fmt not in BITS:
+        raise ValueError(f"unknown format {fmt}")
     if out is None:
         codes = torch.empty((R, K * BITS[fmt] // 8), dtype=torch.uint8, device=dev)
         scales = torch.empty((R, K // GSIZE[fmt]), dtype=torch.uint8, device=dev)
         ts = torch.empty(1, dtype=torch.float32, device=dev) if tensor_scale is None else tensor_scale
         out = Packed(fmt, codes, scales, ts, R, K)
-    elif tensor_scale is not None:
-        out.tensor_scale = tensor_scale
+    else:
+        if (out.fmt, out.rows, out.cols) != (fmt, R, K):
+            raise ValueError(f"out describes format {out.fmt} [{out.rows}, {out.cols}], the call "
+                             f"writes format {fmt} [{R}, {K}]")
+        if tensor_scale is not None:
+            out.tensor_scale = tensor_scale
     if flags & SCALE_IN and tensor_scale is None:
         raise ValueError("SCALE_IN needs tensor_scale")
+    if K % 16 == 0:  # other shapes are rejected by the library itself
+        _require_packed("out", out, dev)
     L = lib()
     wsb = L.ifq_quantize_workspace_bytes(fmt, rows, cols, flags)
     if wsb and workspace is None:
@@ -181,6 +219,8 @@ def ifx_quantize_dual(fmt, x, row_flags=0, col_flags=0, rht_signs=0, row_seed=0,
         raise ValueError("x must be a 2-D bf16 GPU tensor with unit column stride")
     rows, cols = x.shape
     dev = x.device
+    if fmt not in BITS:
+        raise ValueError(f"unknown format {fmt}")
     if out_row is None:
         out_row = _packed_for(fmt, rows, cols, dev, row_tensor_scale)
     elif row_tensor_scale is not None:
@@ -189,6 +229,12 @@ def ifx_quantize_dual(fmt, x, row_flags=0, col_flags=0, rht_signs=0, row_seed=0,
         out_col = _packed_for(fmt, cols, rows, dev, col_tensor_scale)
     elif col_tensor_scale is not None:
         out_col.tensor_scale = col_tensor_scale
+    if (out_row.fmt, out_row.rows, out_row.cols) != (fmt, rows, cols) or \
+            (out_col.fmt, out_col.rows, out_col.cols) != (fmt, cols, rows):
+        raise ValueError("out_row / out_col do not describe this format and shape")
+    if rows % 16 == 0 and cols % 16 == 0:  # other shapes are rejected by the library itself
+        _require_packed("out_row", out_row, dev)
+        _require_packed("out_col", out_col, dev)
     L = lib()
     wsb = L.ifq_quantize_dual_workspace_bytes(fmt, rows, cols, row_flags, col_flags)
     if wsb and workspace is None:
@@ -203,11 +249,18 @@ def ifx_quantize_dual(fmt, x, row_flags=0, col_flags=0, rht_signs=0, row_seed=0,
     return out_row, out_col
 
 
-def _dequantize(fn: str, p: Packed, out_dtype: int = F32, out: torch.Tensor | None = None):
+def _dequantize(fn: str, p: Packed, out_dtype: int = F32, out: torch.Tensor | None = None,
+                fixed_fmt: int | None = None):
     _require_gpu(p.codes, p.scales, p.tensor_scale)
+    if fixed_fmt is not None and p.fmt != fixed_fmt:
+        raise ValueError(f"{fn} takes {FORMAT_NAMES[fixed_fmt]} data, got format {p.fmt}")
+    if out_dtype not in (F32, BF16):
+        raise ValueError(f"unknown output dtype {out_dtype}")
+    _require_packed("p", p)
+    odt = torch.bfloat16 if out_dtype == BF16 else torch.float32
     if out is None:
-        out = torch.empty((p.rows, p.cols), device=p.codes.device,
-                          dtype=torch.bfloat16 if out_dtype == BF16 else torch.float32)
+        out = torch.empty((p.rows, p.cols), device=p.codes.device, dtype=odt)
+    _require_buffer("out", out, (p.rows, p.cols), odt, p.codes.device)
     L = lib()
     args = (p.codes.data_ptr(), p.scales.data_ptr(), p.tensor_scale.data_ptr(), p.rows, p.cols,
             out.data_ptr(), out_dtype, _stream(p.codes))
@@ -219,25 +272,39 @@ def _dequantize(fn: str, p: Packed, out_dtype: int = F32, out: torch.Tensor | No
 
 
 def if4_dequantize(p: Packed, out_dtype=F32, out=None):
-    return _dequantize("if4_dequantize", p, out_dtype, out)
+    return _dequantize("if4_dequantize", p, out_dtype, out, IF4)
 
 
 def nvfp4_dequantize(p: Packed, out_dtype=F32, out=None):
-    return _dequantize("nvfp4_dequantize", p, out_dtype, out)
+    return _dequantize("nvfp4_dequantize", p, out_dtype, out, NVFP4)
 
 
 def ifx_dequantize(p: Packed, out_dtype=F32, out=None):
     return _dequantize("ifx_dequantize", p, out_dtype, out)
 
 
-def _gemm(fn: str, a: Packed, b: Packed, out_dtype: int = F32, out: torch.Tensor | None = None):
+def _gemm(fn: str, a: Packed, b: Packed, out_dtype: int = F32, out: torch.Tensor | None = None,
+          fixed_fmt: int | None = None):
     _require_gpu(a.codes, b.codes)
+    if a.fmt != b.fmt:
+        raise ValueError(f"A is format {a.fmt} and B format {b.fmt}: one GEMM takes one format")
+    if fixed_fmt is not None and a.fmt != fixed_fmt:
+        raise ValueError(f"{fn} takes {FORMAT_NAMES[fixed_fmt]} operands, got format {a.fmt}")
     if a.cols != b.cols:
         raise ValueError("A and B must share the grouped axis K")
+    if out_dtype not in (F32, BF16):
+        raise ValueError(f"unknown output dtype {out_dtype}")
+    dev = a.codes.device
+    _require_packed("A", a, dev)
+    _require_packed("B", b, dev)
     M, N, K = a.rows, b.rows, a.cols
+    odt = torch.bfloat16 if out_dtype == BF16 else torch.float32
     if out is None:
-        out = torch.empty((M, N), device=a.codes.device,
-                          dtype=torch.bfloat16 if out_dtype == BF16 else torch.float32)
+        out = torch.empty((M, N), device=dev, dtype=odt)
+    if out.device != dev or out.dtype != odt or tuple(out.shape) != (M, N) or \
+            (M > 0 and N > 0 and (out.stride(1) != 1 or out.stride(0) < N)):
+        raise ValueError(f"out must be a {odt} [{M}, {N}] tensor on {dev} with unit column stride "
+                         f"and row stride >= N")
     L = lib()
     args = (a.codes.data_ptr(), a.scales.data_ptr(), a.tensor_scale.data_ptr(), b.codes.data_ptr(),
             b.scales.data_ptr(), b.tensor_scale.data_ptr(), M, N, K, out.data_ptr(), out.stride(0),
@@ -250,11 +317,11 @@ def _gemm(fn: str, a: Packed, b: Packed, out_dtype: int = F32, out: torch.Tensor
 
 
 def if4_gemm(a: Packed, b: Packed, out_dtype=F32, out=None):
-    return _gemm("if4_gemm", a, b, out_dtype, out)
+    return _gemm("if4_gemm", a, b, out_dtype, out, IF4)
 
 
 def nvfp4_gemm(a: Packed, b: Packed, out_dtype=F32, out=None):
-    return _gemm("nvfp4_gemm", a, b, out_dtype, out)
+    return _gemm("nvfp4_gemm", a, b, out_dtype, out, NVFP4)
 
 
 def ifx_gemm(a: Packed, b: Packed, out_dtype=F32, out=None):

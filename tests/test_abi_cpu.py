@@ -41,13 +41,16 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_version_and_strings(L):
-    assert L.ifq_abi_version() == 1
+    assert L.ifq_abi_version() == 2
     assert L.ifq_status_string(0) == b"ok"
     assert L.ifq_status_string(-2) == b"invalid shape"
     assert L.ifq_codes_bytes(0, 256, 256) == 256 * 128
     assert L.ifq_codes_bytes(2, 16, 64) == 16 * 64 * 3 // 8
     assert L.ifq_codes_bytes(3, 16, 64) == 16 * 64 * 6 // 8
-    assert L.ifq_scales_bytes(256, 4096) == 256 * 256
+    assert L.ifq_scales_bytes(0, 256, 4096) == 256 * 256
+    assert L.ifq_scales_bytes(7, 256, 4096) == 256 * 512      # block size 8: one byte per 8 values
+    assert L.ifq_scales_bytes(8, 16, 64) == 16 * 8 and L.ifq_scales_bytes(9, 16, 64) == 16 * 8
+    assert L.ifq_scales_bytes(10, 16, 64) == 0 and L.ifq_scales_bytes(0, -1, 64) == 0
     assert L.ifq_quantize_workspace_bytes(0, 8192, 8192, 0) >= 4
     assert L.ifq_quantize_workspace_bytes(0, 8192, 8192, 8) == 0
     assert L.ifq_quantize_dual_workspace_bytes(0, 8192, 8192, 0, 8) >= 8

@@ -107,8 +107,13 @@ def test_dgrad_gemm(fmt):
     pw_row, pw_col = ops.ifx_quantize_dual(fmt, W.cuda())
     c = ops.ifx_gemm(pdy, pw_col, ops.F32).cpu().numpy()
     ody = O.quantize(bits(dy), fmt, O.SR, 0, 7)
+    np.testing.assert_array_equal(pdy.codes.cpu().numpy(), ody[0])
+    np.testing.assert_array_equal(pdy.scales.cpu().numpy(), ody[1])
+    assert float(pdy.tensor_scale.cpu()[0]) == ody[2]
     ow = O.quantize(bits(W), fmt, O.STRIDED)
     np.testing.assert_array_equal(pw_col.codes.cpu().numpy(), ow[0])
+    np.testing.assert_array_equal(pw_col.scales.cpu().numpy(), ow[1])
+    assert float(pw_col.tensor_scale.cpu()[0]) == ow[2]
     ref = O.gemm_ref(ody[0], ody[1], ody[2], ow[0], ow[1], ow[2], fmt)
     assert rel_fro(c, ref) <= 1e-3
     # and the product approximates dY W itself
@@ -134,8 +139,15 @@ def test_full_size_dual_dy_and_dgrad_sampled():
     got = c.cpu().numpy()[np.ix_(rows, cols)]
     A = O.dequantize(pr.codes.cpu().numpy()[rows], pr.scales.cpu().numpy()[rows],
                      float(pr.tensor_scale.cpu()[0]), ops.IF4, np.float64)
-    ow = O.quantize(np.ascontiguousarray(bits(W)[:, cols]), ops.IF4, O.STRIDED | O.SCALE_IN,
-                    tensor_scale=float(pw.tensor_scale.cpu()[0]))
+    # W's column-side alpha from the fused maxima pass against Eq. 1 on the
+    # whole tensor (no RHT on this side, so amax is max|W|) before the oracle
+    # takes it; then its codes and scale bytes of the sampled columns
+    wb = bits(W)
+    alpha_w = float(pw.tensor_scale.cpu()[0])
+    assert alpha_w == O.tensor_scale(ops.IF4, float(np.abs(O.bf16_to_f32(wb)).max()))
+    ow = O.quantize(np.ascontiguousarray(wb[:, cols]), ops.IF4, O.STRIDED | O.SCALE_IN,
+                    tensor_scale=alpha_w)
     np.testing.assert_array_equal(pw.codes.cpu().numpy()[cols], ow[0])
+    np.testing.assert_array_equal(pw.scales.cpu().numpy()[cols], ow[1])
     B = O.dequantize(ow[0], ow[1], ow[2], ops.IF4, np.float64)
     assert rel_fro(got, A @ B.T) <= 1e-3

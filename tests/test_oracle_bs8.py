@@ -1,5 +1,5 @@
 """Pins of the oracle's block-size-8 formats (IF4-BS8, IF3-BS8, NVFP4-BS8;
-Sec. 6 and Table 6: one E4M3 scale per 8 values, 5.0 and 4.0 bits per
+Sec. 5.1 and Table 6 (App. D): one E4M3 scale per 8 values, 5.0 and 4.0 bits per
 parameter for IF4-BS8 and IF3-BS8).
 
 - Bit budget: codes + scales of a tensor come to Table 6's bits/parameter.

@@ -106,3 +106,56 @@ def test_pack_roundtrip_and_density(oracle, fmt, bits_per_param):
         np.testing.assert_array_equal(oracle.unpack_group(fmt, packed), codes)
     # Table 6: code bits plus one 8-bit scale per 16 values
     assert (16 * bits + 8) / 16 == bits_per_param
+
+
+def _bf16_nearest_even_by_definition(f32: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns of finite fp32 values from the definition of
+    round-to-nearest-even: of the two bf16 numbers that bracket x (its
+    truncation toward zero and the next one away from zero), take the
+    nearer, measured exactly in fp64, and on a tie the one with the even
+    significand.  The largest finite bf16 rounds to infinity when the
+    next step would be reached."""
+    x = np.asarray(f32, dtype=np.float32)
+    u = x.view(np.uint32).astype(np.int64)
+    lo = (u >> 16) & 0xFFFF                       # truncation toward zero
+    hi = lo + 1                                   # next bf16 away from zero (sign kept)
+
+    def val(b):
+        return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+    xv = x.astype(np.float64)
+    mag_hi = np.where((hi & 0x7FFF) >= 0x7F80, np.inf, 0.0)
+    d_lo = np.abs(xv - val(lo))
+    vh = np.where(np.isinf(mag_hi), np.copysign(2.0 ** 128, xv), val(np.where((hi & 0x7FFF) >= 0x7F80, lo, hi)))
+    d_hi = np.abs(vh - xv)
+    pick_hi = (d_hi < d_lo) | ((d_hi == d_lo) & ((lo & 1) == 1))
+    return np.where(pick_hi, hi, lo).astype(np.uint16)
+
+
+def test_bf16_rounding_against_definition_and_torch(oracle):
+    """oracle.bf16_bits (the bf16 round-to-nearest-even behind every
+    expected bf16 output) against torch's float -> bfloat16 conversion and
+    against the rounding definition evaluated exactly: random finite fp32
+    bit patterns over every exponent, exact ties with even and odd
+    truncations, values one ulp either side of a tie, fp32 subnormals and
+    values near the bf16 overflow threshold (which round to infinity)."""
+    rng = np.random.default_rng(7)
+    u = rng.integers(0, 1 << 32, 1 << 20, dtype=np.uint64).astype(np.uint32)
+    u = u[(u & 0x7F800000) != 0x7F800000]                       # finite only
+    base = rng.integers(0, 1 << 16, 1 << 16, dtype=np.uint64).astype(np.uint32) << 16
+    base = base[(base & 0x7F800000) != 0x7F800000]
+    ties = base | 0x8000
+    near = np.concatenate([ties - 1, ties + 1])
+    sub = rng.integers(0, 1 << 23, 1 << 14, dtype=np.uint64).astype(np.uint32)
+    sub = np.concatenate([sub, sub | 0x80000000, np.array([0x00008000, 0x00018000, 0x80008000], np.uint32)])
+    top = np.arange(0x7F7F0000, 0x7F800000, 7, dtype=np.uint32)
+    top = np.concatenate([top, top | 0x80000000, np.array([0x7F7F7FFF, 0x7F7F8000, 0x7F7FFFFF], np.uint32)])
+    x = np.concatenate([u, ties, near, sub, top]).view(np.float32)
+    got = oracle.bf16_bits(x)
+    want_torch = torch.from_numpy(x.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(got, want_torch)
+    np.testing.assert_array_equal(got, _bf16_nearest_even_by_definition(x))
+    # spot values: a tie with an even truncation stays, an odd one rounds up
+    assert oracle.bf16_bits(np.array([1.0 + 2.0 ** -8], np.float32))[0] == 0x3F80
+    assert oracle.bf16_bits(np.array([1.0 + 3 * 2.0 ** -8], np.float32))[0] == 0x3F82
+    assert oracle.bf16_bits(np.array([np.float32(3.4e38)], np.float32))[0] == 0x7F80
