@@ -7,10 +7,13 @@ IF4 x IF4 GEMM Y = A_hat W_hat^T with bf16 output.  Inputs are resident in
 HBM before timing starts.  `value` is the step's whole-job throughput,
 2*M*N*K / step time.
 
-Also reported (one JSON line): per-kernel times from HIP events on the
-launch stream, the roofline of the dominant kernel (the GEMM, MFMA-bound) and
-of the quantizer (HBM-bound), the same kernels in NVFP4 mode, and the CPU
-oracle timed on a bounded sample of the same workload.
+Also reported (one JSON line on stdout; progress lines go to stderr):
+per-kernel times from HIP events on the launch stream, the roofline of the
+dominant kernel (the GEMM, MFMA-bound) and of the quantizer (HBM-bound), the
+same kernels in NVFP4 mode, the other measured workloads (the 8192^2
+quantizer sweep with and without the RHT, the weight-gradient quantizers and
+GEMM, the bit-width GEMMs at 8192^3, the dequantizer), and the CPU oracle
+timed on a bounded sample of the step, single- and multi-threaded.
 """
 from __future__ import annotations
 
@@ -35,6 +38,9 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-workloads", action="store_true",
+                   help="skip the other measured workloads (quantizer sweep, weight gradient, "
+                        "bit-width GEMMs, dequantizer) in the default run")
     p.add_argument("--cpu-rows", type=int, default=0,
                    help="activation rows in the CPU oracle's GEMM sample (0: all)")
     p.add_argument("--traffic-from", metavar="DIR",
@@ -44,10 +50,17 @@ def parse():
                                         "nvfp4_46", "if4_bs8", "if3_bs8", "nvfp4_bs8"], default="if4",
                    help="format of the --mode step run")
     p.add_argument("--small", action="store_true", help="1/8-size shapes (quick checks)")
-    p.add_argument("--mode", choices=["full", "step", "copy", "wgrad", "bitwidth", "dual", "dequant"], default="full",
+    p.add_argument("--mode", choices=["full", "step", "copy", "sweep", "wgrad", "bitwidth", "dual",
+                                      "dequant", "context"], default="full",
                    help="step: only the timed IF4 step (for counter runs); copy: a plain 1 GiB "
-                        "device copy, the reference for scaling the HBM byte counters")
+                        "device copy, the reference for scaling the HBM byte counters; sweep, "
+                        "wgrad, bitwidth, dequant: one of the other workloads alone; context: "
+                        "a device copy and a library FP16 GEMM at the step's sizes")
     return p.parse_args()
+
+
+def log(msg):
+    print(f"bench: {msg}", file=sys.stderr, flush=True)
 
 
 def main():
@@ -75,29 +88,19 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"mode": "copy", "bytes_read_per_launch": n, "bytes_written_per_launch": n}))
         return
-    if args.mode == "wgrad":
-        print(json.dumps({"mode": "wgrad", **wgrad_times(ops, workloads, torch)}))
-        return
-    if args.mode == "bitwidth":
-        print(json.dumps({"mode": "bitwidth", **bitwidth_times(ops, workloads, torch)}))
-        return
-    if args.mode == "dual":
-        print(json.dumps({"mode": "dual", **dual_times(ops, workloads, torch)}))
-        return
-    if args.mode == "dequant":
-        print(json.dumps({"mode": "dequant", **dequant_times(ops, workloads, torch)}))
+    single = {"sweep": quant_sweep_times, "wgrad": wgrad_times, "bitwidth": bitwidth_times,
+              "dual": dual_times, "dequant": dequant_times, "context": context_times}
+    if args.mode in single:
+        print(json.dumps({"mode": args.mode, **single[args.mode](ops, workloads, torch)}))
         return
     div = 8 if args.small else 1
     M, N, K = 8192 // div, 14336 // div, 4096 // div
+    t_gen = time.perf_counter()
     w = workloads.fwd_mlp(M, N, K)
     A = w.tensors["A"].cuda()
     W = w.tensors["W"].cuda()
     dev = A.device
-
-    def alloc(fmt, rows, cols):
-        return ops.Packed(fmt, torch.empty((rows, cols * ops.BITS[fmt] // 8), dtype=torch.uint8, device=dev),
-                          torch.empty((rows, cols // ops.GSIZE[fmt]), dtype=torch.uint8, device=dev),
-                          torch.empty(1, dtype=torch.float32, device=dev), rows, cols)
+    log(f"forward workload {M}x{N}x{K} generated ({time.perf_counter() - t_gen:.1f} s)")
 
     ws = torch.empty(4096, dtype=torch.uint8, device=dev)
     Y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
@@ -112,7 +115,7 @@ def main():
         if ev: ev[3].record()
 
     def timed(fmt, steps, warmup):
-        pa, pw = alloc(fmt, M, K), alloc(fmt, N, K)
+        pa, pw = alloc(ops, torch, fmt, M, K), alloc(ops, torch, fmt, N, K)
         for _ in range(warmup):
             run(fmt, pa, pw)
         torch.cuda.synchronize()
@@ -128,33 +131,6 @@ def main():
         step = np.mean([e[0].elapsed_time(e[3]) for e in evs]) * 1e-3
         return {"wall_s": wall, "step_s": step, "quant_A_s": qa, "quant_W_s": qw, "gemm_s": gm}
 
-    # single-pass quantize kernel alone (alpha supplied): the HBM-bound kernel.
-    # Launches run back to back between two events and cycle through COPIES
-    # copies of x and of the outputs: a copy was last touched COPIES - 1
-    # launches earlier (over 256 MB of other traffic), so every launch reads
-    # x from HBM, not from the 256 MB infinity cache, and no per-launch event
-    # or cache flush sits between the launches.
-    COPIES = 5
-
-    def timed_scale_in(fmt, x, steps, warmup):
-        q = ops.if4_quantize if fmt == ops.IF4 else ops.nvfp4_quantize
-        xs = [x.clone() for _ in range(COPIES)]
-        ps = [alloc(fmt, x.shape[0], x.shape[1]) for _ in range(COPIES)]
-        q(x, out=ps[0], workspace=ws)
-        ts = ps[0].tensor_scale.clone()
-        n = max(2 * steps, 8 * COPIES)
-        for i in range(max(warmup, COPIES)):
-            q(xs[i % COPIES], flags=ops.SCALE_IN, tensor_scale=ts, out=ps[i % COPIES])
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for i in range(n):
-            q(xs[i % COPIES], flags=ops.SCALE_IN, tensor_scale=ts, out=ps[i % COPIES])
-        e1.record()
-        torch.cuda.synchronize()
-        del xs, ps
-        return e0.elapsed_time(e1) * 1e-3 / n
-
     if args.mode == "step":
         fmt = {v: k for k, v in ops.FORMAT_NAMES.items()}[args.format]
         r = timed(fmt, args.steps, args.warmup)
@@ -162,14 +138,28 @@ def main():
                           "gemm_us": r["gemm_s"] * 1e6, "quant_A_us": r["quant_A_s"] * 1e6,
                           "quant_W_us": r["quant_W_s"] * 1e6}))
         return
+    # The other measured workloads run first: the step is then timed with
+    # the device already under sustained load, as in serving or training,
+    # rather than inside the power-management transient of a cold start.
+    extra = {}
+    if not args.no_workloads and not args.small:
+        for key, fn in (("quant_sweep", quant_sweep_times), ("wgrad", wgrad_times),
+                        ("bitwidth", bitwidth_times), ("dequant", dequant_times),
+                        ("context", context_times)):
+            t0 = time.perf_counter()
+            extra[key] = fn(ops, workloads, torch)
+            torch.cuda.empty_cache()
+            log(f"{key} workload timed ({time.perf_counter() - t0:.1f} s)")
     res = timed(ops.IF4, args.steps, args.warmup)
+    log(f"IF4 step timed: {res['step_s'] * 1e3:.3f} ms (GEMM {res['gemm_s'] * 1e6:.1f} us)")
     res_nv = timed(ops.NVFP4, max(5, args.steps // 2), 2)
     n_a, n_w = M * K, N * K
     flops = 2.0 * M * N * K
     qbytes_2pass = lambda n: n * (2 + 2 + 0.5 + 1 / 16)  # read for max, read + write codes/scales
     qbytes_1pass = lambda n: n * (2 + 0.5 + 1 / 16)
-    t_w_1p = timed_scale_in(ops.IF4, W, max(5, args.steps // 2), 2)
-    t_w_1p_nv = timed_scale_in(ops.NVFP4, W, max(5, args.steps // 2), 2)
+    t_w_1p = single_pass_time(ops, torch, ops.IF4, W, 0, max(5, args.steps // 2))
+    t_w_1p_nv = single_pass_time(ops, torch, ops.NVFP4, W, 0, max(5, args.steps // 2))
+    log(f"single-pass quantizer on W timed: IF4 {t_w_1p * 1e6:.1f} us, NVFP4 {t_w_1p_nv * 1e6:.1f} us")
 
     gemm_tflops = flops / res["gemm_s"] / 1e12
     out = {
@@ -210,14 +200,242 @@ def main():
                       "quant_W_us": round(res_nv["quant_W_s"] * 1e6, 2),
                       "quant_W_1pass_us": round(t_w_1p_nv * 1e6, 2),
                       "quant_W_1pass_GBps": round(qbytes_1pass(n_w) / t_w_1p_nv / 1e9, 1),
+                      "quant_W_1pass_frac": round(qbytes_1pass(n_w) / t_w_1p_nv / 1e9 / HBM_PEAK_GBS, 4),
                       "gemm_us": round(res_nv["gemm_s"] * 1e6, 2),
                       "gemm_TFLOPs": round(flops / res_nv["gemm_s"] / 1e12, 2),
+                      "gemm_frac": round(flops / res_nv["gemm_s"] / 1e12 / FP16_MFMA_PEAK_TFLOPS, 4),
                       "step_ms": round(res_nv["step_s"] * 1e3, 4)},
         },
     }
+    del A, W, Y
+    torch.cuda.empty_cache()
+    if extra:
+        out["workloads"] = extra
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, M, N, K, args.cpu_rows or M)
+        log("cpu baseline timed")
     print(json.dumps(out), flush=True)
+
+
+def alloc(ops, torch, fmt, rows, cols, dev="cuda"):
+    return ops.Packed(fmt, torch.empty((rows, cols * ops.BITS[fmt] // 8), dtype=torch.uint8, device=dev),
+                      torch.empty((rows, cols // ops.GSIZE[fmt]), dtype=torch.uint8, device=dev),
+                      torch.empty(1, dtype=torch.float32, device=dev), rows, cols)
+
+
+def rotating_time(torch, fns, n, warmup=None):
+    """Mean time of one launch in seconds, for launches that cycle through
+    len(fns) copies of their data: fns[i % len(fns)]() runs n times back to
+    back between two HIP events on the current stream, with no per-launch
+    event or cache flush between the launches.  With enough copies a copy
+    was last touched after more than the 256 MB infinity cache of other
+    traffic, so every launch reads its input from HBM."""
+    for i in range(max(len(fns), warmup or 0)):
+        fns[i % len(fns)]()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(n):
+        fns[i % len(fns)]()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e-3 / n
+
+
+def _copies_for(nbytes_per_launch, floor=3):
+    """Copies needed so that a copy's last use lies over 600 MB of other
+    traffic in the past (well beyond the 256 MB infinity cache)."""
+    return max(floor, int(600e6 // max(nbytes_per_launch, 1)) + 2)
+
+
+def single_pass_time(ops, torch, fmt, x, flags, steps, signs=0, seed=0):
+    """The quantize pass alone (alpha supplied): back-to-back launches over
+    rotating copies of x and of the outputs."""
+    R, Kq = (x.shape[1], x.shape[0]) if flags & ops.AXIS_STRIDED else (x.shape[0], x.shape[1])
+    n = x.numel()
+    copies = _copies_for(n * (2 + ops.BITS[fmt] / 8 + 1 / ops.GSIZE[fmt]), 5)
+    p0 = ops.ifx_quantize(fmt, x, flags, signs, seed)
+    ts = p0.tensor_scale.clone()
+    xs = [x] + [x.clone() for _ in range(copies - 1)]
+    ps = [alloc(ops, torch, fmt, R, Kq) for _ in range(copies)]
+    fns = [lambda i=i: ops.ifx_quantize(fmt, xs[i], flags | ops.SCALE_IN, signs, seed, tensor_scale=ts,
+                                        out=ps[i]) for i in range(copies)]
+    t = rotating_time(torch, fns, max(2 * steps, 8 * copies), 5)
+    del xs, ps, p0
+    return t
+
+
+def two_pass_time(ops, torch, fmt, x, flags, steps, signs=0, seed=0):
+    """Tensor-max pass + quantize pass (alpha from Eq. 1), back to back over
+    rotating copies."""
+    R, Kq = (x.shape[1], x.shape[0]) if flags & ops.AXIS_STRIDED else (x.shape[0], x.shape[1])
+    n = x.numel()
+    copies = _copies_for(n * (4 + ops.BITS[fmt] / 8 + 1 / ops.GSIZE[fmt]), 4)
+    xs = [x] + [x.clone() for _ in range(copies - 1)]
+    ps = [alloc(ops, torch, fmt, R, Kq) for _ in range(copies)]
+    wss = [torch.empty(4096, dtype=torch.uint8, device="cuda") for _ in range(copies)]
+    fns = [lambda i=i: ops.ifx_quantize(fmt, xs[i], flags, signs, seed, out=ps[i], workspace=wss[i])
+           for i in range(copies)]
+    t = rotating_time(torch, fns, max(2 * steps, 8 * copies), 5)
+    del xs, ps
+    return t
+
+
+def _quant_record(ops, fmt, n, t1, t2):
+    b = 2 + ops.BITS[fmt] / 8 + 1 / ops.GSIZE[fmt]
+    r = {"1pass_us": round(t1 * 1e6, 2), "1pass_GBps": round(n * b / t1 / 1e9, 1),
+         "1pass_frac": round(n * b / t1 / 1e9 / HBM_PEAK_GBS, 4)}
+    if t2 is not None:
+        r.update({"2pass_us": round(t2 * 1e6, 2),
+                  "2pass_GBps_algorithmic": round(n * b / t2 / 1e9, 1),
+                  "2pass_GBps_traffic": round(n * (b + 2) / t2 / 1e9, 1)})
+    return r
+
+
+def quant_sweep_times(ops, workloads, torch):
+    """Quantizer bandwidth sweep: X 8192 x 8192 t(3) * 0.5 with 0.1 % of
+    columns x50, row-wise, IF4 and NVFP4, with and without the fused 16-point
+    RHT: the quantize pass alone (alpha supplied) and both passes (alpha
+    from the tensor maximum), each over rotating copies (read from HBM).
+    Algorithmic bytes per element: 2 read, 0.5 + 1/16 written."""
+    w = workloads.quant_sweep()
+    x = w.tensors["X"].cuda()
+    signs = w.info["rht_signs"]
+    n = x.numel()
+    res = {"workload": f"quant_sweep_{x.shape[0]}x{x.shape[1]}",
+           "bytes_per_element": {"1pass": 2.5625, "2pass_traffic": 4.5625}}
+    for fmt in (ops.IF4, ops.NVFP4):
+        for rht in (False, True):
+            fl = ops.RHT if rht else 0
+            t1 = single_pass_time(ops, torch, fmt, x, fl, 20, signs)
+            t2 = two_pass_time(ops, torch, fmt, x, fl, 20, signs)
+            res[f"{ops.FORMAT_NAMES[fmt]}{'_rht' if rht else ''}"] = _quant_record(ops, fmt, n, t1, t2)
+    return res
+
+
+def _steady_time(torch, fn, steps=10, warmup=20):
+    """Mean time of fn() in seconds under sustained load, as in the timed
+    step: `warmup` launches back to back (the GEMM's power-management
+    transient settles within them), then `steps` launches back to back, each
+    between two HIP events, with one synchronisation at the end."""
+    for _ in range(warmup):
+        fn()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for e0, e1 in evs:
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    return float(sum(e0.elapsed_time(e1) for e0, e1 in evs) / steps * 1e-3)
+
+
+def _gemm_record(M, N, K, t):
+    tf = 2.0 * M * N * K / t / 1e12
+    return {"gemm_us": round(t * 1e6, 1), "gemm_TFLOPs": round(tf, 1),
+            "gemm_frac": round(tf / FP16_MFMA_PEAK_TFLOPS, 4)}
+
+
+def wgrad_times(ops, workloads, torch):
+    """Weight gradient dW = dY^T X (dY 8192 x 14336, X 8192 x 4096, both
+    quantized along the token axis with RHT, SR and the 16/17 margin; fp32
+    out): each quantizer's pass alone (alpha supplied) and both passes, over
+    rotating copies, and the GEMM M = 14336, N = 4096, K = 8192 under
+    sustained load, in IF4 and NVFP4."""
+    w = workloads.wgrad()
+    dy, x = w.tensors["dY"].cuda(), w.tensors["X"].cuda()
+    fl = ops.AXIS_STRIDED | ops.RHT | ops.SR | ops.MARGIN_16_17
+    signs = w.info["rht_signs"]
+    sd, sx = w.info["sr_seed_dY"], w.info["sr_seed_X"]
+    M, N, K = w.info["M"], w.info["N"], w.info["K"]
+    res = {"workload": f"wgrad_{M}x{N}x{K}",
+           "quantize": "strided (token axis), RHT + SR + 16/17 margin"}
+    out = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    for fmt in (ops.IF4, ops.NVFP4):
+        r = {}
+        for name, t, seed in (("dY", dy, sd), ("X", x, sx)):
+            t1 = single_pass_time(ops, torch, fmt, t, fl, 10, signs, seed)
+            t2 = two_pass_time(ops, torch, fmt, t, fl, 10, signs, seed)
+            r[f"quant_{name}"] = _quant_record(ops, fmt, t.numel(), t1, t2)
+        pdy = ops.ifx_quantize(fmt, dy, fl, signs, sd)
+        px = ops.ifx_quantize(fmt, x, fl, signs, sx)
+        r.update(_gemm_record(M, N, K, _steady_time(torch, lambda: ops.ifx_gemm(pdy, px, ops.F32, out), 10)))
+        res[ops.FORMAT_NAMES[fmt]] = r
+        del pdy, px
+    return res
+
+
+def bitwidth_times(ops, workloads, torch):
+    """Bit-width study: A, B 8192 x 8192 (N(0,1), 0.05 % of elements x100)
+    quantized along K in every format (both passes, rotating copies of A),
+    then the 8192^3 GEMM with bf16 out under sustained load."""
+    w = workloads.bitwidth()
+    a, b = w.tensors["A"].cuda(), w.tensors["B"].cuda()
+    n = a.shape[0]
+    out = torch.empty((n, n), dtype=torch.bfloat16, device="cuda")
+    res = {"workload": f"bitwidth_{n}^3"}
+    for fmt, name in ops.FORMAT_NAMES.items():
+        pa, pb = ops.ifx_quantize(fmt, a), ops.ifx_quantize(fmt, b)
+        t_q = two_pass_time(ops, torch, fmt, a, 0, 10)
+        t_g = _steady_time(torch, lambda: ops.ifx_gemm(pa, pb, ops.BF16, out), 10)
+        r = {"quant_2pass_us": round(t_q * 1e6, 1)}
+        r.update(_gemm_record(n, n, n, t_g))
+        res[name] = r
+        del pa, pb
+    return res
+
+
+def dequant_times(ops, workloads, torch):
+    """Standalone dequantizer on the weights W 14336 x 4096, bf16 and fp32
+    out, over rotating copies of the packed input and of the output.
+    Algorithmic bytes per element: codes b/8 + scales 1/G read, 2 or 4
+    written."""
+    W = workloads.fwd_mlp().tensors["W"].cuda()
+    n = W.numel()
+    res = {"workload": f"dequant_{W.shape[0]}x{W.shape[1]}"}
+    for fmt in (ops.IF4, ops.NVFP4, ops.NVINT4, ops.IF3, ops.IF6_E2M3):
+        p = ops.ifx_quantize(fmt, W)
+        read = ops.BITS[fmt] / 8 + 1 / ops.GSIZE[fmt]
+        r = {}
+        for dt, tag, wb in ((ops.BF16, "bf16", 2), (ops.F32, "fp32", 4)):
+            copies = _copies_for(n * (read + wb), 4)
+            ps = [p] + [ops.Packed(fmt, p.codes.clone(), p.scales.clone(), p.tensor_scale.clone(), p.rows, p.cols)
+                        for _ in range(copies - 1)]
+            outs = [ops.ifx_dequantize(q, dt) for q in ps]
+            fns = [lambda i=i: ops.ifx_dequantize(ps[i], dt, outs[i]) for i in range(copies)]
+            t = rotating_time(torch, fns, 8 * copies, 5)
+            r[tag + "_us"] = round(t * 1e6, 1)
+            r[tag + "_GBps"] = round(n * (read + wb) / t / 1e9, 1)
+            r[tag + "_frac"] = round(n * (read + wb) / t / 1e9 / HBM_PEAK_GBS, 4)
+            del ps, outs
+        res[ops.FORMAT_NAMES[fmt]] = r
+        del p
+    return res
+
+
+def context_times(ops, workloads, torch):
+    """Context for the fractions, not a result of this library: a plain
+    device-to-device copy of 117 MB (the size of W's bf16 data) over
+    rotating buffers, and the library FP16 GEMM (torch.matmul, hipBLASLt)
+    at the step's 8192 x 14336 x 4096 on N(0,1) FP16 operands under
+    sustained load."""
+    n = 14336 * 4096 * 2
+    copies = _copies_for(2 * n, 4)
+    srcs = [torch.ones(n, dtype=torch.uint8, device="cuda") for _ in range(copies)]
+    dsts = [torch.empty(n, dtype=torch.uint8, device="cuda") for _ in range(copies)]
+    t = rotating_time(torch, [lambda i=i: dsts[i].copy_(srcs[i]) for i in range(copies)], 8 * copies, 5)
+    del srcs, dsts
+    g = torch.Generator(device="cuda").manual_seed(1)
+    a = torch.randn((8192, 4096), generator=g, device="cuda", dtype=torch.float16)
+    bt = torch.randn((14336, 4096), generator=g, device="cuda", dtype=torch.float16)
+    b = bt.t()
+    c = torch.empty((8192, 14336), device="cuda", dtype=torch.float16)
+    tg = _steady_time(torch, lambda: torch.mm(a, b, out=c), 10)
+    del a, bt, b, c
+    return {"copy_117MB_GBps": round(2 * n / t / 1e9, 1),
+            "copy_117MB_frac": round(2 * n / t / 1e9 / HBM_PEAK_GBS, 4),
+            "fp16_matmul_8192x14336x4096_us": round(tg * 1e6, 1),
+            "fp16_matmul_TFLOPs": round(2.0 * 8192 * 14336 * 4096 / tg / 1e12, 1),
+            "fp16_matmul_frac": round(2.0 * 8192 * 14336 * 4096 / tg / 1e12 / FP16_MFMA_PEAK_TFLOPS, 4)}
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
@@ -253,73 +471,6 @@ def _event_time(torch, fn, steps, warmup, flush=None):
     return float(sum(times) / len(times))
 
 
-def _steady_time(torch, fn, steps=10, warmup=20):
-    """Mean time of fn() in seconds under sustained load, as in the timed
-    step: `warmup` launches back to back (the GEMM's power-management
-    transient settles within them), then `steps` launches back to back, each
-    between two HIP events, with one synchronisation at the end."""
-    for _ in range(warmup):
-        fn()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    for e0, e1 in evs:
-        e0.record()
-        fn()
-        e1.record()
-    torch.cuda.synchronize()
-    return float(sum(e0.elapsed_time(e1) for e0, e1 in evs) / steps * 1e-3)
-
-
-def wgrad_times(ops, workloads, torch):
-    """Weight gradient dW = dY^T X (dY 8192 x 14336, X 8192 x 4096, both
-    quantized along the token axis with RHT, SR and the 16/17 margin; fp32
-    out): quantizer times (two-pass, and single-pass with alpha supplied and
-    a cache flush) and the GEMM M = 14336, N = 4096, K = 8192."""
-    w = workloads.wgrad()
-    dy, x = w.tensors["dY"].cuda(), w.tensors["X"].cuda()
-    ws = torch.empty(4096, dtype=torch.uint8, device="cuda")
-    fl = ops.AXIS_STRIDED | ops.RHT | ops.SR | ops.MARGIN_16_17
-    signs = w.info["rht_signs"]
-    sd, sx = w.info["sr_seed_dY"], w.info["sr_seed_X"]
-    pdy = ops.if4_quantize(dy, fl, signs, sd, workspace=ws)
-    px = ops.if4_quantize(x, fl, signs, sx, workspace=ws)
-    flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device="cuda")
-    t_dy = _event_time(torch, lambda: ops.if4_quantize(dy, fl, signs, sd, out=pdy, workspace=ws), 10, 2, flush)
-    t_dy1 = _event_time(torch, lambda: ops.if4_quantize(dy, fl | ops.SCALE_IN, signs, sd,
-                                                        tensor_scale=pdy.tensor_scale, out=pdy), 10, 2, flush)
-    t_x = _event_time(torch, lambda: ops.if4_quantize(x, fl, signs, sx, out=px, workspace=ws), 10, 2, flush)
-    del flush
-    M, N, K = w.info["M"], w.info["N"], w.info["K"]
-    out = torch.empty((M, N), dtype=torch.float32, device="cuda")
-    t_g = _steady_time(torch, lambda: ops.if4_gemm(pdy, px, ops.F32, out), 20)
-    n_dy = dy.numel()
-    return {"workload": f"wgrad_{M}x{N}x{K}", "quant_dY_us": round(t_dy * 1e6, 1),
-            "quant_dY_1pass_us": round(t_dy1 * 1e6, 1),
-            "quant_dY_1pass_GBps": round(n_dy * 2.5625 / t_dy1 / 1e9, 1),
-            "quant_X_us": round(t_x * 1e6, 1), "gemm_us": round(t_g * 1e6, 1),
-            "gemm_TFLOPs": round(2.0 * M * N * K / t_g / 1e12, 1)}
-
-
-def bitwidth_times(ops, workloads, torch):
-    """Bit-width study: A, B 8192 x 8192 (N(0,1), 0.05 % of elements x100)
-    quantized along K in every format (both passes, cache flushed), then the
-    8192^3 GEMM with bf16 out under sustained load."""
-    w = workloads.bitwidth()
-    a, b = w.tensors["A"].cuda(), w.tensors["B"].cuda()
-    n = a.shape[0]
-    ws = torch.empty(4096, dtype=torch.uint8, device="cuda")
-    out = torch.empty((n, n), dtype=torch.bfloat16, device="cuda")
-    res = {"workload": f"bitwidth_{n}^3"}
-    flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device="cuda")
-    for fmt, name in ops.FORMAT_NAMES.items():
-        pa, pb = ops.ifx_quantize(fmt, a, workspace=ws), ops.ifx_quantize(fmt, b, workspace=ws)
-        t_q = _event_time(torch, lambda: ops.ifx_quantize(fmt, a, out=pa, workspace=ws), 5, 2, flush)
-        t_g = _steady_time(torch, lambda: ops.ifx_gemm(pa, pb, ops.BF16, out), 10)
-        res[name] = {"quant_us": round(t_q * 1e6, 1), "gemm_us": round(t_g * 1e6, 1),
-                     "gemm_TFLOPs": round(2.0 * n ** 3 / t_g / 1e12, 1)}
-        del pa, pb
-    return res
-
-
 def dual_times(ops, workloads, torch):
     """Training-step quantization of one linear layer's tensors in both
     layouts (X 8192 x 4096 and W 14336 x 4096 with RTN, RHT on X's token
@@ -351,31 +502,6 @@ def dual_times(ops, workloads, torch):
     t_g = _steady_time(torch, lambda: ops.if4_gemm(pdy, pw, ops.BF16, out), 20)
     res["dgrad"] = {"workload": f"dgrad_{M}x{N}x{K}", "gemm_us": round(t_g * 1e6, 1),
                     "gemm_TFLOPs": round(2.0 * M * N * K / t_g / 1e12, 1)}
-    return res
-
-
-def dequant_times(ops, workloads, torch):
-    """Standalone dequantizer on the weights W 14336 x 4096 in every format,
-    bf16 and fp32 out, cache flushed before every launch.  Algorithmic bytes
-    per element: codes b/8 + scales 1/G read, 2 or 4 written."""
-    W = workloads.fwd_mlp().tensors["W"].cuda()
-    n = W.numel()
-    ws = torch.empty(4096, dtype=torch.uint8, device="cuda")
-    flush = torch.empty(512 * 1024 * 1024, dtype=torch.uint8, device="cuda")
-    res = {"workload": f"dequant_{W.shape[0]}x{W.shape[1]}"}
-    for fmt, name in ops.FORMAT_NAMES.items():
-        p = ops.ifx_quantize(fmt, W, workspace=ws)
-        read = ops.BITS[fmt] / 8 + 1 / ops.GSIZE[fmt]
-        r = {}
-        for dt, tag, wb in ((ops.BF16, "bf16", 2), (ops.F32, "fp32", 4)):
-            out = ops.ifx_dequantize(p, dt)
-            t = _event_time(torch, lambda: ops.ifx_dequantize(p, dt, out), 10, 2, flush)
-            r[tag + "_us"] = round(t * 1e6, 1)
-            r[tag + "_GBps"] = round(n * (read + wb) / t / 1e9, 1)
-            del out
-        res[name] = r
-        del p
-    del flush
     return res
 
 
@@ -434,11 +560,21 @@ def record_traffic(d):
 
 
 def cpu_baseline(w, M, N, K, rows):
-    """The CPU oracle on a bounded sample of the same step: the C oracle
-    quantizes all of A and W (one thread; the step's whole quantize work),
-    then its reference GEMM (dequantize to fp64, numpy BLAS product) runs for
-    `rows` rows of A against all of W.  The product's time is scaled by
-    M/rows; the quantize time and W's dequantize are taken as measured."""
+    """The CPU oracle on the same step, no extrapolation of the quantize work:
+
+    - quantize A and W to IF4 with the C oracle on one thread (alpha from the
+      whole tensor, as the oracle does it), and again with threads over row
+      blocks on the cores this process may use (alpha from the tensor
+      maximum first, then each block quantized with that alpha: row groups
+      are independent given alpha, so the result is the same bytes, which
+      is checked);
+    - dequantize W to fp64 (threads over row blocks) and run the reference
+      GEMM (numpy BLAS, fp64) for `rows` rows of A against all of W; the
+      product's time is scaled by M/rows.
+
+    `value` uses the multi-threaded legs; each leg reports its threads."""
+    import concurrent.futures as cf
+
     import numpy as np
     import torch
 
@@ -449,27 +585,56 @@ def cpu_baseline(w, M, N, K, rows):
         return t.contiguous().view(torch.int16).numpy().view(np.uint16)
 
     a, wt = bits(w.tensors["A"]), bits(w.tensors["W"])
+    nthreads = max(1, min(len(os.sched_getaffinity(0)), 16))
+
     t0 = time.perf_counter()
     ca, sa, aa = O.quantize(a, O.FMT_IF4)
     cw, sw, aw = O.quantize(wt, O.FMT_IF4)
-    t_q = time.perf_counter() - t0
-    t1 = time.perf_counter()
-    Wd = O.dequantize(cw, sw, aw, O.FMT_IF4, np.float64)
-    t_dw = time.perf_counter() - t1
-    t2 = time.perf_counter()
+    t_q1 = time.perf_counter() - t0
+
+    def blocks(n):
+        step = -(-n // (4 * nthreads))
+        return [(r, min(n, r + step)) for r in range(0, n, step)]
+
+    def quantize_mt(x, pool):
+        alpha = O.tensor_scale(O.FMT_IF4, float(np.abs(O.bf16_to_f32(x)).max()))
+        parts = list(pool.map(lambda rr: O.quantize(np.ascontiguousarray(x[rr[0]:rr[1]]), O.FMT_IF4,
+                                                    O.SCALE_IN, tensor_scale=alpha), blocks(x.shape[0])))
+        return np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts]), alpha
+
+    with cf.ThreadPoolExecutor(nthreads) as pool:
+        t1 = time.perf_counter()
+        qa = quantize_mt(a, pool)
+        qw = quantize_mt(wt, pool)
+        t_qm = time.perf_counter() - t1
+        same = all(np.array_equal(u, v) for u, v in ((qa[0], ca), (qa[1], sa), (qw[0], cw), (qw[1], sw))) \
+            and qa[2] == aa and qw[2] == aw
+        t2 = time.perf_counter()
+        Wd = np.concatenate(list(pool.map(lambda rr: O.dequantize(cw[rr[0]:rr[1]], sw[rr[0]:rr[1]], aw, O.FMT_IF4,
+                                                                  np.float64), blocks(N))))
+        t_dw = time.perf_counter() - t2
+    t3 = time.perf_counter()
     Ad = O.dequantize(ca[:rows], sa[:rows], aa, O.FMT_IF4, np.float64)
     _ = Ad @ Wd.T
-    t_g = time.perf_counter() - t2
+    t_g = time.perf_counter() - t3
     blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    t_full = t_q + t_dw + t_g * M / rows
     flops = 2.0 * M * N * K
+    t_full = t_qm + t_dw + t_g * M / rows
+    t_full1 = t_q1 + t_dw + t_g * M / rows
     return {"value": round(flops / t_full / 1e12, 6), "unit": "TFLOP/s",
-            "cores": int(blas_threads), "kind": "oracle",
-            "sample": f"IF4 quantize of all of A and W (C oracle, 1 thread, {t_q:.2f} s), "
-                      f"fp64 dequantize of W ({t_dw:.2f} s), reference GEMM of {rows} of {M} rows of A "
-                      f"against all {N} rows of W (numpy BLAS, {blas_threads} threads, {t_g:.2f} s, "
+            "cores": int(max(nthreads, blas_threads)), "kind": "oracle",
+            "sample": f"the whole step on the CPU: IF4 quantize of all of A and W (C oracle, "
+                      f"{nthreads} threads over row blocks, {t_qm:.2f} s; on 1 thread {t_q1:.2f} s), fp64 "
+                      f"dequantize of W ({nthreads} threads, {t_dw:.2f} s), reference GEMM of {rows} of {M} "
+                      f"rows of A against all {N} rows of W (numpy BLAS, {blas_threads} threads, {t_g:.2f} s, "
                       f"scaled by M/{rows})",
-            "seconds": round(t_q + t_dw + t_g, 2)}
+            "legs": {"quantize_threads": nthreads, "quantize_s": round(t_qm, 3),
+                     "quantize_1thread_s": round(t_q1, 3), "quantize_results_identical": bool(same),
+                     "dequantize_W_threads": nthreads, "dequantize_W_s": round(t_dw, 3),
+                     "gemm_ref_threads": int(blas_threads), "gemm_ref_s": round(t_g, 3),
+                     "gemm_ref_rows": rows},
+            "value_with_1thread_quantize": round(flops / t_full1 / 1e12, 6),
+            "seconds": round(t_q1 + t_qm + t_dw + t_g, 2)}
 
 
 if __name__ == "__main__":
