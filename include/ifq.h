@@ -165,6 +165,24 @@ int ifx_quantize(int format, const void* x, int64_t rows, int64_t cols, int64_t 
                  uint8_t* scales, float* tensor_scale, void* workspace, size_t workspace_bytes,
                  void* stream);
 
+/* ifx_quantize without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, checks and results as
+ * ifx_quantize, bit for bit.  The per-block maxima of the tensor-max pass go
+ * to a 1 KiB scratch array inside the library, one per GPU, held until the
+ * process ends; its address is looked up once per device (the device of
+ * `stream`, or the current device for the null stream).  The scratch holds
+ * at most 256 partial maxima whatever the tensor size, so no size is
+ * rejected for it; a requirement above its 1 KiB (none today) would return
+ * IFQ_EWORKSPACE.  Nothing in it needs to start at zero: each call writes
+ * every entry it reads.  Calls on one GPU share the scratch: calls that can
+ * overlap in time on one GPU (different streams without ordering) race and
+ * must not be made.  Allocates nothing (no hipMalloc, no library allocation).
+ */
+int ifx_quantize_noalloc(int format, const void* x, int64_t rows, int64_t cols, int64_t ld_x,
+                         uint32_t flags, uint32_t rht_signs, uint64_t seed, uint8_t* codes,
+                         uint8_t* scales, float* tensor_scale, void* stream);
+
 /* Bytes of device workspace the quantizer needs (0 with IFQ_SCALE_IN). */
 size_t ifq_quantize_workspace_bytes(int format, int64_t rows, int64_t cols, uint32_t flags);
 

@@ -26,9 +26,12 @@ int bits_of(int f)
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// own_scratch: the partials go to the library's device scratch instead of a
+// caller workspace (the allocation-free entry point).
 int quantize_impl(int fmt, const void* x, int64_t rows, int64_t cols, int64_t ld_x, uint32_t flags,
                   uint32_t rht_signs, uint64_t seed, uint8_t* codes, uint8_t* scales,
-                  float* tensor_scale, void* workspace, size_t workspace_bytes, void* stream)
+                  float* tensor_scale, void* workspace, size_t workspace_bytes, void* stream,
+                  bool own_scratch = false)
 {
     if (!valid_format(fmt)) return IFQ_EINVAL;
     if (flags & ~kKnownFlags) return IFQ_EINVAL;
@@ -49,7 +52,15 @@ int quantize_impl(int fmt, const void* x, int64_t rows, int64_t cols, int64_t ld
         if (!strided && (!aligned(x, 16) || (ld_x % 8))) return IFQ_EALIGN;
         if (!aligned(x, 2)) return IFQ_EALIGN;
         if (!aligned(codes, 16)) return IFQ_EALIGN;
-        if (!(flags & IFQ_SCALE_IN)) {
+        if (own_scratch) {
+            if (ifq_quantize_workspace_bytes(fmt, rows, cols, flags) > ifq::kScratchBytes)
+                return IFQ_EWORKSPACE;
+            if (!(flags & IFQ_SCALE_IN)) {
+                float* p = nullptr;
+                if (ifq::scratch_partials(static_cast<hipStream_t>(stream), &p) != hipSuccess) return IFQ_EHIP;
+                workspace = p;
+            }
+        } else if (!(flags & IFQ_SCALE_IN)) {
             if (!workspace || workspace_bytes < ifq_quantize_workspace_bytes(fmt, rows, cols, flags))
                 return IFQ_EWORKSPACE;
             if (!aligned(workspace, 16)) return IFQ_EALIGN;
@@ -155,6 +166,14 @@ int ifx_quantize(int format, const void* x, int64_t rows, int64_t cols, int64_t 
 {
     return quantize_impl(format, x, rows, cols, ld_x, flags, rht_signs, seed, codes, scales,
                          tensor_scale, workspace, workspace_bytes, stream);
+}
+
+int ifx_quantize_noalloc(int format, const void* x, int64_t rows, int64_t cols, int64_t ld_x,
+                         uint32_t flags, uint32_t rht_signs, uint64_t seed, uint8_t* codes,
+                         uint8_t* scales, float* tensor_scale, void* stream)
+{
+    return quantize_impl(format, x, rows, cols, ld_x, flags, rht_signs, seed, codes, scales,
+                         tensor_scale, nullptr, 0, stream, true);
 }
 
 size_t ifq_quantize_workspace_bytes(int format, int64_t rows, int64_t cols, uint32_t flags)

@@ -25,6 +25,12 @@ struct QuantArgs {
 
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t stream);
 
+// The library's own device scratch for the tensor-max partials (one copy per
+// GPU, kScratchBytes): its address on the device of `stream` (the current
+// device for the null stream), looked up once per device.
+constexpr size_t kScratchBytes = kMaxPartials * sizeof(float);
+hipError_t scratch_partials(hipStream_t stream, float** ptr);
+
 // One side of the dual quantizer (row-wise or strided output).
 struct DualSide {
     uint32_t flags;  // IFQ_* bits of this side (IFQ_AXIS_STRIDED excluded)

@@ -10,6 +10,8 @@
 // Row-wise: a group is 32 contiguous bytes of bf16, read with two 128-bit
 // loads.  Strided axis: a 64x64 tile is staged through LDS so that a lane
 // can gather 16 consecutive rows of one column.
+#include <mutex>
+
 #include "device.h"
 #include "launch.h"
 
@@ -1074,6 +1076,46 @@ hipError_t launch_quantize_dual(const DualArgs& a, hipStream_t s)
         case IFQ_FMT_NVINT4: return launch_dual_fmt<IFQ_FMT_NVINT4>(k, grid, sr_r, sr_c, s);
         default: return launch_dual_fmt<IFQ_FMT_NVFP4_46>(k, grid, sr_r, sr_c, s);
     }
+}
+
+// Scratch of the allocation-free quantize entry point: room for the
+// per-block maxima of the tensor-max pass.  Every GPU the library runs on
+// holds its own copy until the process ends.  In host code the array's name
+// is not a device address; the address is taken once per device, with that
+// device current, from hipGetSymbolAddress and kept in scratch_ptr.
+static __device__ __align__(256) float scratch[kMaxPartials];
+static_assert(sizeof(scratch) == kScratchBytes, "scratch size");
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex scratch_mu;
+float* scratch_ptr[kMaxScratchDevices];
+}  // namespace
+
+hipError_t scratch_partials(hipStream_t s, float** ptr)
+{
+    int dev = -1;
+    hipError_t e = s ? hipStreamGetDevice(s, &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (!scratch_ptr[dev]) {
+        int cur = -1;
+        e = hipGetDevice(&cur);
+        if (e != hipSuccess) return e;
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur != dev) {
+            const hipError_t e2 = hipSetDevice(cur);
+            if (e == hipSuccess) e = e2;
+        }
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        scratch_ptr[dev] = static_cast<float*>(p);
+    }
+    *ptr = scratch_ptr[dev];
+    return hipSuccess;
 }
 
 }  // namespace ifq

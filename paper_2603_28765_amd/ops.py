@@ -61,6 +61,7 @@ def lib() -> C.CDLL:
         for name in ("if4_quantize", "nvfp4_quantize"):
             getattr(L, name).argtypes = _QUANT_ARGS
         L.ifx_quantize.argtypes = [C.c_int] + _QUANT_ARGS
+        L.ifx_quantize_noalloc.argtypes = [C.c_int] + _QUANT_ARGS[:10] + [C.c_void_p]
         for name in ("if4_dequantize", "nvfp4_dequantize"):
             getattr(L, name).argtypes = _DEQ_ARGS
         L.ifx_dequantize.argtypes = [C.c_int] + _DEQ_ARGS
@@ -173,14 +174,16 @@ def _quantize(fn: str, fmt: int, x: torch.Tensor, flags: int = 0, rht_signs: int
     if K % 16 == 0:  # other shapes are rejected by the library itself
         _require_packed("out", out, dev)
     L = lib()
-    wsb = L.ifq_quantize_workspace_bytes(fmt, rows, cols, flags)
+    wsb = 0 if fn == "ifx_quantize_noalloc" else L.ifq_quantize_workspace_bytes(fmt, rows, cols, flags)
     if wsb and workspace is None:
         workspace = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
     ws_ptr = workspace.data_ptr() if workspace is not None else None
     ws_len = workspace.numel() if workspace is not None else 0
     args = (x.data_ptr(), rows, cols, x.stride(0), flags, rht_signs, seed, out.codes.data_ptr(),
             out.scales.data_ptr(), out.tensor_scale.data_ptr(), ws_ptr, ws_len, _stream(x))
-    if fn == "ifx_quantize":
+    if fn == "ifx_quantize_noalloc":
+        _check(fn, L.ifx_quantize_noalloc(fmt, *args[:10], args[12]))
+    elif fn == "ifx_quantize":
         _check(fn, L.ifx_quantize(fmt, *args))
     else:
         _check(fn, getattr(L, fn)(*args))
@@ -199,6 +202,14 @@ def nvfp4_quantize(x, flags=0, rht_signs=0, seed=0, tensor_scale=None, out=None,
 def ifx_quantize(fmt, x, flags=0, rht_signs=0, seed=0, tensor_scale=None, out=None,
                  workspace=None):
     return _quantize("ifx_quantize", fmt, x, flags, rht_signs, seed, tensor_scale, out, workspace)
+
+
+def ifx_quantize_noalloc(fmt, x, flags=0, rht_signs=0, seed=0, tensor_scale=None, out=None):
+    """ifx_quantize through the entry point that allocates nothing: the
+    library keeps its tensor-max partials in its own device scratch.  Pass
+    `out` (and `tensor_scale`) to keep this call free of allocations on the
+    Python side as well."""
+    return _quantize("ifx_quantize_noalloc", fmt, x, flags, rht_signs, seed, tensor_scale, out)
 
 
 def _packed_for(fmt: int, R: int, K: int, dev, tensor_scale=None) -> Packed:

@@ -94,6 +94,23 @@ def test_quantize_validation(L):
     assert q(L, wsb=8) == EWORKSPACE
 
 
+def test_noalloc_quantize_validation(L):
+    """The allocation-free entry point checks its arguments like
+    ifx_quantize before it touches the device (no workspace argument)."""
+    qn = lambda fmt=0, x=P16, rows=32, cols=64, ld=64, flags=0, signs=0, codes=P16, ts=P16: \
+        L.ifx_quantize_noalloc(fmt, x, rows, cols, ld, flags, signs, 0, codes, P16, ts, None)
+    assert qn(ts=None) == EINVAL
+    assert qn(x=None) == EINVAL
+    assert qn(fmt=10) == EINVAL
+    assert qn(flags=1 << 7) == EINVAL
+    assert qn(signs=1 << 16) == EINVAL
+    assert qn(cols=40, ld=40) == ESHAPE
+    assert qn(rows=40, flags=16) == ESHAPE
+    assert qn(ld=48) == ESHAPE
+    assert qn(x=P_ODD) == EALIGN
+    assert qn(codes=P16 + 8) == EALIGN
+
+
 def g(L, fmt=None, a=P16, b=P16, M=64, N=64, K=64, c=P16, ldc=64, dtype=0, ts=P16):
     args = (a, P16, ts, b, P16, ts, M, N, K, c, ldc, dtype, None)
     if fmt is None:
