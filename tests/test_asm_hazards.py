@@ -102,3 +102,157 @@ def test_fast_gemm_kernels_have_no_pending_load_hazards(gemm_asm):
         assert loads >= 16, (name, loads)
         bad = vmem_violations(body, header, back)
         assert bad == [], (name, bad[:3])
+
+
+# ----------------------------------------------------------------- LDS side
+# The copies into LDS (global_load_lds_dwordx4) are asm too.  Their data is
+# safe to read once the copying wave has drained them with a vmcnt wait and
+# every wave has passed a barrier after that, and a slot may be refilled only
+# after a barrier that follows its last read.  Two checks: the compiled code
+# drains every copy before the second barrier after its issue (so it is
+# visible one barrier period later), and the slot schedule of the kernel
+# reads every chunk at least one barrier after that and refills a slot only
+# after its last read.
+
+def lds_copy_violations(lines, loop_header, back_edge):
+    """At every s_barrier along prologue, two loop iterations and epilogue,
+    return the copies into LDS still outstanding that were issued before the
+    previous barrier."""
+    path = (list(range(0, back_edge + 1)) + list(range(loop_header, back_edge + 1)) * 2
+            + list(range(back_edge + 1, len(lines))))
+    queue, bad, barriers = [], [], 0
+    for i in path:
+        ln = lines[i].strip()
+        if not ln or ln.startswith((".", ";")) or ln.endswith(":"):
+            continue
+        op = ln.split()[0]
+        m = re.match(r"s_waitcnt.*vmcnt\((\d+)\)", ln)
+        if m:
+            del queue[: max(0, len(queue) - int(m.group(1)))]
+            continue
+        if op == "s_barrier":
+            bad += [(i, q) for q in queue if q is not None and q < barriers]
+            barriers += 1
+        elif op.startswith(("global_load", "buffer_load")):
+            queue.append(barriers if "lds" in op else None)
+        elif op.startswith(("global_store", "buffer_store", "global_atomic")):
+            queue.append(None)
+    return bad
+
+
+def test_lds_checker_finds_the_pattern():
+    asm = ["\tglobal_load_lds_dwordx4 v[6:7], off",
+           "\ts_barrier",
+           ".LBB0_1:  ; Inner Loop Header",
+           "\tv_add_u32_e32 v1, v2, v3",
+           "\ts_cbranch_scc1 .LBB0_1",
+           "\ts_barrier"]
+    assert len(lds_copy_violations(asm, 2, 4)) == 1
+    fixed = asm[:5] + ["\ts_waitcnt vmcnt(0)"] + asm[5:]
+    assert lds_copy_violations(fixed, 2, 4) == []
+
+
+def test_fast_gemm_copies_are_drained_within_one_barrier_period(gemm_asm):
+    names = re.findall(r"^(_ZN3ifq12gemm_tn_fast\S+):", gemm_asm, re.M)
+    assert len(names) >= 6
+    for name in names:
+        start = gemm_asm.index(name + ":")
+        body = gemm_asm[start: gemm_asm.index(".Lfunc_end", start)].split("\n")
+        header = next(i for i, ln in enumerate(body) if "Inner Loop Header" in ln)
+        back = max(i for i, ln in enumerate(body)
+                   if ln.strip().startswith("s_cbranch_scc1") and i > header)
+        assert sum(1 for ln in body if "global_load_lds_dwordx4" in ln) >= 6, name
+        assert sum(1 for ln in body if ln.strip() == "s_barrier") >= 4, name
+        bad = lds_copy_violations(body, header, back)
+        assert bad == [], (name, bad[:3])
+
+
+def _fast_gemm_lds_events(nch):
+    """The copy and read schedule of the fast GEMM's raw-code and scale slots
+    for K = 128 nch (nch % 4 == 0), as the kernel issues it: a list of
+    (phase, kind, region, data) with phase the number of barriers passed
+    before the event, kind 'copy' or 'read', region (slot kind, slot, half)
+    and data the chunk it holds or needs (None: past the end, never used).
+    Even steps end with a vmcnt wait that drains every copy issued before
+    them: a copy issued in phase p (step p - 2) is drained before the barrier
+    that ends the first even step from then on, and the prologue's before
+    the first barrier."""
+    nsc = nch // 4
+    ev = []
+    # prologue: B chunks 0, 1; scale chunk 0 (A and B halves), scale chunk 1's A half
+    ev += [(0, "copy", ("raw", 0, 0), 0), (0, "copy", ("raw", 1, 0), min(1, nch - 1)),
+           (0, "copy", ("scl", 0, 0), 0), (0, "copy", ("scl", 0, 1), 0),
+           (0, "copy", ("scl", 1, 0), min(1, nsc - 1))]
+    # (vmcnt(0); barrier 1) reads of B steps 0, 1, 2 and the A scales of chunk 0
+    def read_b(phase, sd):
+        c = sd >> 1
+        ok = c < nch
+        return [(phase, "read", ("raw", c & 1, 0), c if ok else None),
+                (phase, "read", ("scl", (c >> 2) & 1, 1), (c >> 2) if ok else None)]
+    for sd in (0, 1, 2):
+        ev += read_b(1, sd)
+    ev.append((1, "read", ("scl", 0, 0), 0))
+    # (barrier 2) the odd step before step 0: B chunk 2 into raw slot 0
+    ev.append((2, "copy", ("raw", 0, 0), min(2, nch - 1)))
+    for s in range(2 * nch):
+        phase = 2 + s            # barriers passed before step s
+        q, c = s % 4, s >> 1
+        j, cs = q & 1, q >> 1
+        if j == 1:
+            ev.append((phase, "copy", ("raw", cs ^ 1, 0), min(c + 3, nch - 1)))
+            if q == 1:
+                u = s >> 2
+                e = (u + 3) >> 1
+                ev.append((phase, "copy", ("scl", e & 1, (u + 1) & 1), min(e, nsc - 1)))
+        else:
+            ca = min(c + 1, nch - 1)
+            ev.append((phase, "read", ("scl", (ca >> 2) & 1, 0), ca >> 2))
+        ev += read_b(phase, s + 3)
+    return ev
+
+
+def _check_lds_schedule(ev):
+    """Every read sees its chunk, copied and drained at least one barrier
+    earlier, and no copy of other data into that slot is issued before the
+    read's barrier.  (Past the last chunk the kernel clamps its copy indices,
+    so a slot can be rewritten with the bytes it already holds; such a copy
+    changes nothing a read can see.)"""
+    problems = []
+    for idx, (ph, kind, reg, data) in enumerate(ev):
+        if kind != "read" or data is None:
+            continue
+        copies = [(p, d) for (p, k, r, d) in ev[:idx] if k == "copy" and r == reg]
+        if not copies:
+            problems.append(("never copied", ph, reg, data))
+            continue
+        if copies[-1][1] != data:
+            problems.append(("slot holds another chunk", ph, reg, data, copies[-1][1]))
+            continue
+        # the copy that brought this data in (identical rewrites after it change nothing)
+        k = len(copies) - 1
+        while k > 0 and copies[k - 1][1] == data:
+            k -= 1
+        p_last = copies[k][0]
+        # first phase in which the copy is drained and fenced
+        visible = 1 if p_last == 0 else (p_last + 1 if (p_last - 2) % 2 == 0 else p_last + 2)
+        if ph < visible:
+            problems.append(("read before the copy is drained and fenced", ph, reg, data, p_last))
+        same_phase = [p for (p, k, r, d) in ev[idx + 1:] if k == "copy" and r == reg and p <= ph and d != data]
+        if same_phase:
+            problems.append(("slot refilled before the read's barrier", ph, reg, data))
+    return problems
+
+
+def test_fast_gemm_lds_slot_schedule():
+    for nch in (4, 8, 12, 32):
+        assert _check_lds_schedule(_fast_gemm_lds_events(nch)) == [], nch
+
+
+def test_lds_schedule_checker_finds_a_slot_reused_too_early():
+    ev = _fast_gemm_lds_events(8)
+    # move the first main-loop copy into raw slot 1 one phase earlier
+    i = next(i for i, e in enumerate(ev) if e[1] == "copy" and e[2] == ("raw", 1, 0) and e[0] > 2)
+    p, k, r, d = ev[i]
+    bad = ev[:i] + [(p - 1, k, r, d)] + ev[i + 1:]
+    bad.sort(key=lambda e: e[0])
+    assert _check_lds_schedule(bad) != []
