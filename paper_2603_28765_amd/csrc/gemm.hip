@@ -243,6 +243,210 @@ __device__ __forceinline__ void decode_if6_group(const uint32_t* w, bool is_int,
     }
 }
 
+// ------------------------------------------------- single-conversion decode
+// Shared by the fast kernel and the general one for 4-bit codes.
+namespace dec {
+
+// Fold constants of the two groups whose scale bytes are the low and high
+// byte of sw, one half each: the operand is K x + C, x the converted code.
+//   IF4 FP group : K = 14 Delta, C = 0 (x = E2M1 value times 2^-6)
+//   IF4 INT group: K = 96 Delta, C = -1.5 Delta (x = (q + 8) 2^-9)
+//   NVFP4        : K = Delta, C = 0 (x = E2M1 value)
+//   NVINT4       : K = 128 Delta, C = -2 Delta (every group INT)
+// For IF4 the E4M3 conversion keeps the indicator bit as the sign (d = -Delta
+// for INT groups), so max(14 d, -96 d) and min(1.5 d, 0) select the
+// constants without masks; C != 0 marks an INT group (an INT group with
+// Delta = 0 decodes to zeros either way).
+struct KC {
+    half2v K, C;
+};
+
+template <int FMT>
+__device__ __forceinline__ KC pair_kc(uint32_t sw)
+{
+    KC r;
+    if constexpr (Fmt<FMT>::KIND == kKindInt) {
+        const half2v d = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw & 0x7F7Fu, 1.0f, false);
+        const half2v ki = {(_Float16)128.0f, (_Float16)128.0f}, cn = {(_Float16)-2.0f, (_Float16)-2.0f};
+        r.K = d * ki;
+        r.C = d * cn;
+    } else if constexpr (Fmt<FMT>::ADAPTIVE) {
+        const half2v d = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw, 1.0f, false);
+        constexpr float kf = Fold<FMT>::FP * 64.0f;
+        const half2v f = {(_Float16)kf, (_Float16)kf};
+        const half2v fi = {(_Float16)-96.0f, (_Float16)-96.0f};
+        const half2v c = {(_Float16)1.5f, (_Float16)1.5f};
+        const half2v z = {(_Float16)0.0f, (_Float16)0.0f};
+        r.K = __builtin_elementwise_max(d * f, d * fi);
+        r.C = __builtin_elementwise_min(d * c, z);
+    } else {
+        const half2v f = {(_Float16)Fold<FMT>::FP, (_Float16)Fold<FMT>::FP};
+        r.K = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw & 0x7F7Fu, 1.0f, false) * f;
+        r.C = half2v{(_Float16)0.0f, (_Float16)0.0f};
+    }
+    return r;
+}
+
+// Per-group selector of the IF4 byte mapping: M = all ones, P = 0 for an INT
+// group, M = 0, P = 2 for an FP group (unused by the other formats).  M is
+// the sign of the group's C (negative exactly for INT groups; a zero INT
+// scale gives C = -0 or +0, and K = 0 makes the group zero either way).
+struct TypeSel {
+    uint32_t M, P;
+};
+
+template <int FMT, int HS>
+__device__ __forceinline__ TypeSel type_sel(const KC& kc)
+{
+    if constexpr (Fmt<FMT>::ADAPTIVE) {
+        const int32_t cb = (int32_t)h2_as_u32(kc.C);
+        const uint32_t m = (uint32_t)(HS ? (cb >> 31) : ((cb << 16) >> 31));
+        return TypeSel{m, ~m & 2u};
+    } else {
+        return TypeSel{0u, 0u};
+    }
+}
+
+// IF4 codes as E4M3 bytes, one code per byte (d holds a code in the low
+// nibble of each byte).  FP group: the sign goes to bit 7 and the three
+// magnitude bits to bits 2..4, which is the E4M3 pattern of the E2M1 value
+// times 2^-6 (subnormal 0.5 included).  INT group: n ^ 8, the E4M3 pattern
+// of (q + 8) 2^-9.  Both types thus share one conversion per two codes.
+__device__ __forceinline__ uint32_t if4_bytes(uint32_t d, const TypeSel& ts)
+{
+    const uint32_t a = d & 0x07070707u;
+    const uint32_t sg = (d ^ ts.M) & 0x08080808u;
+    return ((sg << ts.P) | a) << ts.P;
+}
+
+// Empty asm statements that pin a stage's results to a program point: the
+// slice schedule below places each decode stage between two MFMAs, and
+// without them instruction selection would sink every stage to the last
+// use of its results.
+template <bool ON> __device__ __forceinline__ void pin(uint32_t& a)
+{
+    if constexpr (ON) asm volatile("" : "+v"(a));
+}
+template <bool ON> __device__ __forceinline__ void pin4(uint32_t (&a)[4])
+{
+    if constexpr (ON) asm volatile("" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]));
+}
+
+// Decode of one dword w of eight 4-bit codes (code 2i in the low nibble of
+// byte i) into four FP16 operand pairs, in four stages of a few VALU
+// operations each.  The E4M3 paths (IF4, NVINT4) convert the even codes
+// (low nibbles) and the odd codes (high nibbles) as two byte vectors, so the
+// pairs come out as (0, 2), (4, 6), (1, 3), (5, 7); NVFP4 converts nibble
+// pairs in place: (0, 1), (2, 3), (4, 5), (6, 7).  Both operands of a GEMM
+// are decoded alike, so either order is the same contraction over K.
+//   s1: even codes to bytes (IF4, NVINT4) or the E2M1 conversions (NVFP4)
+//   s2: odd codes to bytes
+//   s3: E4M3 conversions
+//   s4: K x + C
+struct WordDec {
+    uint32_t d0, d1;
+    uint32_t x[4];
+};
+
+template <int FMT, bool PIN>
+__device__ __forceinline__ void wd_s1(uint32_t w, const TypeSel& ts, WordDec& s)
+{
+    if constexpr (Fmt<FMT>::KIND == kKindInt) {
+        s.d0 = (w & 0x0F0F0F0Fu) ^ 0x08080808u;
+        pin<PIN>(s.d0);
+    } else if constexpr (Fmt<FMT>::ADAPTIVE) {
+        s.d0 = if4_bytes(w, ts);
+        pin<PIN>(s.d0);
+    } else {
+        s.x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 0));
+        s.x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 1));
+        s.x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 2));
+        s.x[3] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 3));
+        pin4<PIN>(s.x);
+    }
+}
+
+template <int FMT, bool PIN>
+__device__ __forceinline__ void wd_s2(uint32_t w, const TypeSel& ts, WordDec& s)
+{
+    if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
+        const uint32_t w4 = w >> 4;
+        if constexpr (Fmt<FMT>::KIND == kKindInt) s.d1 = (w4 & 0x0F0F0F0Fu) ^ 0x08080808u;
+        else s.d1 = if4_bytes(w4, ts);
+        pin<PIN>(s.d1);
+    }
+}
+
+template <int FMT, bool PIN>
+__device__ __forceinline__ void wd_s3(WordDec& s)
+{
+    if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
+        s.x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d0, 1.0f, false));
+        s.x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d0, 1.0f, true));
+        s.x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d1, 1.0f, false));
+        s.x[3] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d1, 1.0f, true));
+        pin4<PIN>(s.x);
+    }
+}
+
+template <int FMT, int HS, bool PIN>
+__device__ __forceinline__ void wd_s4(const WordDec& s, const KC& kc, uint32_t (&out)[4])
+{
+    const half2v K2 = {kc.K[HS], kc.K[HS]};
+    const half2v C2 = {kc.C[HS], kc.C[HS]};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[i] = h2_as_u32(__builtin_elementwise_fma(u32_as_h2(s.x[i]), K2, C2));
+    pin4<PIN>(out);
+}
+
+// Two words w[0], w[1] of a block-size-8 unit: word 0 with the constants of
+// half 0 of kc, word 1 with half 1.
+template <int FMT>
+__device__ __forceinline__ void decode_words_kc2(const uint32_t* w, const KC& kc, uint32_t (&out)[8])
+{
+    const TypeSel t0 = type_sel<FMT, 0>(kc), t1 = type_sel<FMT, 1>(kc);
+    WordDec a, b;
+    uint32_t o0[4], o1[4];
+    wd_s1<FMT, false>(w[0], t0, a);
+    wd_s2<FMT, false>(w[0], t0, a);
+    wd_s3<FMT, false>(a);
+    wd_s4<FMT, 0, false>(a, kc, o0);
+    wd_s1<FMT, false>(w[1], t1, b);
+    wd_s2<FMT, false>(w[1], t1, b);
+    wd_s3<FMT, false>(b);
+    wd_s4<FMT, 1, false>(b, kc, o1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        out[i] = o0[i];
+        out[4 + i] = o1[i];
+    }
+}
+
+// One group (two dwords w[0], w[1]) with the constants of half HS of kc,
+// all stages in a row.
+template <int FMT, int HS>
+__device__ __forceinline__ void decode_group_kc(const uint32_t* w, const KC& kc, uint32_t (&out)[8])
+{
+    const TypeSel ts = type_sel<FMT, HS>(kc);
+    WordDec a, b;
+    uint32_t o0[4], o1[4];
+    wd_s1<FMT, false>(w[0], ts, a);
+    wd_s2<FMT, false>(w[0], ts, a);
+    wd_s3<FMT, false>(a);
+    wd_s4<FMT, HS, false>(a, kc, o0);
+    wd_s1<FMT, false>(w[1], ts, b);
+    wd_s2<FMT, false>(w[1], ts, b);
+    wd_s3<FMT, false>(b);
+    wd_s4<FMT, HS, false>(b, kc, o1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        out[i] = o0[i];
+        out[4 + i] = o1[i];
+    }
+}
+
+}  // namespace dec
+
 // ------------------------------------------------------------ raw chunks
 // A: one lane's 32 k-values of one row for one step (2 groups);
 // B: one thread's 64 k-values of one row (4 groups).  IF3 keeps 6-byte groups.
@@ -384,23 +588,30 @@ template <int FMT>
 __device__ __forceinline__ void decode_group(const uint32_t* w, const uint16_t* h, ScaleBits<FMT> sb, int g,
                                              uint32_t (&out)[8])
 {
-    if constexpr (Fmt<FMT>::G == 8) {
+    if constexpr (Fmt<FMT>::BITS == 4) {
+        // 4-bit codes: one conversion per two codes for both group types
+        // (dec::); with block size 8 the two scale bytes of these 16 values
+        // hold the constants of codes 0-7 (low byte, word 0) and 8-15 (high
+        // byte, word 1), with block size 16 the pair of groups g & ~1, g | 1
+        if constexpr (Fmt<FMT>::G == 8) {
+            const dec::KC kc = dec::pair_kc<FMT>((uint32_t)(sb >> (16 * g)) & 0xFFFFu);
+            dec::decode_words_kc2<FMT>(w + 2 * g, kc, out);
+        } else {
+            const dec::KC kc = dec::pair_kc<FMT>((uint32_t)(sb >> (16 * (g >> 1))) & 0xFFFFu);
+            if (g & 1)
+                dec::decode_group_kc<FMT, 1>(w + 2 * g, kc, out);
+            else
+                dec::decode_group_kc<FMT, 0>(w + 2 * g, kc, out);
+        }
+        return;
+    } else if constexpr (Fmt<FMT>::G == 8) {
         // block size 8: the two scale bytes of these 16 values hold the
         // constants of codes 0-7 (low byte) and 8-15 (high byte)
         const uint32_t sw = (uint32_t)(sb >> (16 * g)) & 0xFFFFu;
         uint32_t K, Cb;
         pair_scales<FMT>(sw, K, Cb);
         const bool i0 = Fmt<FMT>::ADAPTIVE && ((sw >> 7) & 1u), i1 = Fmt<FMT>::ADAPTIVE && ((sw >> 15) & 1u);
-        if constexpr (Fmt<FMT>::BITS == 4) {
-            uint32_t o0[4], o1[4];
-            decode_word<FMT>(w[2 * g], i0, bcast_lo(K), bcast_lo(Cb), o0);
-            decode_word<FMT>(w[2 * g + 1], i1, bcast_hi(K), bcast_hi(Cb), o1);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                out[i] = o0[i];
-                out[4 + i] = o1[i];
-            }
-        } else {
+        {
             const uint64_t bitsv = (uint64_t)h[3 * g] | ((uint64_t)h[3 * g + 1] << 16) |
                                    ((uint64_t)h[3 * g + 2] << 32);
             decode_if3_group(bitsv, i0, bcast_lo(K), i1, bcast_hi(K), out);
@@ -700,6 +911,8 @@ __device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, i
 // 64 banks at a time.
 namespace fast {
 
+using namespace dec;
+
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kStageBytes = kBN * kBK * 2;       // decoded B stage, 32 KiB
 constexpr int kRawBytes = kBN * 64;              // B codes of one chunk, 16 KiB
@@ -752,181 +965,6 @@ __device__ __forceinline__ void vm_drain(u32x4 (&a)[2][2][2])
                    "+v"(a[1][0][0]), "+v"(a[1][0][1]), "+v"(a[1][1][0]), "+v"(a[1][1][1])
                  :
                  : "memory");
-}
-
-// Fold constants of the two groups whose scale bytes are the low and high
-// byte of sw, one half each: the operand is K x + C, x the converted code.
-//   IF4 FP group : K = 14 Delta, C = 0 (x = E2M1 value times 2^-6)
-//   IF4 INT group: K = 96 Delta, C = -1.5 Delta (x = (q + 8) 2^-9)
-//   NVFP4        : K = Delta, C = 0 (x = E2M1 value)
-//   NVINT4       : K = 128 Delta, C = -2 Delta (every group INT)
-// For IF4 the E4M3 conversion keeps the indicator bit as the sign (d = -Delta
-// for INT groups), so max(14 d, -96 d) and min(1.5 d, 0) select the
-// constants without masks; C != 0 marks an INT group (an INT group with
-// Delta = 0 decodes to zeros either way).
-struct KC {
-    half2v K, C;
-};
-
-template <int FMT>
-__device__ __forceinline__ KC pair_kc(uint32_t sw)
-{
-    KC r;
-    if constexpr (Fmt<FMT>::KIND == kKindInt) {
-        const half2v d = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw & 0x7F7Fu, 1.0f, false);
-        const half2v ki = {(_Float16)128.0f, (_Float16)128.0f}, cn = {(_Float16)-2.0f, (_Float16)-2.0f};
-        r.K = d * ki;
-        r.C = d * cn;
-    } else if constexpr (Fmt<FMT>::ADAPTIVE) {
-        const half2v d = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw, 1.0f, false);
-        constexpr float kf = Fold<FMT>::FP * 64.0f;
-        const half2v f = {(_Float16)kf, (_Float16)kf};
-        const half2v fi = {(_Float16)-96.0f, (_Float16)-96.0f};
-        const half2v c = {(_Float16)1.5f, (_Float16)1.5f};
-        const half2v z = {(_Float16)0.0f, (_Float16)0.0f};
-        r.K = __builtin_elementwise_max(d * f, d * fi);
-        r.C = __builtin_elementwise_min(d * c, z);
-    } else {
-        const half2v f = {(_Float16)Fold<FMT>::FP, (_Float16)Fold<FMT>::FP};
-        r.K = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw & 0x7F7Fu, 1.0f, false) * f;
-        r.C = half2v{(_Float16)0.0f, (_Float16)0.0f};
-    }
-    return r;
-}
-
-// Per-group selector of the IF4 byte mapping: M = all ones, P = 0 for an INT
-// group, M = 0, P = 2 for an FP group (unused by the other formats).  M is
-// the sign of the group's C (negative exactly for INT groups; a zero INT
-// scale gives C = -0 or +0, and K = 0 makes the group zero either way).
-struct TypeSel {
-    uint32_t M, P;
-};
-
-template <int FMT, int HS>
-__device__ __forceinline__ TypeSel type_sel(const KC& kc)
-{
-    if constexpr (Fmt<FMT>::ADAPTIVE) {
-        const int32_t cb = (int32_t)h2_as_u32(kc.C);
-        const uint32_t m = (uint32_t)(HS ? (cb >> 31) : ((cb << 16) >> 31));
-        return TypeSel{m, ~m & 2u};
-    } else {
-        return TypeSel{0u, 0u};
-    }
-}
-
-// IF4 codes as E4M3 bytes, one code per byte (d holds a code in the low
-// nibble of each byte).  FP group: the sign goes to bit 7 and the three
-// magnitude bits to bits 2..4, which is the E4M3 pattern of the E2M1 value
-// times 2^-6 (subnormal 0.5 included).  INT group: n ^ 8, the E4M3 pattern
-// of (q + 8) 2^-9.  Both types thus share one conversion per two codes.
-__device__ __forceinline__ uint32_t if4_bytes(uint32_t d, const TypeSel& ts)
-{
-    const uint32_t a = d & 0x07070707u;
-    const uint32_t sg = (d ^ ts.M) & 0x08080808u;
-    return ((sg << ts.P) | a) << ts.P;
-}
-
-// Empty asm statements that pin a stage's results to a program point: the
-// slice schedule below places each decode stage between two MFMAs, and
-// without them instruction selection would sink every stage to the last
-// use of its results.
-template <bool ON> __device__ __forceinline__ void pin(uint32_t& a)
-{
-    if constexpr (ON) asm volatile("" : "+v"(a));
-}
-template <bool ON> __device__ __forceinline__ void pin4(uint32_t (&a)[4])
-{
-    if constexpr (ON) asm volatile("" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]));
-}
-
-// Decode of one dword w of eight 4-bit codes (code 2i in the low nibble of
-// byte i) into four FP16 operand pairs, in four stages of a few VALU
-// operations each.  The E4M3 paths (IF4, NVINT4) convert the even codes
-// (low nibbles) and the odd codes (high nibbles) as two byte vectors, so the
-// pairs come out as (0, 2), (4, 6), (1, 3), (5, 7); NVFP4 converts nibble
-// pairs in place: (0, 1), (2, 3), (4, 5), (6, 7).  Both operands of a GEMM
-// are decoded alike, so either order is the same contraction over K.
-//   s1: even codes to bytes (IF4, NVINT4) or the E2M1 conversions (NVFP4)
-//   s2: odd codes to bytes
-//   s3: E4M3 conversions
-//   s4: K x + C
-struct WordDec {
-    uint32_t d0, d1;
-    uint32_t x[4];
-};
-
-template <int FMT, bool PIN>
-__device__ __forceinline__ void wd_s1(uint32_t w, const TypeSel& ts, WordDec& s)
-{
-    if constexpr (Fmt<FMT>::KIND == kKindInt) {
-        s.d0 = (w & 0x0F0F0F0Fu) ^ 0x08080808u;
-        pin<PIN>(s.d0);
-    } else if constexpr (Fmt<FMT>::ADAPTIVE) {
-        s.d0 = if4_bytes(w, ts);
-        pin<PIN>(s.d0);
-    } else {
-        s.x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 0));
-        s.x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 1));
-        s.x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 2));
-        s.x[3] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 1.0f, 3));
-        pin4<PIN>(s.x);
-    }
-}
-
-template <int FMT, bool PIN>
-__device__ __forceinline__ void wd_s2(uint32_t w, const TypeSel& ts, WordDec& s)
-{
-    if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
-        const uint32_t w4 = w >> 4;
-        if constexpr (Fmt<FMT>::KIND == kKindInt) s.d1 = (w4 & 0x0F0F0F0Fu) ^ 0x08080808u;
-        else s.d1 = if4_bytes(w4, ts);
-        pin<PIN>(s.d1);
-    }
-}
-
-template <int FMT, bool PIN>
-__device__ __forceinline__ void wd_s3(WordDec& s)
-{
-    if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
-        s.x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d0, 1.0f, false));
-        s.x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d0, 1.0f, true));
-        s.x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d1, 1.0f, false));
-        s.x[3] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d1, 1.0f, true));
-        pin4<PIN>(s.x);
-    }
-}
-
-template <int FMT, int HS, bool PIN>
-__device__ __forceinline__ void wd_s4(const WordDec& s, const KC& kc, uint32_t (&out)[4])
-{
-    const half2v K2 = {kc.K[HS], kc.K[HS]};
-    const half2v C2 = {kc.C[HS], kc.C[HS]};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) out[i] = h2_as_u32(__builtin_elementwise_fma(u32_as_h2(s.x[i]), K2, C2));
-    pin4<PIN>(out);
-}
-
-// One group (two dwords w[0], w[1]) with the constants of half HS of kc,
-// all stages in a row.
-template <int FMT, int HS>
-__device__ __forceinline__ void decode_group_kc(const uint32_t* w, const KC& kc, uint32_t (&out)[8])
-{
-    const TypeSel ts = type_sel<FMT, HS>(kc);
-    WordDec a, b;
-    uint32_t o0[4], o1[4];
-    wd_s1<FMT, false>(w[0], ts, a);
-    wd_s2<FMT, false>(w[0], ts, a);
-    wd_s3<FMT, false>(a);
-    wd_s4<FMT, HS, false>(a, kc, o0);
-    wd_s1<FMT, false>(w[1], ts, b);
-    wd_s2<FMT, false>(w[1], ts, b);
-    wd_s3<FMT, false>(b);
-    wd_s4<FMT, HS, false>(b, kc, o1);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        out[i] = o0[i];
-        out[4 + i] = o1[i];
-    }
 }
 
 struct Ctx {
