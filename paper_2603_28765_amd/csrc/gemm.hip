@@ -973,23 +973,28 @@ struct Ctx {
     const uint8_t* b_codes;
     const uint8_t* b_scales;
     int64_t rowb;    // bytes per code row (K / 2)
-    int64_t gpr;     // groups (scale bytes) per row
+    int64_t gpr;     // scale bytes per row (K / 16, or K / 8 for block size 8)
     int nch;         // 2-step chunks
-    int nsc;         // 8-step scale chunks
+    int nsc;         // scale chunks (8 steps, or 4 for block size 8: 32 bytes per row either way)
     int64_t m0, n0;
     uint8_t* dec;    // 3 decoded stages
     uint8_t* raw;    // 2 raw B slots
     uint8_t* scl;    // 2 scale slots
 };
 
-struct State {
-    u32x4 a[2][2][2];   // A codes [chunk slot][row block][16-byte half]
-    uint32_t as[2][2];  // A scale bytes [chunk slot][row block] (4 groups)
-    uint32_t bw[8];     // B codes of the next decode (4 groups, decode order)
-    uint32_t bs;        // their scale bytes
-    KC akc[2];          // A fold constants of the pair in use [row block]
-    half8 af[2][2][2];  // A fragments [group gg][row block][slice parity]
-    half8 bf[2][8];     // B fragments, double buffered over slices
+// SPG: scale bytes per 16 values (1, or 2 for block size 8).
+template <int FMT> constexpr int kSpg = Fmt<FMT>::G == 8 ? 2 : 1;
+template <int SPG> using SclWord = typename std::conditional<SPG == 2, uint64_t, uint32_t>::type;
+
+template <int SPG> struct StateT {
+    u32x4 a[2][2][2];        // A codes [chunk slot][row block][16-byte half]
+    SclWord<SPG> as[2][2];   // A scale bytes [chunk slot][row block] (4 groups)
+    uint32_t bw[8];          // B codes of the next decode (4 groups, decode order)
+    SclWord<SPG> bs;         // their scale bytes
+    KC akc[2];               // A fold constants [row block]: of the pair in use, or
+                             // (block size 8) of the second group of the step
+    half8 af[2][2][2];       // A fragments [group gg][row block][slice parity]
+    half8 bf[2][8];          // B fragments, double buffered over slices
 };
 
 // B codes of chunk cc (rows n0 .. n0 + 255, 64 bytes each) into raw slot:
@@ -1035,18 +1040,28 @@ __device__ __forceinline__ void load_a_chunk(const Ctx& x, int64_t arow0, int h,
     }
 }
 
-// Scale bytes of A chunk c for this lane (4 groups per row block).
-__device__ __forceinline__ void read_a_scales(const Ctx& x, int c, int arow_local, int h, uint32_t (&as)[2])
+// Scale bytes of A chunk c for this lane (4 groups per row block; two
+// bytes per group with block size 8, whose scale chunks hold 2 code chunks).
+template <int SPG>
+__device__ __forceinline__ void read_a_scales(const Ctx& x, int c, int arow_local, int h, SclWord<SPG> (&as)[2])
 {
-    const uint8_t* sl = x.scl + ((c >> 2) & 1) * kSclBytes;
+    if constexpr (SPG == 1) {
+        const uint8_t* sl = x.scl + ((c >> 2) & 1) * kSclBytes;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-        as[i] = *reinterpret_cast<const uint32_t*>(sl + (arow_local + 32 * i) * 32 + 8 * (c & 3) + 4 * h);
+        for (int i = 0; i < 2; ++i)
+            as[i] = *reinterpret_cast<const uint32_t*>(sl + (arow_local + 32 * i) * 32 + 8 * (c & 3) + 4 * h);
+    } else {
+        const uint8_t* sl = x.scl + ((c >> 1) & 1) * kSclBytes;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+            as[i] = *reinterpret_cast<const uint64_t*>(sl + (arow_local + 32 * i) * 32 + 16 * (c & 1) + 8 * h);
+    }
 }
 
 // B codes and scale bytes that step s decodes (B of step s + 2) -- chunk
 // (s + 2) / 2, step j = s % 2 of it -- for row t.
-__device__ __forceinline__ void read_b_raw(const Ctx& x, int sd, State& st)
+template <int SPG>
+__device__ __forceinline__ void read_b_raw(const Ctx& x, int sd, StateT<SPG>& st)
 {
     const int t = threadIdx.x;
     const int c = sd >> 1, j = sd & 1;
@@ -1056,19 +1071,29 @@ __device__ __forceinline__ void read_b_raw(const Ctx& x, int sd, State& st)
     const u32x4 hi = *reinterpret_cast<const u32x4*>(rs + 16 * ((2 + j) ^ sw));
     st.bw[0] = lo.x; st.bw[1] = lo.y; st.bw[2] = lo.z; st.bw[3] = lo.w;
     st.bw[4] = hi.x; st.bw[5] = hi.y; st.bw[6] = hi.z; st.bw[7] = hi.w;
-    const uint2 v = *reinterpret_cast<const uint2*>(x.scl + ((c >> 2) & 1) * kSclBytes + kSclB + t * 32 + 8 * (c & 3));
-    st.bs = __builtin_amdgcn_perm(v.y, v.x, j ? 0x07060302u : 0x05040100u);
+    if constexpr (SPG == 1) {
+        const uint2 v = *reinterpret_cast<const uint2*>(x.scl + ((c >> 2) & 1) * kSclBytes + kSclB + t * 32 + 8 * (c & 3));
+        st.bs = __builtin_amdgcn_perm(v.y, v.x, j ? 0x07060302u : 0x05040100u);
+    } else {
+        // 16 bytes of chunk c: groups 2j, 2j + 1 at bytes 4j .. 4j + 3 and
+        // groups 4 + 2j, 5 + 2j at bytes 8 + 4j .. 8 + 4j + 3
+        const u32x4 v = *reinterpret_cast<const u32x4*>(x.scl + ((c >> 1) & 1) * kSclBytes + kSclB + t * 32 + 16 * (c & 1));
+        st.bs = j ? ((uint64_t)v.y | ((uint64_t)v.w << 32)) : ((uint64_t)v.x | ((uint64_t)v.z << 32));
+    }
 }
 
 // Decode B group G (0..3, decode order) of row t into stage `stg`: halves
 // 16 G .. 16 G + 15, i.e. pieces 2 G and 2 G + 1 (swizzled); kc holds the
 // constants of groups 2 (G / 2) and 2 (G / 2) + 1.
 template <int FMT, int G>
-__device__ __forceinline__ void decode_b_fast(const State& st, const KC& kc, uint8_t* stg)
+__device__ __forceinline__ void decode_b_fast(const StateT<kSpg<FMT>>& st, const KC& kc, uint8_t* stg)
 {
     const int t = threadIdx.x;
     uint32_t v[8];
-    decode_group_kc<FMT, G & 1>(st.bw + 2 * G, kc, v);
+    if constexpr (kSpg<FMT> == 2)
+        decode_words_kc2<FMT>(st.bw + 2 * G, kc, v);
+    else
+        decode_group_kc<FMT, G & 1>(st.bw + 2 * G, kc, v);
     const int sw = swz8(t);
     uint8_t* row = stg + t * 128;
     *reinterpret_cast<u32x4*>(row + 16 * ((2 * G) ^ sw)) = u32x4{v[0], v[1], v[2], v[3]};
@@ -1076,13 +1101,20 @@ __device__ __forceinline__ void decode_b_fast(const State& st, const KC& kc, uin
 }
 
 template <int FMT>
-__device__ __forceinline__ void decode_b_all(const State& st, uint8_t* stg)
+__device__ __forceinline__ void decode_b_all(const StateT<kSpg<FMT>>& st, uint8_t* stg)
 {
-    const KC k0 = pair_kc<FMT>(st.bs & 0xFFFFu), k1 = pair_kc<FMT>(st.bs >> 16);
-    decode_b_fast<FMT, 0>(st, k0, stg);
-    decode_b_fast<FMT, 1>(st, k0, stg);
-    decode_b_fast<FMT, 2>(st, k1, stg);
-    decode_b_fast<FMT, 3>(st, k1, stg);
+    if constexpr (kSpg<FMT> == 2) {
+        decode_b_fast<FMT, 0>(st, pair_kc<FMT>((uint32_t)st.bs & 0xFFFFu), stg);
+        decode_b_fast<FMT, 1>(st, pair_kc<FMT>((uint32_t)(st.bs >> 16) & 0xFFFFu), stg);
+        decode_b_fast<FMT, 2>(st, pair_kc<FMT>((uint32_t)(st.bs >> 32) & 0xFFFFu), stg);
+        decode_b_fast<FMT, 3>(st, pair_kc<FMT>((uint32_t)(st.bs >> 48)), stg);
+    } else {
+        const KC k0 = pair_kc<FMT>(st.bs & 0xFFFFu), k1 = pair_kc<FMT>(st.bs >> 16);
+        decode_b_fast<FMT, 0>(st, k0, stg);
+        decode_b_fast<FMT, 1>(st, k0, stg);
+        decode_b_fast<FMT, 2>(st, k1, stg);
+        decode_b_fast<FMT, 3>(st, k1, stg);
+    }
 }
 
 // Decode local group G (0..3) of the lane's A chunk (one row block) with the
@@ -1093,7 +1125,10 @@ __device__ __forceinline__ void decode_a_fast(const u32x4 (&a)[2], const KC& kc,
     const uint32_t w[2] = {G < 2 ? a[0][2 * (G & 1)] : a[1][2 * (G & 1)],
                            G < 2 ? a[0][2 * (G & 1) + 1] : a[1][2 * (G & 1) + 1]};
     uint32_t v[8];
-    decode_group_kc<FMT, G & 1>(w, kc, v);
+    if constexpr (kSpg<FMT> == 2)
+        decode_words_kc2<FMT>(w, kc, v);   // kc: this group's two scale bytes
+    else
+        decode_group_kc<FMT, G & 1>(w, kc, v);
     f0 = __builtin_bit_cast(half8, u32x4{v[0], v[1], v[2], v[3]});
     f1 = __builtin_bit_cast(half8, u32x4{v[4], v[5], v[6], v[7]});
 }
@@ -1128,10 +1163,11 @@ __device__ __forceinline__ void read_bfrag2(const uint8_t* stg, int kk, int lane
 //                first group at kk = 2, 3)
 // Every MFMA operand was produced at least one slice earlier.
 template <int FMT, int Q>
-__device__ __forceinline__ void step(const Ctx& x, State& st, int s, int64_t arow0, int arow_local,
+__device__ __forceinline__ void step(const Ctx& x, StateT<kSpg<FMT>>& st, int s, int64_t arow0, int arow_local,
                                      uint8_t* Bs, uint8_t* Bn, uint8_t* Bd, floatx16 (&acc)[2][8])
 {
     constexpr int j = Q & 1, CS = Q >> 1;
+    constexpr int SPG = kSpg<FMT>;
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int h = lane >> 5;
@@ -1139,14 +1175,18 @@ __device__ __forceinline__ void step(const Ctx& x, State& st, int s, int64_t aro
     const int swb = swz8(t);
     if constexpr (j == 1) {
         copy_b_chunk(x, min(c + 3, x.nch - 1), x.raw + (CS ^ 1) * kRawBytes);
-        if constexpr (Q == 1) {
+        if constexpr (SPG == 1 && Q == 1) {
             // scale chunk e = (u + 3) / 2, half (u + 1) % 2, for u = s / 4
             const int u = s >> 2;
             const int e = (u + 3) >> 1;
             copy_scales(x, min(e, x.nsc - 1), (u + 1) & 1, x.scl + (e & 1) * kSclBytes);
+        } else if constexpr (SPG == 2) {
+            // 4-step scale chunks: e = u + 2, its A half at Q = 1, its B half at Q = 3
+            const int e = (s >> 2) + 2;
+            copy_scales(x, min(e, x.nsc - 1), Q >> 1, x.scl + (e & 1) * kSclBytes);
         }
     } else {
-        read_a_scales(x, min(c + 1, x.nch - 1), arow_local, h, st.as[CS ^ 1]);
+        read_a_scales<SPG>(x, min(c + 1, x.nch - 1), arow_local, h, st.as[CS ^ 1]);
     }
     __builtin_amdgcn_sched_barrier(0);
     KC bkc;
@@ -1162,9 +1202,16 @@ __device__ __forceinline__ void step(const Ctx& x, State& st, int s, int64_t aro
 #define IFQ_SLOT_END() __builtin_amdgcn_sched_barrier(0)
         IFQ_MFMA(0);
         read_bfrag2(nstg, nkk, lane, st.bf[f ^ 1], 0);
-        if (kk == 0) bkc = pair_kc<FMT>(st.bs & 0xFFFFu);
-        if (kk == 2) bkc = pair_kc<FMT>(st.bs >> 16);
-        const TypeSel bts = (kk & 1) ? type_sel<FMT, 1>(bkc) : type_sel<FMT, 0>(bkc);
+        if constexpr (SPG == 1) {
+            if (kk == 0) bkc = pair_kc<FMT>(st.bs & 0xFFFFu);
+            if (kk == 2) bkc = pair_kc<FMT>(st.bs >> 16);
+        } else {
+            bkc = pair_kc<FMT>((uint32_t)(st.bs >> (16 * kk)) & 0xFFFFu);   // group kk's two bytes
+        }
+        // word 0 and word 1 of the group: the same half of bkc, or (block size
+        // 8) halves 0 and 1
+        const TypeSel bts = (SPG == 1 && (kk & 1)) ? type_sel<FMT, 1>(bkc) : type_sel<FMT, 0>(bkc);
+        const TypeSel bts1 = (SPG == 1 && !(kk & 1)) ? type_sel<FMT, 0>(bkc) : type_sel<FMT, 1>(bkc);
         IFQ_SLOT_END();
         IFQ_MFMA(1);
         read_bfrag2(nstg, nkk, lane, st.bf[f ^ 1], 2);
@@ -1180,19 +1227,19 @@ __device__ __forceinline__ void step(const Ctx& x, State& st, int s, int64_t aro
         IFQ_SLOT_END();
         IFQ_MFMA(4);
         uint32_t v0[4], v1[4];
-        if (kk & 1) wd_s4<FMT, 1, true>(b0, bkc, v0); else wd_s4<FMT, 0, true>(b0, bkc, v0);
+        if (SPG == 1 && (kk & 1)) wd_s4<FMT, 1, true>(b0, bkc, v0); else wd_s4<FMT, 0, true>(b0, bkc, v0);
         IFQ_SLOT_END();
         IFQ_MFMA(5);
-        wd_s1<FMT, true>(st.bw[2 * kk + 1], bts, b1);
+        wd_s1<FMT, true>(st.bw[2 * kk + 1], bts1, b1);
         IFQ_SLOT_END();
         IFQ_MFMA(6);
-        wd_s2<FMT, true>(st.bw[2 * kk + 1], bts, b1);
+        wd_s2<FMT, true>(st.bw[2 * kk + 1], bts1, b1);
         IFQ_SLOT_END();
         IFQ_MFMA(7);
         wd_s3<FMT, true>(b1);
         IFQ_SLOT_END();
         IFQ_MFMA(8);
-        if (kk & 1) wd_s4<FMT, 1, true>(b1, bkc, v1); else wd_s4<FMT, 0, true>(b1, bkc, v1);
+        if (SPG == 2 || (kk & 1)) wd_s4<FMT, 1, true>(b1, bkc, v1); else wd_s4<FMT, 0, true>(b1, bkc, v1);
         {
             // B group kk of row t: pieces 2 kk and 2 kk + 1 of the stage row
             uint8_t* row = Bd + t * 128;
@@ -1207,6 +1254,9 @@ __device__ __forceinline__ void step(const Ctx& x, State& st, int s, int64_t aro
         // chunk c + 1 (j = 1, loaded two steps ago; then slot CS, whose last
         // group was decoded at kk = 1, is refilled) or local group 2 of chunk
         // c (j = 0)
+        // (block size 8: the constants of each group come from its own two
+        // scale bytes -- the first group's here, the second's kept for the
+        // next step -- word 0 with half 0, word 1 with half 1)
         uint32_t aw0, aw1;
         KC akc;
         if (kk < 2) {
@@ -1216,21 +1266,32 @@ __device__ __forceinline__ void step(const Ctx& x, State& st, int s, int64_t aro
         } else {
             if constexpr (j == 1) {
                 if (kk == 2) {
-                    vm_wait<Q == 1 ? 6 : 4>(st.a[CS ^ 1][0][0], st.a[CS ^ 1][0][1], st.a[CS ^ 1][1][0],
-                                            st.a[CS ^ 1][1][1]);
+                    vm_wait<(SPG == 2 || Q == 1) ? 6 : 4>(st.a[CS ^ 1][0][0], st.a[CS ^ 1][0][1],
+                                                           st.a[CS ^ 1][1][0], st.a[CS ^ 1][1][1]);
                     load_a_chunk(x, arow0, h, min(c + 2, x.nch - 1), st.a[CS]);
                 }
-                st.akc[kk - 2] = pair_kc<FMT>(st.as[CS ^ 1][kk - 2] & 0xFFFFu);
+                if constexpr (SPG == 1) {
+                    st.akc[kk - 2] = pair_kc<FMT>(st.as[CS ^ 1][kk - 2] & 0xFFFFu);
+                } else {
+                    akc = pair_kc<FMT>((uint32_t)st.as[CS ^ 1][kk - 2] & 0xFFFFu);
+                    st.akc[kk - 2] = pair_kc<FMT>((uint32_t)(st.as[CS ^ 1][kk - 2] >> 16) & 0xFFFFu);
+                }
                 aw0 = st.a[CS ^ 1][kk - 2][0][0];
                 aw1 = st.a[CS ^ 1][kk - 2][0][1];
             } else {
-                st.akc[kk - 2] = pair_kc<FMT>(st.as[CS][kk - 2] >> 16);
+                if constexpr (SPG == 1) {
+                    st.akc[kk - 2] = pair_kc<FMT>(st.as[CS][kk - 2] >> 16);
+                } else {
+                    akc = pair_kc<FMT>((uint32_t)(st.as[CS][kk - 2] >> 32) & 0xFFFFu);
+                    st.akc[kk - 2] = pair_kc<FMT>((uint32_t)(st.as[CS][kk - 2] >> 48));
+                }
                 aw0 = st.a[CS][kk - 2][1][0];
                 aw1 = st.a[CS][kk - 2][1][1];
             }
-            akc = st.akc[kk - 2];
+            if constexpr (SPG == 1) akc = st.akc[kk - 2];
         }
-        const TypeSel ats = (kk < 2) ? type_sel<FMT, 1>(akc) : type_sel<FMT, 0>(akc);
+        const TypeSel ats = (SPG == 1 && kk < 2) ? type_sel<FMT, 1>(akc) : type_sel<FMT, 0>(akc);
+        const TypeSel ats1 = (SPG == 1 && kk >= 2) ? type_sel<FMT, 0>(akc) : type_sel<FMT, 1>(akc);
         wd_s1<FMT, true>(aw0, ats, a0);
         IFQ_SLOT_END();
         IFQ_MFMA(10);
@@ -1241,24 +1302,24 @@ __device__ __forceinline__ void step(const Ctx& x, State& st, int s, int64_t aro
         IFQ_SLOT_END();
         IFQ_MFMA(12);
         uint32_t o0[4], o1[4];
-        if (kk < 2) wd_s4<FMT, 1, true>(a0, akc, o0); else wd_s4<FMT, 0, true>(a0, akc, o0);
-        wd_s1<FMT, true>(aw1, ats, a1);
+        if (SPG == 1 && kk < 2) wd_s4<FMT, 1, true>(a0, akc, o0); else wd_s4<FMT, 0, true>(a0, akc, o0);
+        wd_s1<FMT, true>(aw1, ats1, a1);
         IFQ_SLOT_END();
         IFQ_MFMA(13);
-        wd_s2<FMT, true>(aw1, ats, a1);
+        wd_s2<FMT, true>(aw1, ats1, a1);
         IFQ_SLOT_END();
         IFQ_MFMA(14);
         wd_s3<FMT, true>(a1);
         IFQ_SLOT_END();
         IFQ_MFMA(15);
-        if (kk < 2) wd_s4<FMT, 1, true>(a1, akc, o1); else wd_s4<FMT, 0, true>(a1, akc, o1);
+        if (SPG == 2 || kk < 2) wd_s4<FMT, 1, true>(a1, akc, o1); else wd_s4<FMT, 0, true>(a1, akc, o1);
         {
             const half8 f0 = __builtin_bit_cast(half8, u32x4{o0[0], o0[1], o0[2], o0[3]});
             const half8 f1 = __builtin_bit_cast(half8, u32x4{o1[0], o1[1], o1[2], o1[3]});
             st.af[kk < 2 ? 1 : 0][kk & 1][0] = f0;
             st.af[kk < 2 ? 1 : 0][kk & 1][1] = f1;
         }
-        if (kk == 3) read_b_raw(x, s + 3, st);
+        if (kk == 3) read_b_raw<SPG>(x, s + 3, st);
         IFQ_SLOT_END();
 #undef IFQ_MFMA
 #undef IFQ_SLOT_END
@@ -1281,8 +1342,9 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
     const int h = lane >> 5;
     const int arow_local = 64 * wave + (lane & 31);
     const int64_t arow0 = m0 + arow_local;
-    Ctx x{a_codes, a_scales, b_codes, b_scales, K / 2, K / kGroup, (int)(K / 128), (int)(K / 512),
-          m0, n0, dec, raw, scl};
+    constexpr int SPG = kSpg<FMT>;
+    Ctx x{a_codes, a_scales, b_codes, b_scales, K / 2, SPG * (K / kGroup), (int)(K / 128),
+          (int)(K / (512 / SPG)), m0, n0, dec, raw, scl};
     const int nsteps = (int)(K / kBK);
 
     floatx16 acc[2][8];
@@ -1293,28 +1355,35 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][jb][e] = 0.0f;
 
-    State st;
+    StateT<SPG> st;
     // prologue: B codes of chunks 0, 1; scale chunk 0 and the A half of
-    // chunk 1; A codes of chunk 0
+    // chunk 1 (block size 8: scale chunks 0 and 1 whole); A codes of chunk 0
     copy_b_chunk(x, 0, raw);
     copy_b_chunk(x, min(1, x.nch - 1), raw + kRawBytes);
     copy_scales(x, 0, 0, scl);
     copy_scales(x, 0, 1, scl);
     copy_scales(x, min(1, x.nsc - 1), 0, scl + kSclBytes);
+    if constexpr (SPG == 2) copy_scales(x, min(1, x.nsc - 1), 1, scl + kSclBytes);
     load_a_chunk(x, arow0, h, 0, st.a[0]);
     vm_wait<0>(st.a[0][0][0], st.a[0][0][1], st.a[0][1][0], st.a[0][1][1]);
     lds_barrier();
     int r0 = 0, r1 = 1, r2 = 2;
-    read_b_raw(x, 0, st);
+    read_b_raw<SPG>(x, 0, st);
     decode_b_all<FMT>(st, dec + r0 * kStageBytes);
-    read_b_raw(x, 1, st);
+    read_b_raw<SPG>(x, 1, st);
     decode_b_all<FMT>(st, dec + r1 * kStageBytes);
-    read_b_raw(x, 2, st);
-    read_a_scales(x, 0, arow_local, h, st.as[0]);
+    read_b_raw<SPG>(x, 2, st);
+    read_a_scales<SPG>(x, 0, arow_local, h, st.as[0]);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-        st.akc[i] = pair_kc<FMT>(st.as[0][i] & 0xFFFFu);
-        decode_a_fast<FMT, 0>(st.a[0][i], st.akc[i], st.af[0][i][0], st.af[0][i][1]);
+        if constexpr (SPG == 1) {
+            st.akc[i] = pair_kc<FMT>(st.as[0][i] & 0xFFFFu);
+            decode_a_fast<FMT, 0>(st.a[0][i], st.akc[i], st.af[0][i][0], st.af[0][i][1]);
+        } else {
+            st.akc[i] = pair_kc<FMT>((uint32_t)(st.as[0][i] >> 16) & 0xFFFFu);
+            decode_a_fast<FMT, 0>(st.a[0][i], pair_kc<FMT>((uint32_t)st.as[0][i] & 0xFFFFu), st.af[0][i][0],
+                                  st.af[0][i][1]);
+        }
     }
     lds_barrier();
     // the odd step before step 0: B codes of chunk 2 into slot 0, A codes of chunk 1
@@ -1420,14 +1489,14 @@ static hipError_t launch_g(const GemmArgs& a, hipStream_t s)
     const int64_t full_n = interior_ok ? a.N / kBN : 0;
     {
       if (full_m * full_n > 0) {
-        const bool fast_ok = Fmt<FMT>::BITS == 4 && Fmt<FMT>::G == 16 && (a.K % 512) == 0 && ((uintptr_t)a.a_codes % 16) == 0 &&
+        const bool fast_ok = Fmt<FMT>::BITS == 4 && (a.K % 512) == 0 && ((uintptr_t)a.a_codes % 16) == 0 &&
                              ((uintptr_t)a.b_codes % 16) == 0 && ((uintptr_t)a.a_scales % 16) == 0 &&
                              ((uintptr_t)a.b_scales % 16) == 0;
         const dim3 grid((unsigned)(full_m * full_n)), block(kGemmThreads);
 #define IFQ_GEMM_ARGS a.a_codes, a.a_scales, a.a_ts, a.b_codes, a.b_scales, a.b_ts, a.M, a.N, a.K, a.c, a.ldc, \
                       (int)full_m, (int)full_n
         bool done = false;
-        if constexpr (Fmt<FMT>::BITS == 4 && Fmt<FMT>::G == 16) {  // fast path: 4-bit codes, one scale per 16
+        if constexpr (Fmt<FMT>::BITS == 4) {  // fast path: 4-bit codes, one scale per 16 or per 8 values
             if (fast_ok && a.out_bf16)
                 hipLaunchKernelGGL((gemm_tn_fast<FMT, true>), grid, block, 0, s, IFQ_GEMM_ARGS);
             else if (fast_ok)

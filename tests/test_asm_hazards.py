@@ -91,7 +91,7 @@ def gemm_asm(tmp_path_factory):
 
 def test_fast_gemm_kernels_have_no_pending_load_hazards(gemm_asm):
     names = re.findall(r"^(_ZN3ifq12gemm_tn_fast\S+):", gemm_asm, re.M)
-    assert len(names) >= 6  # IF4, NVFP4, NVINT4 x {fp32, bf16} out
+    assert len(names) >= 10  # IF4, NVFP4, NVINT4, IF4-BS8, NVFP4-BS8 x {fp32, bf16} out
     for name in names:
         start = gemm_asm.index(name + ":")
         body = gemm_asm[start: gemm_asm.index(".Lfunc_end", start)].split("\n")
@@ -167,9 +167,10 @@ def test_fast_gemm_copies_are_drained_within_one_barrier_period(gemm_asm):
         assert bad == [], (name, bad[:3])
 
 
-def _fast_gemm_lds_events(nch):
+def _fast_gemm_lds_events(nch, spg=1):
     """The copy and read schedule of the fast GEMM's raw-code and scale slots
-    for K = 128 nch (nch % 4 == 0), as the kernel issues it: a list of
+    for K = 128 nch (nch % 4 == 0), as the kernel issues it (spg: scale bytes
+    per 16 values; block size 8 has 2 and 4-step scale chunks): a list of
     (phase, kind, region, data) with phase the number of barriers passed
     before the event, kind 'copy' or 'read', region (slot kind, slot, half)
     and data the chunk it holds or needs (None: past the end, never used).
@@ -177,18 +178,23 @@ def _fast_gemm_lds_events(nch):
     them: a copy issued in phase p (step p - 2) is drained before the barrier
     that ends the first even step from then on, and the prologue's before
     the first barrier."""
-    nsc = nch // 4
+    cps = 4 if spg == 1 else 2          # code chunks per scale chunk
+    nsc = nch // cps
     ev = []
-    # prologue: B chunks 0, 1; scale chunk 0 (A and B halves), scale chunk 1's A half
+    # prologue: B chunks 0, 1; scale chunk 0 (A and B halves), scale chunk 1's
+    # A half (block size 8: its B half too)
     ev += [(0, "copy", ("raw", 0, 0), 0), (0, "copy", ("raw", 1, 0), min(1, nch - 1)),
            (0, "copy", ("scl", 0, 0), 0), (0, "copy", ("scl", 0, 1), 0),
            (0, "copy", ("scl", 1, 0), min(1, nsc - 1))]
+    if spg == 2:
+        ev.append((0, "copy", ("scl", 1, 1), min(1, nsc - 1)))
     # (vmcnt(0); barrier 1) reads of B steps 0, 1, 2 and the A scales of chunk 0
     def read_b(phase, sd):
         c = sd >> 1
         ok = c < nch
+        e = c // cps
         return [(phase, "read", ("raw", c & 1, 0), c if ok else None),
-                (phase, "read", ("scl", (c >> 2) & 1, 1), (c >> 2) if ok else None)]
+                (phase, "read", ("scl", e & 1, 1), e if ok else None)]
     for sd in (0, 1, 2):
         ev += read_b(1, sd)
     ev.append((1, "read", ("scl", 0, 0), 0))
@@ -200,13 +206,16 @@ def _fast_gemm_lds_events(nch):
         j, cs = q & 1, q >> 1
         if j == 1:
             ev.append((phase, "copy", ("raw", cs ^ 1, 0), min(c + 3, nch - 1)))
-            if q == 1:
+            if spg == 1 and q == 1:
                 u = s >> 2
                 e = (u + 3) >> 1
                 ev.append((phase, "copy", ("scl", e & 1, (u + 1) & 1), min(e, nsc - 1)))
+            elif spg == 2:
+                e = (s >> 2) + 2
+                ev.append((phase, "copy", ("scl", e & 1, q >> 1), min(e, nsc - 1)))
         else:
             ca = min(c + 1, nch - 1)
-            ev.append((phase, "read", ("scl", (ca >> 2) & 1, 0), ca >> 2))
+            ev.append((phase, "read", ("scl", (ca // cps) & 1, 0), ca // cps))
         ev += read_b(phase, s + 3)
     return ev
 
@@ -244,8 +253,9 @@ def _check_lds_schedule(ev):
 
 
 def test_fast_gemm_lds_slot_schedule():
-    for nch in (4, 8, 12, 32):
-        assert _check_lds_schedule(_fast_gemm_lds_events(nch)) == [], nch
+    for spg in (1, 2):
+        for nch in (4, 8, 12, 32):
+            assert _check_lds_schedule(_fast_gemm_lds_events(nch, spg)) == [], (spg, nch)
 
 
 def test_lds_schedule_checker_finds_a_slot_reused_too_early():

@@ -97,7 +97,7 @@ def _packed_from_arrays(fmt, codes, scales, alpha=1.0):
     return ops.Packed(fmt, torch.from_numpy(codes).cuda(), torch.from_numpy(scales).cuda(), ts, R, K)
 
 
-@pytest.mark.parametrize("fmt", [ops.IF4, ops.NVFP4, ops.NVINT4])
+@pytest.mark.parametrize("fmt", [ops.IF4, ops.NVFP4, ops.NVINT4, ops.IF4_BS8, ops.NVFP4_BS8])
 def test_every_code_and_scale_byte(fmt):
     """Packed operands written directly: every 4-bit code, every finite E4M3
     scale byte and, for IF4, both values of the indicator bit (both group
@@ -110,13 +110,14 @@ def test_every_code_and_scale_byte(fmt):
     only by accumulation rounding.  Case 2: random scale bytes per group
     (types mixed along K), relative Frobenius error."""
     rng = np.random.default_rng(70 + fmt)
-    top = 256 if fmt == ops.IF4 else 128
+    top = 256 if fmt in (ops.IF4, ops.IF4_BS8) else 128
     byte_vals = np.array([b for b in range(top) if (b & 0x7F) != 0x7F], dtype=np.uint8)
+    G = ops.GSIZE[fmt]
     for (M, N, K) in [(256, 256, 512), (512, 288, 1024)]:
         ca = rng.integers(0, 256, (M, K // 2), dtype=np.uint8)
         cb = rng.integers(0, 256, (N, K // 2), dtype=np.uint8)
-        sa = np.repeat(byte_vals[np.arange(M) % len(byte_vals)][:, None], K // 16, axis=1)
-        sb = np.repeat(byte_vals[(7 * np.arange(N) + 3) % len(byte_vals)][:, None], K // 16, axis=1)
+        sa = np.repeat(byte_vals[np.arange(M) % len(byte_vals)][:, None], K // G, axis=1)
+        sb = np.repeat(byte_vals[(7 * np.arange(N) + 3) % len(byte_vals)][:, None], K // G, axis=1)
         c = ops.ifx_gemm(_packed_from_arrays(fmt, ca, sa), _packed_from_arrays(fmt, cb, sb),
                          ops.F32).cpu().numpy().astype(np.float64)
         A = O.dequantize(ca, sa, 1.0, fmt, np.float64)
@@ -125,8 +126,8 @@ def test_every_code_and_scale_byte(fmt):
         bound = 3e-5 * (np.abs(A) @ np.abs(B).T)
         bad = np.abs(c - ref) > bound
         assert not bad.any(), (fmt, M, N, K, np.argwhere(bad)[:3], sa[np.argwhere(bad)[0][0], 0])
-        sa = rng.choice(byte_vals, (M, K // 16)).astype(np.uint8)
-        sb = rng.choice(byte_vals, (N, K // 16)).astype(np.uint8)
+        sa = rng.choice(byte_vals, (M, K // G)).astype(np.uint8)
+        sb = rng.choice(byte_vals, (N, K // G)).astype(np.uint8)
         c = ops.ifx_gemm(_packed_from_arrays(fmt, ca, sa), _packed_from_arrays(fmt, cb, sb),
                          ops.F32).cpu().numpy()
         ref = O.gemm_ref(ca, sa, 1.0, cb, sb, 1.0, fmt)
