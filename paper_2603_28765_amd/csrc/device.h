@@ -126,6 +126,19 @@ __device__ __forceinline__ float e4m3_value(uint32_t c)
     return __builtin_amdgcn_cvt_f32_fp8((int)(c & 0x7Fu), 0);
 }
 
+// 1/s rounded to nearest for a normal s > 0: the hardware reciprocal
+// estimate with one fma correction.  An exhaustive comparison over every
+// normal fp32 found it equal to the correctly rounded quotient up to
+// s = 2^126; above, where 1/s is subnormal, the correctly rounded division
+// is used.  (Three operations instead of the division's nine.)
+__device__ __forceinline__ float recip_rn(float s)
+{
+    if (s > 0x1p126f) return 1.0f / s;
+    const float r0 = __builtin_amdgcn_rcpf(s);
+    const float e = __builtin_fmaf(-s, r0, 1.0f);
+    return __builtin_fmaf(e, r0, r0);
+}
+
 // --------------------------------------------------------- Philox4x32-10
 // Salmon et al., SC'11.
 __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1)
@@ -271,7 +284,7 @@ __device__ __forceinline__ uint32_t quantize_group(const float (&v)[N], float al
         for (int j = 0; j < N; ++j) code[j] = 0;
         return 0;
     }
-    float inv = 1.0f / s;
+    float inv = recip_rn(s);
 
     float ef = 0.0f, ei = 0.0f;
     float rf = 0.0f, ri = 0.0f;  // RTN errors (RTN_TYPE only)
@@ -413,7 +426,7 @@ __device__ __forceinline__ uint32_t quantize_group_e2m1(const float (&v)[kGroup]
         packed = make_uint2(0, 0);
         return 0;
     }
-    const float inv = 1.0f / s;
+    const float inv = recip_rn(s);
     float xb[kGroup];
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) xb[j] = v[j] * inv;
@@ -461,7 +474,7 @@ __device__ __forceinline__ uint32_t quantize_group_int4(const float (&v)[kGroup]
         packed = make_uint2(0, 0);
         return 0;
     }
-    const float inv = 1.0f / s;
+    const float inv = recip_rn(s);
     uint32_t tb[kGroup];
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) {
@@ -537,7 +550,7 @@ __device__ __forceinline__ uint32_t quantize_group_46(const float (&v)[kGroup], 
         return 0;
     }
     float xb[kGroup];
-    const float inv4 = 1.0f / s4;
+    const float inv4 = recip_rn(s4);
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) xb[j] = v[j] * inv4;
     uint32_t b0, b1;
@@ -545,7 +558,7 @@ __device__ __forceinline__ uint32_t quantize_group_46(const float (&v)[kGroup], 
     bool keep4 = true;
     uint32_t a0 = 0, a1 = 0;
     if (s6 >= 1.17549435e-38f) {
-        const float inv6 = 1.0f / s6;
+        const float inv6 = recip_rn(s6);
 #pragma unroll
         for (int j = 0; j < kGroup; ++j) xb[j] = v[j] * inv6;
         const float e6 = (d6 * d6) * e2m1_candidate(xb, a0, a1);
@@ -573,10 +586,10 @@ __device__ __forceinline__ uint32_t quantize_group_46_sr(const float (&v)[kGroup
     }
     uint32_t c4[kGroup], c6[kGroup];
     float e4, r4, e6 = 0.0f, r6 = 0.0f;
-    e2m1_candidate_sr<true, RTN_TYPE>(v, 1.0f / s4, w, c4, e4, r4);
+    e2m1_candidate_sr<true, RTN_TYPE>(v, recip_rn(s4), w, c4, e4, r4);
     bool keep4 = true;
     if (s6 >= 1.17549435e-38f) {
-        e2m1_candidate_sr<true, RTN_TYPE>(v, 1.0f / s6, w, c6, e6, r6);
+        e2m1_candidate_sr<true, RTN_TYPE>(v, recip_rn(s6), w, c6, e6, r6);
         keep4 = RTN_TYPE ? ((d4 * d4) * r4 < (d6 * d6) * r6) : ((d4 * d4) * e4 < (d6 * d6) * e6);
     }
 #pragma unroll
@@ -680,7 +693,7 @@ __device__ __forceinline__ uint32_t quantize_group_e2m1_sr(const float (&v)[kGro
         packed = make_uint2(0, 0);
         return 0;
     }
-    const float inv = 1.0f / s;
+    const float inv = recip_rn(s);
     float xb[kGroup], qf[kGroup];
     uint32_t tb[kGroup];
     float ef = 0.0f, ei = 0.0f;
@@ -772,7 +785,7 @@ __device__ __forceinline__ uint32_t quantize_group_fp6(const float (&v)[kGroup],
         out.w[0] = out.w[1] = out.w[2] = 0;
         return 0;
     }
-    const float inv = 1.0f / s;
+    const float inv = recip_rn(s);
     float xa[kGroup];
     f16v ev, od;
 #pragma unroll
