@@ -211,6 +211,7 @@ __device__ __forceinline__ void decode_if6_group(const uint32_t* w, bool is_int,
     const half2v KF = D * half2v{(_Float16)Fold<FMT>::FP, (_Float16)Fold<FMT>::FP};
     const half2v KI = D * half2v{(_Float16)Fold<FMT>::INT, (_Float16)Fold<FMT>::INT};
     const uint32_t im = 0u - (uint32_t)is_int;  // all-ones in an INT group: branch-free select
+    const half2v KS = u32_as_h2((h2_as_u32(KI) & im) | (h2_as_u32(KF) & ~im));
     const v6i32 src = {(int)w[0], (int)w[1], (int)w[2], 0, 0, 0};
     v32f16 f;
     if constexpr (Fmt<FMT>::EB == 2)
@@ -222,24 +223,36 @@ __device__ __forceinline__ void decode_if6_group(const uint32_t* w, bool is_int,
     const uint32_t x10 = __builtin_amdgcn_alignbit(w[2], w[1], 28);
     const u16x2 bias = {0x6600, 0x6600};          // 1536 in FP16: ulp 1 on [1024, 2048)
     const half2v off = {(_Float16)1536.0f, (_Float16)1536.0f};
+    int q[16];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        int q[2];
+    for (int j = 0; j < 16; ++j) {
+        if (j < 5) q[j] = __builtin_amdgcn_sbfe((int)w[0], 6 * j, 6);
+        else if (j == 5) q[j] = __builtin_amdgcn_sbfe((int)x5, 0, 6);
+        else if (j < 10) q[j] = __builtin_amdgcn_sbfe((int)w[1], 6 * j - 32, 6);
+        else if (j == 10) q[j] = __builtin_amdgcn_sbfe((int)x10, 0, 6);
+        else q[j] = __builtin_amdgcn_sbfe((int)w[2], 6 * j - 64, 6);
+    }
+    // the INT6 pairs as FP16: bits of 1536 + q (exact), minus 1536; two
+    // pairs side by side, so that no packed operation waits on the one
+    // before it
+#pragma unroll
+    for (int i = 0; i < 8; i += 2) {
+        half2v hv[2], fv[2];
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
-            const int j = 2 * i + e;
-            if (j < 5) q[e] = __builtin_amdgcn_sbfe((int)w[0], 6 * j, 6);
-            else if (j == 5) q[e] = __builtin_amdgcn_sbfe((int)x5, 0, 6);
-            else if (j < 10) q[e] = __builtin_amdgcn_sbfe((int)w[1], 6 * j - 32, 6);
-            else if (j == 10) q[e] = __builtin_amdgcn_sbfe((int)x10, 0, 6);
-            else q[e] = __builtin_amdgcn_sbfe((int)w[2], 6 * j - 64, 6);
+            const u16x2 qq = __builtin_bit_cast(
+                u16x2, __builtin_amdgcn_perm((uint32_t)q[2 * (i + e) + 1], (uint32_t)q[2 * (i + e)], 0x05040100u));
+            hv[e] = __builtin_bit_cast(half2v, qq + bias);
+            fv[e] = half2v{f[2 * (i + e)], f[2 * (i + e) + 1]};
         }
-        // the INT6 pair as FP16: bits of 1536 + q (exact), minus 1536
-        const u16x2 qq = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm((uint32_t)q[1], (uint32_t)q[0], 0x05040100u));
-        const half2v hv = __builtin_bit_cast(half2v, qq + bias) - off;
-        const half2v fv = {f[2 * i], f[2 * i + 1]};
-        const uint32_t ri = h2_as_u32(hv * KI), rf = h2_as_u32(fv * KF);
-        out[i] = (ri & im) | (rf & ~im);
+#pragma unroll
+        for (int e = 0; e < 2; ++e) hv[e] = hv[e] - off;
+        // the group's own pair and constant, then one rounding of their product
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const uint32_t x = (h2_as_u32(hv[e]) & im) | (h2_as_u32(fv[e]) & ~im);
+            out[i + e] = h2_as_u32(u32_as_h2(x) * KS);
+        }
     }
 }
 
