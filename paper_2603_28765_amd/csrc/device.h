@@ -182,6 +182,25 @@ __device__ __forceinline__ float sr_uniform(const uint32_t (&w)[8], int j)
     return (float)h * (1.0f / 65536.0f);
 }
 
+// Stochastic rounding of t >= 0 to an integer with the draw u = h / 2^16:
+// floor(t) + 1 iff u < t - floor(t), which is ceil(t - u) of the exact
+// values.  The subtraction is exact wherever the result depends on it: for
+// t in [2^k, 2^(k+1)) with 0 <= k <= 7, t is a multiple of 2^(k-23) and u of
+// 2^-16, so t - u is a multiple of 2^(k-23) below 2^(k+1) (24 bits); for
+// t < 1, ceil is 0 or 1 and only the sign of t - u matters, which rounding
+// keeps (t - u is a multiple of 2^-149 and above -1).  The result may be -0
+// (t - u in (-1, 0)); callers use its magnitude.
+__device__ __forceinline__ float sr_ceil(float t, float u)
+{
+    return __builtin_ceilf(t - u);
+}
+
+// |m| with the sign of x (one bit-field insert)
+__device__ __forceinline__ float with_sign_of(float m, float x)
+{
+    return __uint_as_float((__float_as_uint(m) & 0x7FFFFFFFu) | (__float_as_uint(x) & 0x80000000u));
+}
+
 // --------------------------------------------------------------- RHT-16
 // v <- (1/4) H16 diag(s) v; Sylvester order, butterfly strides 1, 2, 4, 8.
 __device__ __forceinline__ void rht16(float (&v)[kGroup], uint32_t signs)
@@ -250,11 +269,9 @@ template <int FMT> __device__ __forceinline__ uint32_t fp_sr_index(float m, floa
     m = fminf(m, F::FP_MAX);
     int e = (int)((__float_as_uint(m) >> 23) & 0xFFu) - 127;
     int ee = e > 1 - BIAS ? e : 1 - BIAS;
-    float q = __uint_as_float((uint32_t)(127 + ee - F::MB) << 23);        // grid step
+    // m / q for the grid step q = 2^(ee - MB): exact, below 2^(MB + 1)
     float inv_q = __uint_as_float((uint32_t)(127 - (ee - F::MB)) << 23);
-    float lo_r = __builtin_floorf(m * inv_q);
-    float lo = lo_r * q;
-    int r = (int)lo_r + ((u * q < m - lo) ? 1 : 0);
+    int r = (int)sr_ceil(m * inv_q, u);
     return (uint32_t)(((ee + BIAS) << F::MB) + r - (1 << F::MB));
 }
 
@@ -320,11 +337,7 @@ __device__ __forceinline__ uint32_t quantize_group(const float (&v)[N], float al
             float r;
             if constexpr (SR) {
                 float y = xb * D::C_UP;
-                float a = fabsf(y);
-                float lo = __builtin_floorf(a);
-                float rr = (sr_uniform(w, j) < a - lo) ? lo + 1.0f : lo;
-                rr = fminf(rr, (float)F::IMAX);
-                r = (y < 0.0f) ? -rr : rr;
+                r = with_sign_of(fminf(sr_ceil(fabsf(y), sr_uniform(w, j)), (float)F::IMAX), y);
             } else {
                 float xc = __builtin_amdgcn_fmed3f(xb, -F::FP_MAX, F::FP_MAX);
                 float t = __builtin_fmaf(xc, D::C_UP, 12582912.0f);  // rint(xc*c_up) + 1.5*2^23
@@ -481,10 +494,8 @@ __device__ __forceinline__ uint32_t quantize_group_int4(const float (&v)[kGroup]
         const float xb = v[j] * inv;
         float t;
         if constexpr (SR) {
-            const float a = fabsf(xb);
-            const float lo = __builtin_floorf(a);
-            const float rr = fminf((sr_uniform(w, j) < a - lo) ? lo + 1.0f : lo, 7.0f);
-            t = ((xb < 0.0f) ? -rr : rr) + 12582912.0f;  // exact: an integer
+            const float rr = fminf(sr_ceil(fabsf(xb), sr_uniform(w, j)), 7.0f);
+            t = with_sign_of(rr, xb) + 12582912.0f;  // exact: an integer
         } else {
             t = __builtin_amdgcn_fmed3f(xb, -7.0f, 7.0f) + 12582912.0f;  // rint, ties to even
         }
@@ -675,9 +686,10 @@ template <int BITS> __device__ __forceinline__ void load_unpack16(const uint8_t*
 // with SR (FP: grid neighbours lo <= m < lo + q of the clamped magnitude m,
 // up iff u q < m - lo; INT: y = x c_up, up iff u < |y| - floor|y|, clamped to
 // 7), with fewer steps: the grid step q of m's binade (0.5 below 2, 1 below
-// 4, 2 above) comes from m's exponent bits, the candidate is the chosen grid
-// value itself (lo or lo + q, exact) with x's sign instead of a rebuild from
-// its code, and the codes come from the converters -- the E2M1 code of an
+// 4, 2 above) comes from m's exponent bits, both roundings are sr_ceil of the
+// exact ratio (m / q, |y|), the candidate is the chosen grid value itself
+// (lo or lo + q, exact) with x's sign instead of a rebuild from its code,
+// and the codes come from the converters -- the E2M1 code of an
 // exact grid value (round to nearest even leaves it in place, the sign and a
 // signed zero kept) and, for INT, the low nibble of r + 1.5 * 2^23.  RTN_TYPE
 // decides the type on the round-to-nearest candidates' errors (App. B).
@@ -706,17 +718,12 @@ __device__ __forceinline__ uint32_t quantize_group_e2m1_sr(const float (&v)[kGro
         const float p2 = __uint_as_float(__float_as_uint(m) & 0x7F800000u);
         const float q = fmaxf(p2 * 0.5f, 0.5f);
         const float inv_q = __uint_as_float((254u << 23) - __float_as_uint(q));
-        const float lo = __builtin_floorf(m * inv_q) * q;
-        const float mag = (u * q < m - lo) ? lo + q : lo;
-        qf[j] = __uint_as_float(__float_as_uint(mag) | (__float_as_uint(xb[j]) & 0x80000000u));
+        qf[j] = with_sign_of(sr_ceil(m * inv_q, u) * q, xb[j]);
         const float d = qf[j] - xb[j];
         ef = __builtin_fmaf(d, d, ef);
         if constexpr (ADAPTIVE) {
             const float y = xb[j] * C_UP;
-            const float a = fabsf(y);
-            const float il = __builtin_floorf(a);
-            const float rr = fminf((u < a - il) ? il + 1.0f : il, 7.0f);
-            const float r = (y < 0.0f) ? -rr : rr;
+            const float r = with_sign_of(fminf(sr_ceil(fabsf(y), u), 7.0f), y);
             tb[j] = __float_as_uint(r + 12582912.0f);
             const float di = __builtin_fmaf(r, K_DN, -xb[j]);
             ei = __builtin_fmaf(di, di, ei);
