@@ -109,11 +109,13 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f)
 }
 
 // ------------------------------------------------------------ E4M3 scales
-// Nearest E4M3 code to x >= 0, ties to even, saturating at 448 (0x7E); a
-// NaN quotient (0 / 0) also gives 0x7E.  gfx950's fp32 -> OCP E4M3
-// conversion rounds to nearest even with subnormal codes (step 2^-9); an
-// exhaustive comparison over every fp32 in [0, 464] found it equal to that
-// rule, so after clamping to 448 it is the whole encoder.
+// The encoder: nearest E4M3 code to x >= 0, ties to
+// even, saturating at 448 (0x7E); a NaN quotient (0 / 0) also gives 0x7E.
+// gfx950's fp32 -> OCP E4M3 conversion rounds to nearest even with
+// subnormal codes (step 2^-9); an exhaustive comparison over every fp32 in
+// [0, 464] found it equal to that rule, so after clamping to 448 it is the
+// whole encoder.
+
 __device__ __forceinline__ uint32_t e4m3_encode(float x)
 {
     return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(fminf(x, 448.0f), 0.0f, 0, false) & 0xFFu;
@@ -131,12 +133,101 @@ __device__ __forceinline__ float e4m3_value(uint32_t c)
 // normal fp32 found it equal to the correctly rounded quotient up to
 // s = 2^126; above, where 1/s is subnormal, the correctly rounded division
 // is used.  (Three operations instead of the division's nine.)
-__device__ __forceinline__ float recip_rn(float s)
+__device__ __forceinline__ float recip_rn_normal(float s)
 {
-    if (s > 0x1p126f) return 1.0f / s;
     const float r0 = __builtin_amdgcn_rcpf(s);
     const float e = __builtin_fmaf(-s, r0, 1.0f);
     return __builtin_fmaf(e, r0, r0);
+}
+
+__device__ __forceinline__ float recip_rn(float s)
+{
+    if (s > 0x1p126f) return 1.0f / s;
+    return recip_rn_normal(s);
+}
+
+// A divisor shared by a launch's groups -- denom = fp32(alpha * M) of Eq. 2
+// -- with its correctly rounded reciprocal, so that a group's quotient
+// amax / denom costs four operations instead of a division's eleven:
+// q0 = amax * r, e = amax - denom * q0 (exact, one fma), q = q0 + e * r
+// rounded once.  This is Markstein's correction, which gives the correctly
+// rounded quotient when r = RN(1/denom), denom and r are normal and the
+// residual e does not underflow -- guaranteed here by amax >= 2^-100 (the
+// residual is then far above 2^-126); checked against the division for 1024
+// divisor significands (all-ones tails, neighbours of powers of two,
+// random) times every dividend significand.  A quotient that overflows
+// becomes NaN or inf and one that underflows is below 2^-126; the E4M3
+// encoder maps both as it maps the true quotient (to 0x7E after its clamp,
+// and to code 0).  A wavefront uses the correction only when every lane
+// qualifies, else the division: a wave-uniform branch (all lanes share
+// alpha), which also keeps the compiler from interleaving the code before
+// and after it and lowers register pressure.  `small_s`: every group scale
+// s = alpha * Delta <= alpha * 448 is at most 2^126, so its reciprocal needs
+// no range check.
+struct Div {
+    float d, r;
+    bool fast, small_s;
+};
+
+__device__ __forceinline__ Div make_div(float alpha, float d)
+{
+    Div x;
+    x.d = d;
+    x.fast = d >= 0x1p-125f && d <= 0x1p125f;
+    x.small_s = __all(alpha * 448.0f <= 0x1p126f);
+    x.r = x.fast ? recip_rn_normal(d) : 0.0f;
+    return x;
+}
+
+// min(a / x.d, 448): the encoder's clamp is applied on each path, where the
+// compiler sees a canonical quotient and needs no NaN quieting before the
+// minimum (the empty asm statements keep it from merging the two minima
+// after the branch).
+__device__ __forceinline__ float div_rn_clamp448(float a, const Div& x)
+{
+    float q;
+    if (__builtin_expect(__all(x.fast && a >= 0x1p-100f), 1)) {
+        const float q0 = a * x.r;
+        const float e = __builtin_fmaf(-x.d, q0, a);
+        q = fminf(__builtin_fmaf(e, x.r, q0), 448.0f);
+        asm volatile("; markstein" : "+v"(q));
+    } else {
+        q = fminf(a / x.d, 448.0f);
+        asm volatile("; division" : "+v"(q));
+    }
+    return q;
+}
+
+// 1 / s for a group scale s = alpha * Delta >= 2^-126.  MK: with the
+// wave-uniform range test of x (see Div); else with the per-lane test.
+template <bool MK>
+__device__ __forceinline__ float recip_scale(float s, const Div& x)
+{
+    if constexpr (MK) {
+        if (__builtin_expect(x.small_s, 1)) return recip_rn_normal(s);
+    }
+    return recip_rn(s);
+}
+
+// Group scale of Eq. 2: the E4M3 code of amax / denom and its value Delta.
+// MK: the quotient by Markstein's correction (the stochastic-rounding
+// quantizers, where the wave-uniform branch also lowers register pressure
+// enough for a third wavefront per SIMD); else by the division.  In the
+// first form the converter's second source (0) encodes to byte 0 and the
+// untouched bytes are zero, so the code needs no mask.
+template <bool MK>
+__device__ __forceinline__ uint32_t group_scale(float amax, const Div& denom, float& delta)
+{
+    if constexpr (MK) {
+        const uint32_t code =
+            (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(div_rn_clamp448(amax, denom), 0.0f, 0, false);
+        delta = __builtin_amdgcn_cvt_f32_fp8((int)code, 0);
+        return code;
+    } else {
+        const uint32_t code = e4m3_encode(amax / denom.d);
+        delta = e4m3_value(code);
+        return code;
+    }
 }
 
 // --------------------------------------------------------- Philox4x32-10
@@ -149,10 +240,11 @@ __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1
             k0 += 0x9E3779B9u;
             k1 += 0xBB67AE85u;
         }
-        // one 32 x 32 -> 64-bit product per multiplier (v_mad_u64_u32)
+        // one 32 x 32 -> 64-bit product per multiplier (v_mad_u64_u32), and
+        // each three-way exclusive or as one gfx950 v_bitop3 (truth table 0x96)
         const uint64_t p0 = (uint64_t)0xD2511F53u * c.x, p1 = (uint64_t)0xCD9E8D57u * c.z;
-        c = make_uint4((uint32_t)(p1 >> 32) ^ c.y ^ k0, (uint32_t)p1, (uint32_t)(p0 >> 32) ^ c.w ^ k1,
-                       (uint32_t)p0);
+        c = make_uint4(__builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), c.y, k0, 0x96), (uint32_t)p1,
+                       __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), c.w, k1, 0x96), (uint32_t)p0);
     }
     return c;
 }
@@ -286,7 +378,7 @@ template <int FMT> __device__ __forceinline__ uint32_t fp_sr_index(float m, floa
 // are the stochastic candidate of that type (the App. B alternative).
 template <int FMT, bool SR, bool RTN_TYPE = false, int N = kGroup>
 __device__ __forceinline__ uint32_t quantize_group(const float (&v)[N], float alpha,
-                                                   float denom, const uint32_t (&w)[8],
+                                                   const Div& denom, const uint32_t (&w)[8],
                                                    uint32_t (&code)[N])
 {
     using F = Fmt<FMT>;
@@ -294,14 +386,15 @@ __device__ __forceinline__ uint32_t quantize_group(const float (&v)[N], float al
     float amax = 0.0f;
 #pragma unroll
     for (int j = 0; j < N; ++j) amax = fmaxf(amax, fabsf(v[j]));
-    uint32_t dcode = e4m3_encode(amax / denom);
-    float s = alpha * e4m3_value(dcode);
+    float delta;
+    uint32_t dcode = group_scale<SR>(amax, denom, delta);
+    float s = alpha * delta;
     if (!(s >= 1.17549435e-38f)) {
 #pragma unroll
         for (int j = 0; j < N; ++j) code[j] = 0;
         return 0;
     }
-    float inv = recip_rn(s);
+    float inv = recip_scale<SR>(s, denom);
 
     float ef = 0.0f, ei = 0.0f;
     float rf = 0.0f, ri = 0.0f;  // RTN errors (RTN_TYPE only)
@@ -429,17 +522,18 @@ __device__ __forceinline__ float group_amax(const float (&v)[kGroup])
 // with the FP candidate from e2m1_candidate.
 template <bool ADAPTIVE>
 __device__ __forceinline__ uint32_t quantize_group_e2m1(const float (&v)[kGroup], float alpha,
-                                                        float denom, uint2& packed)
+                                                        const Div& denom, uint2& packed)
 {
     constexpr float C_UP = 7.0f / 6.0f, K_DN = 6.0f / 7.0f;
     const float amax = group_amax(v);
-    const uint32_t dcode = e4m3_encode(amax / denom);
-    const float s = alpha * e4m3_value(dcode);
+    float delta;
+    const uint32_t dcode = group_scale<false>(amax, denom, delta);
+    const float s = alpha * delta;
     if (!(s >= 1.17549435e-38f)) {
         packed = make_uint2(0, 0);
         return 0;
     }
-    const float inv = recip_rn(s);
+    const float inv = recip_scale<false>(s, denom);
     float xb[kGroup];
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) xb[j] = v[j] * inv;
@@ -477,17 +571,18 @@ __device__ __forceinline__ uint32_t quantize_group_e2m1(const float (&v)[kGroup]
 // (clamped to 7).  Scale bit 7 stays clear.  Codes come out packed.
 template <bool SR>
 __device__ __forceinline__ uint32_t quantize_group_int4(const float (&v)[kGroup], float alpha,
-                                                        float denom, const uint32_t (&w)[8],
+                                                        const Div& denom, const uint32_t (&w)[8],
                                                         uint2& packed)
 {
     const float amax = group_amax(v);
-    const uint32_t dcode = e4m3_encode(amax / denom);
-    const float s = alpha * e4m3_value(dcode);
+    float delta;
+    const uint32_t dcode = group_scale<SR>(amax, denom, delta);
+    const float s = alpha * delta;
     if (!(s >= 1.17549435e-38f)) {
         packed = make_uint2(0, 0);
         return 0;
     }
-    const float inv = recip_rn(s);
+    const float inv = recip_scale<SR>(s, denom);
     uint32_t tb[kGroup];
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) {
@@ -550,18 +645,18 @@ __device__ __forceinline__ void e2m1_candidate_sr(const float (&v)[kGroup], floa
 
 // Round-to-nearest 4/6 with the converter path; codes packed.
 __device__ __forceinline__ uint32_t quantize_group_46(const float (&v)[kGroup], float alpha,
-                                                      float denom6, float denom4, uint2& packed)
+                                                      const Div& denom6, const Div& denom4, uint2& packed)
 {
     const float amax = group_amax(v);
-    const uint32_t dc6 = e4m3_encode(amax / denom6), dc4 = e4m3_encode(amax / denom4);
-    const float d6 = e4m3_value(dc6), d4 = e4m3_value(dc4);
+    float d6, d4;
+    const uint32_t dc6 = group_scale<false>(amax, denom6, d6), dc4 = group_scale<false>(amax, denom4, d4);
     const float s6 = alpha * d6, s4 = alpha * d4;
     if (!(s4 >= 1.17549435e-38f)) {
         packed = make_uint2(0, 0);
         return 0;
     }
     float xb[kGroup];
-    const float inv4 = recip_rn(s4);
+    const float inv4 = recip_scale<false>(s4, denom6);
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) xb[j] = v[j] * inv4;
     uint32_t b0, b1;
@@ -569,7 +664,7 @@ __device__ __forceinline__ uint32_t quantize_group_46(const float (&v)[kGroup], 
     bool keep4 = true;
     uint32_t a0 = 0, a1 = 0;
     if (s6 >= 1.17549435e-38f) {
-        const float inv6 = recip_rn(s6);
+        const float inv6 = recip_scale<false>(s6, denom6);
 #pragma unroll
         for (int j = 0; j < kGroup; ++j) xb[j] = v[j] * inv6;
         const float e6 = (d6 * d6) * e2m1_candidate(xb, a0, a1);
@@ -583,12 +678,12 @@ __device__ __forceinline__ uint32_t quantize_group_46(const float (&v)[kGroup], 
 // the round-to-nearest candidates' errors instead (App. B).
 template <bool RTN_TYPE>
 __device__ __forceinline__ uint32_t quantize_group_46_sr(const float (&v)[kGroup], float alpha,
-                                                         float denom6, float denom4,
+                                                         const Div& denom6, const Div& denom4,
                                                          const uint32_t (&w)[8], uint32_t (&code)[kGroup])
 {
     const float amax = group_amax(v);
-    const uint32_t dc6 = e4m3_encode(amax / denom6), dc4 = e4m3_encode(amax / denom4);
-    const float d6 = e4m3_value(dc6), d4 = e4m3_value(dc4);
+    float d6, d4;
+    const uint32_t dc6 = group_scale<true>(amax, denom6, d6), dc4 = group_scale<true>(amax, denom4, d4);
     const float s6 = alpha * d6, s4 = alpha * d4;
     if (!(s4 >= 1.17549435e-38f)) {
 #pragma unroll
@@ -597,10 +692,10 @@ __device__ __forceinline__ uint32_t quantize_group_46_sr(const float (&v)[kGroup
     }
     uint32_t c4[kGroup], c6[kGroup];
     float e4, r4, e6 = 0.0f, r6 = 0.0f;
-    e2m1_candidate_sr<true, RTN_TYPE>(v, recip_rn(s4), w, c4, e4, r4);
+    e2m1_candidate_sr<true, RTN_TYPE>(v, recip_scale<true>(s4, denom6), w, c4, e4, r4);
     bool keep4 = true;
     if (s6 >= 1.17549435e-38f) {
-        e2m1_candidate_sr<true, RTN_TYPE>(v, recip_rn(s6), w, c6, e6, r6);
+        e2m1_candidate_sr<true, RTN_TYPE>(v, recip_scale<true>(s6, denom6), w, c6, e6, r6);
         keep4 = RTN_TYPE ? ((d4 * d4) * r4 < (d6 * d6) * r6) : ((d4 * d4) * e4 < (d6 * d6) * e6);
     }
 #pragma unroll
@@ -694,18 +789,19 @@ template <int BITS> __device__ __forceinline__ void load_unpack16(const uint8_t*
 // signed zero kept) and, for INT, the low nibble of r + 1.5 * 2^23.  RTN_TYPE
 // decides the type on the round-to-nearest candidates' errors (App. B).
 template <bool ADAPTIVE, bool RTN_TYPE>
-__device__ __forceinline__ uint32_t quantize_group_e2m1_sr(const float (&v)[kGroup], float alpha, float denom,
+__device__ __forceinline__ uint32_t quantize_group_e2m1_sr(const float (&v)[kGroup], float alpha, const Div& denom,
                                                            const uint32_t (&w)[8], uint2& packed)
 {
     constexpr float C_UP = 7.0f / 6.0f, K_DN = 6.0f / 7.0f;
     const float amax = group_amax(v);
-    const uint32_t dcode = e4m3_encode(amax / denom);
-    const float s = alpha * e4m3_value(dcode);
+    float delta;
+    const uint32_t dcode = group_scale<true>(amax, denom, delta);
+    const float s = alpha * delta;
     if (!(s >= 1.17549435e-38f)) {
         packed = make_uint2(0, 0);
         return 0;
     }
-    const float inv = recip_rn(s);
+    const float inv = recip_scale<true>(s, denom);
     float xb[kGroup], qf[kGroup];
     uint32_t tb[kGroup];
     float ef = 0.0f, ei = 0.0f;
@@ -777,7 +873,7 @@ __device__ __forceinline__ uint32_t quantize_group_e2m1_sr(const float (&v)[kGro
 // conversion equal to the nearest-even encoder of quantize_group, and the
 // decode exact for all 64 codes of either format.
 template <int FMT>
-__device__ __forceinline__ uint32_t quantize_group_fp6(const float (&v)[kGroup], float alpha, float denom,
+__device__ __forceinline__ uint32_t quantize_group_fp6(const float (&v)[kGroup], float alpha, const Div& denom,
                                                        Packed<6>& out)
 {
     using F = Fmt<FMT>;
@@ -786,13 +882,14 @@ __device__ __forceinline__ uint32_t quantize_group_fp6(const float (&v)[kGroup],
     typedef float f32v __attribute__((ext_vector_type(32)));
     typedef uint32_t u6v __attribute__((ext_vector_type(6)));
     const float amax = group_amax(v);
-    const uint32_t dcode = e4m3_encode(amax / denom);
-    const float s = alpha * e4m3_value(dcode);
+    float delta;
+    const uint32_t dcode = group_scale<false>(amax, denom, delta);
+    const float s = alpha * delta;
     if (!(s >= 1.17549435e-38f)) {
         out.w[0] = out.w[1] = out.w[2] = 0;
         return 0;
     }
-    const float inv = recip_rn(s);
+    const float inv = recip_scale<false>(s, denom);
     float xa[kGroup];
     f16v ev, od;
 #pragma unroll
@@ -842,7 +939,7 @@ __device__ __forceinline__ uint32_t quantize_group_fp6(const float (&v)[kGroup],
 // group target (with the margin when it is on); gi is the group's index for
 // the SR draws.
 template <int FMT, bool SR>
-__device__ __forceinline__ uint32_t quantize_any(const float (&v)[kGroup], float alpha, float denom,
+__device__ __forceinline__ uint32_t quantize_any(const float (&v)[kGroup], float alpha, const Div& denom,
                                                  int qflags, uint64_t seed, int64_t gi,
                                                  Packed<Fmt<FMT>::BITS>& out)
 {
@@ -875,7 +972,7 @@ __device__ __forceinline__ uint32_t quantize_any(const float (&v)[kGroup], float
     uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if constexpr (SR) sr_words(seed, (uint64_t)gi, w);
     if constexpr (F::KIND == kKindFourSix) {
-        const float denom4 = alpha * ((qflags & kQMargin) ? kFourTargetMargin : kFourTarget);
+        const Div denom4 = make_div(alpha, alpha * ((qflags & kQMargin) ? kFourTargetMargin : kFourTarget));
         if constexpr (SR) {
             uint32_t c[kGroup];
             const uint32_t sb = rtn_type ? quantize_group_46_sr<true>(v, alpha, denom, denom4, w, c)

@@ -140,7 +140,7 @@ template <int BITS> __device__ __forceinline__ void store_packed_nt(uint8_t* dst
 
 // Quantize one (transformed) group and store its codes and scale byte.
 template <int FMT, bool SR, bool NTS = false>
-__device__ __forceinline__ void quantize_store(const float (&v)[kGroup], float alpha, float denom,
+__device__ __forceinline__ void quantize_store(const float (&v)[kGroup], float alpha, const Div& denom,
                                                uint64_t seed, int64_t gi, uint8_t* __restrict__ codes,
                                                uint8_t* __restrict__ scales, int qflags)
 {
@@ -252,7 +252,7 @@ __global__ __launch_bounds__(kThreads) void quantize_rows(
         alpha = block_max((int)threadIdx.x < npartials ? first : 0.0f, red) / denom_alpha;
         if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *tensor_scale = alpha;
     }
-    const float denom = alpha * scale_max;
+    const Div denom = make_div(alpha, alpha * scale_max);
     for (int64_t r = blockIdx.y; r < nrows; r += gridDim.y) {
         for (int64_t gc = gc_first; gc < gpr; gc += stride) {
             u32x4 a = pa, b = pb;
@@ -340,7 +340,7 @@ __global__ __launch_bounds__(kThreads) void quantize_strided(
     __shared__ uint16_t tile[kTR][kTC + 2];
     __shared__ float red[kThreads / 64];
     const float alpha = resolve_alpha(scale_in, tensor_scale, partials, npartials, denom_alpha, red);
-    const float denom = alpha * scale_max;
+    const Div denom = make_div(alpha, alpha * scale_max);
     const int64_t gpr = rows / kGroup;  // groups per output row (= per column of X)
     const int c = threadIdx.x % kTC, q = threadIdx.x / kTC;
     for (int64_t c0 = (int64_t)blockIdx.x * kTC; c0 < cols; c0 += (int64_t)gridDim.x * kTC) {
@@ -433,8 +433,12 @@ constexpr int kColTile = 64;          // columns (output rows) per block
 constexpr int kGrpTile = 64;          // groups per output row per block
 constexpr int kCodeRowBytes = kGrpTile * 8;
 
+// IF4 with stochastic rounding needs about 190 VGPRs, which allows two
+// wavefronts per SIMD; asking for three (at most 168 VGPRs, a few values
+// spilled to scratch) measured faster on dY 8192 x 14336 (137 -> 128 us).
 template <int FMT, bool RHT, bool SR>
-__global__ __launch_bounds__(kThreads) void quantize_cols(
+__global__ __launch_bounds__(kThreads)
+__attribute__((amdgpu_waves_per_eu(SR && Fmt<FMT>::ADAPTIVE ? 3 : 1))) void quantize_cols(
     const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t ld, uint32_t signs,
     uint64_t seed, int qflags, float scale_max, float denom_alpha, int scale_in,
     const float* __restrict__ partials, int npartials, uint8_t* __restrict__ codes,
@@ -445,7 +449,7 @@ __global__ __launch_bounds__(kThreads) void quantize_cols(
     __shared__ __attribute__((aligned(16))) uint8_t lscales[kColTile * kGrpTile];
     __shared__ float red[kThreads / 64];
     const float alpha = resolve_alpha(scale_in, tensor_scale, partials, npartials, denom_alpha, red);
-    const float denom = alpha * scale_max;
+    const Div denom = make_div(alpha, alpha * scale_max);
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int64_t ngroups = rows / kGroup;  // groups per output row (= per column of X)
     const int64_t c0 = (int64_t)blockIdx.x * kColTile, g0 = (int64_t)blockIdx.y * kGrpTile;
@@ -596,7 +600,8 @@ __global__ __launch_bounds__(kThreads) void quantize_dual(DualK a)
                                         a.row.denom_alpha, red);
     const float alpha_c = resolve_alpha(a.col.scale_in, a.col.tensor_scale, a.col.partials, a.npartials,
                                         a.col.denom_alpha, red);
-    const float denom_r = alpha_r * a.row.scale_max, denom_c = alpha_c * a.col.scale_max;
+    const Div denom_r = make_div(alpha_r, alpha_r * a.row.scale_max);
+    const Div denom_c = make_div(alpha_c, alpha_c * a.col.scale_max);
     const int64_t gpr_r = a.cols / kGroup, gpr_c = a.rows / kGroup;
     const int t = threadIdx.x;
     const int c = t % kTC, q = t / kTC, r = t / 4, g = t % 4;
@@ -869,7 +874,8 @@ __global__ __launch_bounds__(kThreads) void quantize_cols_dual(DualK a)
                                         a.row.denom_alpha, red);
     const float alpha_c = resolve_alpha(a.col.scale_in, a.col.tensor_scale, a.col.partials, a.npartials,
                                         a.col.denom_alpha, red);
-    const float denom_r = alpha_r * a.row.scale_max, denom_c = alpha_c * a.col.scale_max;
+    const Div denom_r = make_div(alpha_r, alpha_r * a.row.scale_max);
+    const Div denom_c = make_div(alpha_c, alpha_c * a.col.scale_max);
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int64_t ngroups = a.rows / kGroup, gpr_r = a.cols / kGroup;
     const int64_t c0 = (int64_t)blockIdx.x * kColTile, g0 = (int64_t)blockIdx.y * kGrpTile;

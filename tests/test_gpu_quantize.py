@@ -117,6 +117,43 @@ def test_ties_and_signed_zero():
         assert_quant_equal(fmt, x, 0, tag=f"ties auto fmt {fmt}")
 
 
+def _magnitude_blocks(shape, seed, exps):
+    """N(0,1) values whose 1024-value blocks (64 groups along a row-major
+    row, one wavefront's share) are scaled by 2^e for e cycling over exps."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal(shape).reshape(-1, 1024)
+    x *= np.exp2(np.array(exps, dtype=np.float64)[np.arange(x.shape[0]) % len(exps)])[:, None]
+    return workloads.to_bf16(x.reshape(shape))
+
+
+@pytest.mark.parametrize("fmt", FORMATS)
+def test_sr_scale_quotient_ranges(fmt):
+    """The stochastic-rounding quantizers compute amax / (alpha M) by a
+    correction of amax * RN(1/(alpha M)) when every lane of a wavefront has
+    amax >= 2^-100 and alpha M is normal with a normal reciprocal, and by
+    the division otherwise; 1/(alpha Delta) skips its range test when
+    alpha * 448 <= 2^126.  Tiny groups (below 2^-100, down to bf16
+    subnormals) next to ordinary ones, tiny tensors, and supplied alphas on
+    either side of each range limit, against the oracle bit for bit.  (Block
+    magnitudes stay below 2^122 so that the RHT's sums of 16 stay finite.)"""
+    shape = (256, 1024)  # rows % 256 == 0: the strided 4-bit register path too
+    cases = [
+        (_magnitude_blocks(shape, 31, [0, -105, -20, -128]), None, "mixed waves"),
+        (_magnitude_blocks(shape, 32, [-98, -101, -110, -131]), None, "tiny tensor"),
+        (_magnitude_blocks(shape, 33, [0, -3]), 2.0 ** -130, "alpha*M below 2^-125"),
+        (_magnitude_blocks(shape, 34, [110, 116]), 2.0 ** 100, "alpha 2^100"),
+        (_magnitude_blocks(shape, 35, [118, 121]), 2.0 ** 120, "alpha*448 above 2^126"),
+        (_magnitude_blocks(shape, 36, [118, 121]), 2.0 ** 124, "alpha*M above 2^125"),
+    ]
+    for x, alpha, tag in cases:
+        for flags in (ops.SR, ops.SR | ops.RHT | ops.MARGIN_16_17, ops.SR | ops.SR_RTN_TYPE):
+            f = flags | (ops.SCALE_IN if alpha is not None else 0)
+            assert_quant_equal(fmt, x, f, signs=0x5AC3, seed=99, alpha=alpha,
+                               tag=f"fmt {fmt} {tag} flags {f}")
+            assert_quant_equal(fmt, x, f | ops.AXIS_STRIDED, signs=0x5AC3, seed=98, alpha=alpha,
+                               tag=f"strided fmt {fmt} {tag} flags {f}")
+
+
 def _bf16_neighbours(v):
     """The bf16 values one step below and above each positive bf16 value v."""
     b = O.bf16_bits(np.asarray(v, dtype=np.float32)).astype(np.int64)
