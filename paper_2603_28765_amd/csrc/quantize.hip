@@ -211,7 +211,11 @@ __global__ __launch_bounds__(kThreads) void tensor_max_rows(const uint16_t* __re
     if (threadIdx.x == 0) partials[blockIdx.y * gridDim.x + blockIdx.x] = m;
 }
 
-template <int FMT, bool RHT, bool SR>
+// ONE: the grid has a thread for every group of every row (nrows <= the
+// grid's rows), so a thread quantizes at most one group and the kernel has
+// no loop -- and none of the loop's 64-bit address registers, which keeps
+// the IF4 kernel within 64 VGPRs (eight wavefronts per SIMD).
+template <int FMT, bool RHT, bool SR, bool ONE>
 __global__ __launch_bounds__(kThreads) void quantize_rows(
     const uint16_t* __restrict__ x, int64_t nrows, int64_t gpr, int64_t ld, uint32_t signs,
     uint64_t seed, int qflags, float scale_max, float denom_alpha, int scale_in,
@@ -253,6 +257,21 @@ __global__ __launch_bounds__(kThreads) void quantize_rows(
         if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *tensor_scale = alpha;
     }
     const Div denom = make_div(alpha, alpha * scale_max);
+    if constexpr (ONE) {
+        // a wavefront with pwave has all 64 of its groups in the row, so
+        // every lane takes part in wave_groups' cross-lane swaps
+        if (blockIdx.y < nrows && gc_first < gpr) {
+            float v[kGroup];
+            if (pwave)
+                wave_groups(pa, pb, v);
+            else
+                unpack_group(pa, pb, v);
+            if constexpr (RHT) rht16(v, signs);
+            quantize_store<FMT, SR, true>(v, alpha, denom, seed, (int64_t)blockIdx.y * gpr + gc_first, codes,
+                                          scales, qflags);
+        }
+        return;
+    }
     for (int64_t r = blockIdx.y; r < nrows; r += gridDim.y) {
         for (int64_t gc = gc_first; gc < gpr; gc += stride) {
             u32x4 a = pa, b = pb;
@@ -684,9 +703,14 @@ static hipError_t launch_q(const QuantArgs& a, hipStream_t s, int npartials, flo
         const int64_t gpr = flat ? a.rows * a.cols / kGroup : a.cols / kGroup;
         const int64_t ld = flat ? 0 : a.ld;
         dim3 grid((unsigned)cdiv(gpr, kThreads), (unsigned)std::min<int64_t>(nrows, 65535));
-        hipLaunchKernelGGL((quantize_rows<FMT, RHT, SR>), grid, dim3(kThreads), 0, s, a.x, nrows,
-                           gpr, ld, a.signs, a.seed, qflags, scale_max, denom_alpha, scale_in, a.partials,
-                           npartials, a.codes, a.scales, a.tensor_scale);
+        if (nrows <= 65535)
+            hipLaunchKernelGGL((quantize_rows<FMT, RHT, SR, true>), grid, dim3(kThreads), 0, s, a.x, nrows,
+                               gpr, ld, a.signs, a.seed, qflags, scale_max, denom_alpha, scale_in, a.partials,
+                               npartials, a.codes, a.scales, a.tensor_scale);
+        else
+            hipLaunchKernelGGL((quantize_rows<FMT, RHT, SR, false>), grid, dim3(kThreads), 0, s, a.x, nrows,
+                               gpr, ld, a.signs, a.seed, qflags, scale_max, denom_alpha, scale_in, a.partials,
+                               npartials, a.codes, a.scales, a.tensor_scale);
     }
     return hipGetLastError();
 }
