@@ -294,12 +294,10 @@ __device__ __forceinline__ float with_sign_of(float m, float x)
 }
 
 // --------------------------------------------------------------- RHT-16
-// v <- (1/4) H16 diag(s) v; Sylvester order, butterfly strides 1, 2, 4, 8.
-__device__ __forceinline__ void rht16(float (&v)[kGroup], uint32_t signs)
+// The butterflies of the 16-point Hadamard transform, Sylvester order,
+// strides 1, 2, 4, 8 (no signs, no scale).
+__device__ __forceinline__ void hadamard16(float (&v)[kGroup])
 {
-#pragma unroll
-    for (int j = 0; j < kGroup; ++j)
-        v[j] = __uint_as_float(__float_as_uint(v[j]) ^ (((signs >> j) & 1u) << 31));
 #pragma unroll
     for (int h = 1; h < kGroup; h <<= 1) {
 #pragma unroll
@@ -310,9 +308,31 @@ __device__ __forceinline__ void rht16(float (&v)[kGroup], uint32_t signs)
             v[i + h] = a - b;
         }
     }
+}
+
+// v <- (1/4) H16 diag(s) v
+__device__ __forceinline__ void rht16(float (&v)[kGroup], uint32_t signs)
+{
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j)
+        v[j] = __uint_as_float(__float_as_uint(v[j]) ^ (((signs >> j) & 1u) << 31));
+    hadamard16(v);
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) v[j] = v[j] * 0.25f;
 }
+
+// The signs of elements 2d and 2d + 1 as the sign bits (15, 31) of a dword
+// holding them as a bf16 pair: one exclusive or flips both before unpacking.
+__device__ __forceinline__ uint32_t rht_pair_mask(uint32_t signs, int d)
+{
+    return (((signs >> (2 * d)) & 1u) << 15) | (((signs >> (2 * d + 1)) & 1u) << 31);
+}
+
+// For bf16 inputs every value the butterflies produce is a multiple of 2^-133
+// (the bf16 quantum; a rounded sum is a multiple of its ulp, which is at
+// least 2^-133 wherever rounding happens), so H diag(s) v / 4 is exact: a
+// maximum of |H diag(s) v| times 1/4 is the maximum of the transformed
+// values.
 
 // ---------------------------------------------------- FP element rounding
 // Magnitude of non-negative FP code `idx` (both forms computed and selected:

@@ -26,7 +26,8 @@ __device__ __forceinline__ float wave_max(float m)
     return m;
 }
 
-// Block-wide max (kThreads threads); result valid in every thread.
+// Block-wide max (NT threads, red[NT / 64]); result valid in every thread.
+template <int NT = kThreads>
 __device__ __forceinline__ float block_max(float m, float* red)
 {
     m = wave_max(m);
@@ -35,10 +36,16 @@ __device__ __forceinline__ float block_max(float m, float* red)
     __syncthreads();
     float r = red[0];
 #pragma unroll
-    for (int i = 1; i < kThreads / 64; ++i) r = fmaxf(r, red[i]);
+    for (int i = 1; i < NT / 64; ++i) r = fmaxf(r, red[i]);
     __syncthreads();
     return r;
 }
+
+// Workgroup size of the tensor-max passes.  Their grid is capped at
+// kMaxPartials workgroups (one partial each), so with the RHT -- about 130
+// VALU operations per group of 16 -- 256-thread workgroups leave one
+// wavefront per SIMD; 1024 threads give four.
+template <bool RHT> constexpr int kMaxThreads = RHT ? 1024 : kThreads;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -50,12 +57,6 @@ __device__ __forceinline__ void unpack_group(u32x4 a, u32x4 b, float (&v)[kGroup
     v[4] = bf16lo(a.z);  v[5] = bf16hi(a.z);  v[6] = bf16lo(a.w);  v[7] = bf16hi(a.w);
     v[8] = bf16lo(b.x);  v[9] = bf16hi(b.x);  v[10] = bf16lo(b.y); v[11] = bf16hi(b.y);
     v[12] = bf16lo(b.z); v[13] = bf16hi(b.z); v[14] = bf16lo(b.w); v[15] = bf16hi(b.w);
-}
-
-__device__ __forceinline__ void load_group_rowwise(const uint16_t* p, float (&v)[kGroup])
-{
-    const u32x4* q = reinterpret_cast<const u32x4*>(p);
-    unpack_group(__builtin_nontemporal_load(q), __builtin_nontemporal_load(q + 1), v);
 }
 
 // 64 consecutive groups (2 KiB at p, 16-byte aligned) read by one wavefront
@@ -75,21 +76,43 @@ __device__ __forceinline__ void load_wave_raw(const uint16_t* p, u32x4& a, u32x4
     b = __builtin_nontemporal_load(q + 64 + piece);
 }
 
-__device__ __forceinline__ void wave_groups(u32x4 a, u32x4 b, float (&v)[kGroup])
+// A group's 16 values from its raw bytes (wave: as loaded by load_wave_raw,
+// else its two 16-byte pieces), with the RHT when RHT is set.  SCALE (the
+// quantize passes): the transform as rht16 computes it.  Otherwise (the
+// tensor-max passes, which scale their maximum instead): signs flipped on
+// the packed bf16 pairs and the butterflies, without the 1/4.  (Flipping
+// the packed pairs measured slower in the quantize pass.)
+template <bool RHT, bool SCALE>
+__device__ __forceinline__ void row_group_values(u32x4 a, u32x4 b, bool wave, uint32_t signs, float (&v)[kGroup])
 {
-    u32x4 lo, hi;
+    u32x4 lo = a, hi = b;
+    if (wave) {
 #pragma unroll
-    for (int d = 0; d < 4; ++d) {
-        const auto r = __builtin_amdgcn_permlane32_swap(a[d], b[d], false, false);
-        lo[d] = r[0];
-        hi[d] = r[1];
+        for (int d = 0; d < 4; ++d) {
+            const auto r = __builtin_amdgcn_permlane32_swap(a[d], b[d], false, false);
+            lo[d] = r[0];
+            hi[d] = r[1];
+        }
+    }
+    if constexpr (RHT && !SCALE) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            lo[d] ^= rht_pair_mask(signs, d);
+            hi[d] ^= rht_pair_mask(signs, d + 4);
+        }
     }
     unpack_group(lo, hi, v);
+    if constexpr (RHT) {
+        if constexpr (SCALE)
+            rht16(v, signs);
+        else
+            hadamard16(v);
+    }
 }
 
 // Raw bytes of group gc of row r: whole-wavefront loads when the wavefront's
-// 64 groups lie in the row (returns true; wave_groups then assembles lane
-// l's group), else the group's own two 16-byte pieces (returns false).
+// 64 groups lie in the row (returns true; row_group_values then assembles
+// lane l's group), else the group's own two 16-byte pieces (returns false).
 __device__ __forceinline__ bool load_row_group(const uint16_t* x, int64_t r, int64_t ld, int64_t gc,
                                                int64_t gpr, u32x4& a, u32x4& b)
 {
@@ -167,17 +190,17 @@ __device__ __forceinline__ void quantize_store(const float (&v)[kGroup], float a
 
 // --------------------------------------------------------------- row-wise
 
-template <bool RHT>
-__global__ __launch_bounds__(kThreads) void tensor_max_rows(const uint16_t* __restrict__ x,
-                                                            int64_t nrows, int64_t gpr,
-                                                            int64_t ld, uint32_t signs,
-                                                            float* __restrict__ partials)
+template <bool RHT, int NT = kMaxThreads<RHT>>
+__global__ __launch_bounds__(NT) void tensor_max_rows(const uint16_t* __restrict__ x,
+                                                      int64_t nrows, int64_t gpr,
+                                                      int64_t ld, uint32_t signs,
+                                                      float* __restrict__ partials)
 {
-    __shared__ float red[kThreads / 64];
+    __shared__ float red[NT / 64];
     float m = 0.0f;
-    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    const int64_t stride = (int64_t)gridDim.x * NT;
     for (int64_t r = blockIdx.y; r < nrows; r += gridDim.y) {
-        int64_t gc = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+        int64_t gc = (int64_t)blockIdx.x * NT + threadIdx.x;
         const int64_t gc0 = gc - (threadIdx.x & 63);  // the wavefront's first group
         // four chunks of 64 groups in flight per wavefront: the grid is small
         // (at most kMaxPartials blocks), so bytes in flight come from unrolling.
@@ -189,25 +212,23 @@ __global__ __launch_bounds__(kThreads) void tensor_max_rows(const uint16_t* __re
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 float v[kGroup];
-                if constexpr (RHT) {
-                    wave_groups(a[u], b[u], v);
-                    rht16(v, signs);
-                } else {
-                    unpack_group(a[u], b[u], v);  // which group a value is in does not matter
-                }
+                // without the RHT, which group a value is in does not matter
+                row_group_values<RHT, false>(a[u], b[u], RHT, signs, v);
 #pragma unroll
                 for (int j = 0; j < kGroup; ++j) m = fmaxf(m, fabsf(v[j]));
             }
         }
         for (; gc < gpr; gc += stride) {
+            const u32x4* q = reinterpret_cast<const u32x4*>(x + r * ld + gc * kGroup);
             float v[kGroup];
-            load_group_rowwise(x + r * ld + gc * kGroup, v);
-            if constexpr (RHT) rht16(v, signs);
+            row_group_values<RHT, false>(__builtin_nontemporal_load(q), __builtin_nontemporal_load(q + 1), false,
+                                         signs, v);
 #pragma unroll
             for (int j = 0; j < kGroup; ++j) m = fmaxf(m, fabsf(v[j]));
         }
     }
-    m = block_max(m, red);
+    if constexpr (RHT) m *= 0.25f;  // exact: the maximum of the transformed values
+    m = block_max<NT>(m, red);
     if (threadIdx.x == 0) partials[blockIdx.y * gridDim.x + blockIdx.x] = m;
 }
 
@@ -259,14 +280,10 @@ __global__ __launch_bounds__(kThreads) void quantize_rows(
     const Div denom = make_div(alpha, alpha * scale_max);
     if constexpr (ONE) {
         // a wavefront with pwave has all 64 of its groups in the row, so
-        // every lane takes part in wave_groups' cross-lane swaps
+        // every lane takes part in row_group_values' cross-lane swaps
         if (blockIdx.y < nrows && gc_first < gpr) {
             float v[kGroup];
-            if (pwave)
-                wave_groups(pa, pb, v);
-            else
-                unpack_group(pa, pb, v);
-            if constexpr (RHT) rht16(v, signs);
+            row_group_values<RHT, true>(pa, pb, pwave, signs, v);
             quantize_store<FMT, SR, true>(v, alpha, denom, seed, (int64_t)blockIdx.y * gpr + gc_first, codes,
                                           scales, qflags);
         }
@@ -278,11 +295,7 @@ __global__ __launch_bounds__(kThreads) void quantize_rows(
             bool wave = pwave;
             if (r != blockIdx.y || gc != gc_first) wave = load_row_group(x, r, ld, gc, gpr, a, b);
             float v[kGroup];
-            if (wave)
-                wave_groups(a, b, v);
-            else
-                unpack_group(a, b, v);
-            if constexpr (RHT) rht16(v, signs);
+            row_group_values<RHT, true>(a, b, wave, signs, v);
             const int64_t gi = r * gpr + gc;
             quantize_store<FMT, SR, true>(v, alpha, denom, seed, gi, codes, scales, qflags);
         }
@@ -386,9 +399,10 @@ __global__ __launch_bounds__(kThreads) void quantize_strided(
 // the same 16 bytes (8 columns) from 16 consecutive rows: one wave
 // instruction reads 1 KiB of one row, fully coalesced.  The lane then holds
 // 8 complete column groups in 16 registers and quantizes them one after
-// another -- no LDS and no barriers.  A block covers 512 columns (4
-// wavefronts x 64 lanes x 8 columns); wavefront w of a block takes row
-// groups w, w + 4, ... of the block's row range.
+// another -- no LDS and no barriers.  In the tensor-max pass every
+// wavefront of a block covers the block's 512 columns (64 lanes x 8
+// columns), and wavefront w of a block of W wavefronts takes row groups w,
+// w + W, ... of the block's row range.
 constexpr int kColsPerBlock = 64 * 8;          // 512: every wave spans the block's 512 columns
 
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
@@ -397,6 +411,14 @@ __device__ __forceinline__ void load_col_block(const uint16_t* __restrict__ p, i
 {
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) r[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(p + j * ld));
+}
+
+// The RHT signs of a 16 x 8 bf16 block: row j is element j of each of the 8
+// column groups, so one exclusive or per dword flips both of its values.
+__device__ __forceinline__ void sign_rows(u32x4v (&r)[kGroup], uint32_t signs)
+{
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) r[j] ^= ((signs >> j) & 1u) ? 0x80008000u : 0u;
 }
 
 // Column c (0..7) of the 16 x 8 bf16 block as 16 floats.
@@ -409,32 +431,34 @@ __device__ __forceinline__ void column_of(const u32x4v (&r)[kGroup], int c, floa
     }
 }
 
-template <bool RHT>
-__global__ __launch_bounds__(kThreads) void tensor_max_cols(const uint16_t* __restrict__ x,
-                                                            int64_t rows, int64_t cols, int64_t ld,
-                                                            uint32_t signs, float* __restrict__ partials)
+template <bool RHT, int NT = kMaxThreads<RHT>>
+__global__ __launch_bounds__(NT) void tensor_max_cols(const uint16_t* __restrict__ x,
+                                                      int64_t rows, int64_t cols, int64_t ld,
+                                                      uint32_t signs, float* __restrict__ partials)
 {
-    __shared__ float red[kThreads / 64];
+    __shared__ float red[NT / 64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t ngroups = rows / kGroup;
     float m = 0.0f;
     for (int64_t cb = blockIdx.x; cb * kColsPerBlock < cols; cb += gridDim.x) {
         const int64_t col = cb * kColsPerBlock + 8 * lane;
         if (col >= cols) continue;
-        for (int64_t g = (int64_t)blockIdx.y * 4 + wave; g < ngroups; g += (int64_t)gridDim.y * 4) {
+        for (int64_t g = (int64_t)blockIdx.y * (NT / 64) + wave; g < ngroups; g += (int64_t)gridDim.y * (NT / 64)) {
             u32x4v r[kGroup];
             load_col_block(x + g * kGroup * ld + col, ld, r);
+            if constexpr (RHT) sign_rows(r, signs);
 #pragma unroll
             for (int c = 0; c < 8; ++c) {
                 float v[kGroup];
                 column_of(r, c, v);
-                if constexpr (RHT) rht16(v, signs);
+                if constexpr (RHT) hadamard16(v);
 #pragma unroll
                 for (int j = 0; j < kGroup; ++j) m = fmaxf(m, fabsf(v[j]));
             }
         }
     }
-    m = block_max(m, red);
+    if constexpr (RHT) m *= 0.25f;  // exact: the maximum of the transformed values
+    m = block_max<NT>(m, red);
     if (threadIdx.x == 0) partials[blockIdx.y * gridDim.x + blockIdx.x] = m;
 }
 
@@ -481,11 +505,16 @@ __attribute__((amdgpu_waves_per_eu(SR && Fmt<FMT>::ADAPTIVE ? 3 : 1))) void quan
         if (gl < ntg && 8 * cc < ncol) {
             u32x4v r[kGroup];
             load_col_block(x + (g0 + gl) * kGroup * ld + c0 + 8 * cc, ld, r);
+            if constexpr (RHT) sign_rows(r, signs);
 #pragma unroll
             for (int c = 0; c < 8; ++c) {
                 float v[kGroup];
                 column_of(r, c, v);
-                if constexpr (RHT) rht16(v, signs);
+                if constexpr (RHT) {
+                    hadamard16(v);
+#pragma unroll
+                    for (int j = 0; j < kGroup; ++j) v[j] = v[j] * 0.25f;
+                }
                 const int64_t gi = (c0 + 8 * cc + c) * ngroups + g0 + gl;  // SR counter: global group index
                 Packed<4> pp;
                 const uint32_t sb = quantize_any<FMT, SR>(v, alpha, denom, qflags, seed, gi, pp);
@@ -720,9 +749,10 @@ static hipError_t launch_tensor_max(const QuantArgs& a, hipStream_t s, int* npar
 {
     if ((a.flags & IFQ_AXIS_STRIDED) && strided_load_ok(a)) {
         int64_t bx = std::min<int64_t>(cdiv(a.cols, kColsPerBlock), kMaxPartials);
-        int64_t by = std::max<int64_t>(1, std::min<int64_t>(cdiv(a.rows / kGroup, 4), kMaxPartials / bx));
+        int64_t by = std::max<int64_t>(
+            1, std::min<int64_t>(cdiv(a.rows / kGroup, kMaxThreads<RHT> / 64), kMaxPartials / bx));
         *npartials = (int)(bx * by);
-        hipLaunchKernelGGL((tensor_max_cols<RHT>), dim3((unsigned)bx, (unsigned)by), dim3(kThreads), 0,
+        hipLaunchKernelGGL((tensor_max_cols<RHT>), dim3((unsigned)bx, (unsigned)by), dim3(kMaxThreads<RHT>), 0,
                            s, a.x, a.rows, a.cols, a.ld, a.signs, a.partials);
     } else if (a.flags & IFQ_AXIS_STRIDED) {
         int64_t tx = cdiv(a.cols, kTC), ty = cdiv(a.rows, kTR);
@@ -737,9 +767,9 @@ static hipError_t launch_tensor_max(const QuantArgs& a, hipStream_t s, int* npar
         const int64_t gpr = flat ? a.rows * a.cols / kGroup : a.cols / kGroup;
         const int64_t ld = flat ? 0 : a.ld;
         int64_t by = std::min<int64_t>(nrows, kMaxPartials);
-        int64_t bx = std::max<int64_t>(1, std::min<int64_t>(cdiv(gpr, kThreads), kMaxPartials / by));
+        int64_t bx = std::max<int64_t>(1, std::min<int64_t>(cdiv(gpr, kMaxThreads<RHT>), kMaxPartials / by));
         *npartials = (int)(bx * by);
-        hipLaunchKernelGGL((tensor_max_rows<RHT>), dim3((unsigned)bx, (unsigned)by), dim3(kThreads), 0,
+        hipLaunchKernelGGL((tensor_max_rows<RHT>), dim3((unsigned)bx, (unsigned)by), dim3(kMaxThreads<RHT>), 0,
                            s, a.x, nrows, gpr, ld, a.signs, a.partials);
     }
     return hipGetLastError();
