@@ -223,20 +223,29 @@ def alloc(ops, torch, fmt, rows, cols, dev="cuda"):
                       torch.empty(1, dtype=torch.float32, device=dev), rows, cols)
 
 
-def rotating_time(torch, fns, n, warmup=None):
+def rotating_time(torch, fns, n, warmup=None, min_warm_s=0.02):
     """Mean time of one launch in seconds, for launches that cycle through
     len(fns) copies of their data: fns[i % len(fns)]() runs n times back to
     back between two HIP events on the current stream, with no per-launch
     event or cache flush between the launches.  With enough copies a copy
     was last touched after more than the 256 MB infinity cache of other
-    traffic, so every launch reads its input from HBM."""
-    for i in range(max(len(fns), warmup or 0)):
-        fns[i % len(fns)]()
-    torch.cuda.synchronize()
+    traffic, so every launch reads its input from HBM.  Warm-up: batches of
+    max(len(fns), warmup) launches until at least min_warm_s of them have
+    run, so that the timed launches find the clocks settled under this
+    load (the first milliseconds after a change of workload run slower)."""
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    batch, warm, i = max(len(fns), warmup or 0), 0.0, 0
+    while warm < min_warm_s and i < 100000:
+        e0.record()
+        for _ in range(batch):
+            fns[i % len(fns)]()
+            i += 1
+        e1.record()
+        torch.cuda.synchronize()
+        warm += e0.elapsed_time(e1) * 1e-3
     e0.record()
-    for i in range(n):
-        fns[i % len(fns)]()
+    for k in range(n):  # the rotation continues where the warm-up stopped
+        fns[(i + k) % len(fns)]()
     e1.record()
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) * 1e-3 / n
@@ -415,9 +424,11 @@ def dequant_times(ops, workloads, torch):
 def context_times(ops, workloads, torch):
     """Context for the fractions, not a result of this library: a plain
     device-to-device copy of 117 MB (the size of W's bf16 data) over
-    rotating buffers, and the library FP16 GEMM (torch.matmul, hipBLASLt)
-    at the step's 8192 x 14336 x 4096 on N(0,1) FP16 operands under
-    sustained load."""
+    rotating buffers; the library FP16 GEMM (torch.matmul, hipBLASLt) at the
+    step's 8192 x 14336 x 4096 on N(0,1) FP16 operands under sustained load;
+    and this library's IF4 GEMM at that shape on all-zero operands (the same
+    instructions with no operand bit activity: the part's clock under the
+    GEMM depends on the data)."""
     n = 14336 * 4096 * 2
     copies = _copies_for(2 * n, 4)
     srcs = [torch.ones(n, dtype=torch.uint8, device="cuda") for _ in range(copies)]
@@ -430,12 +441,19 @@ def context_times(ops, workloads, torch):
     b = bt.t()
     c = torch.empty((8192, 14336), device="cuda", dtype=torch.float16)
     tg = _steady_time(torch, lambda: torch.mm(a, b, out=c), 10)
-    del a, bt, b, c
+    del a, bt, b
+    za = ops.if4_quantize(torch.zeros((8192, 4096), dtype=torch.bfloat16, device="cuda"))
+    zw = ops.if4_quantize(torch.zeros((14336, 4096), dtype=torch.bfloat16, device="cuda"))
+    cz = c.view(torch.bfloat16)
+    tz = _steady_time(torch, lambda: ops.if4_gemm(za, zw, ops.BF16, cz), 10)
+    del c, cz, za, zw
     return {"copy_117MB_GBps": round(2 * n / t / 1e9, 1),
             "copy_117MB_frac": round(2 * n / t / 1e9 / HBM_PEAK_GBS, 4),
             "fp16_matmul_8192x14336x4096_us": round(tg * 1e6, 1),
             "fp16_matmul_TFLOPs": round(2.0 * 8192 * 14336 * 4096 / tg / 1e12, 1),
-            "fp16_matmul_frac": round(2.0 * 8192 * 14336 * 4096 / tg / 1e12 / FP16_MFMA_PEAK_TFLOPS, 4)}
+            "fp16_matmul_frac": round(2.0 * 8192 * 14336 * 4096 / tg / 1e12 / FP16_MFMA_PEAK_TFLOPS, 4),
+            "if4_gemm_zero_operands_us": round(tz * 1e6, 1),
+            "if4_gemm_zero_operands_TFLOPs": round(2.0 * 8192 * 14336 * 4096 / tz / 1e12, 1)}
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
@@ -444,7 +462,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 TRAFFIC_KERNELS = {
     "gemm": ("ifq::gemm_tn_fast<0, true>", None,
              ("paper_2603_28765_amd/csrc/gemm.hip", "paper_2603_28765_amd/csrc/device.h")),
-    "quantize_W": ("ifq::quantize_rows<0, false, false>", 1,
+    "quantize_W": ("ifq::quantize_rows<0, false, false, true>", 1,
                    ("paper_2603_28765_amd/csrc/quantize.hip", "paper_2603_28765_amd/csrc/device.h")),
 }
 # Per-dispatch calibration of the byte counters against a plain 1 GiB device
