@@ -940,18 +940,20 @@ __device__ __forceinline__ uint32_t lds_off(const void* p)
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-// 16 bytes per lane from global memory into LDS at lds + 16 * lane (lds is
-// wave-uniform).
-__device__ __forceinline__ void copy16(const void* g, uint32_t lds)
+// 16 bytes per lane from global memory (wave-uniform base + this lane's
+// 32-bit offset) into LDS at lds + 16 * lane (lds is wave-uniform).
+__device__ __forceinline__ void copy16(const uint8_t* base, uint32_t voff, uint32_t lds)
 {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds)
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base),
+                 "s"(lds)
                  : "memory", "m0");
 }
 
-__device__ __forceinline__ u32x4 load16(const void* g)
+// 16 bytes per lane from base + voff + OFS into registers.
+template <int OFS> __device__ __forceinline__ u32x4 load16(const uint8_t* base, uint32_t voff)
 {
     u32x4 v;
-    asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(g) : "memory");
+    asm volatile("global_load_dwordx4 %0, %1, %2 offset:%3" : "=v"(v) : "v"(voff), "s"(base), "n"(OFS) : "memory");
     return v;
 }
 
@@ -993,6 +995,20 @@ struct Ctx {
     uint8_t* dec;    // 3 decoded stages
     uint8_t* raw;    // 2 raw B slots
     uint8_t* scl;    // 2 scale slots
+    // Loop-invariant parts of the copy and load addresses: wave-uniform bases
+    // of the tile's first row (codes and scales of A and B) and per-lane
+    // 32-bit byte offsets from them (a tile spans 256 rows, so every offset
+    // is below 256 * max(rowb, gpr)).
+    const uint8_t* a_row0;
+    const uint8_t* b_row0;
+    const uint8_t* as_row0;
+    const uint8_t* bs_row0;
+    uint32_t vb[4];      // B code copy q: row (4 q + wave) 16 + lane / 4, piece (lane % 4) ^ swz4(row)
+    uint32_t vs[2];      // scale copy q: row (2 wave + q) 32 + lane / 2, half lane % 2
+    uint32_t va[2];      // A code loads: row arow_local + 32 i, bytes 32 h ..
+    uint32_t lds_raw;    // LDS byte address of raw slot 0 (wave-uniform)
+    uint32_t lds_scl;    // LDS byte address of scale slot 0 (wave-uniform)
+    int wave;            // wave-uniform wavefront index
 };
 
 // SPG: scale bytes per 16 values (1, or 2 for block size 8).
@@ -1006,6 +1022,9 @@ template <int SPG> struct StateT {
     SclWord<SPG> bs;         // their scale bytes
     KC akc[2];               // A fold constants [row block]: of the pair in use, or
                              // (block size 8) of the second group of the step
+    KC akf;                  // (block size 8) constants of the A group decoded in
+                             // the next slice, when it is the first group of a step
+    KC bkc;                  // constants of the B group(s) decoded in the next slice
     half8 af[2][2][2];       // A fragments [group gg][row block][slice parity]
     half8 bf[2][8];          // B fragments, double buffered over slices
 };
@@ -1013,43 +1032,35 @@ template <int SPG> struct StateT {
 // B codes of chunk cc (rows n0 .. n0 + 255, 64 bytes each) into raw slot:
 // instruction q of wave w covers rows 16 (4 q + w) .. + 15, four lanes per
 // row; piece p of a row is stored at position p ^ swz4(row).
-__device__ __forceinline__ void copy_b_chunk(const Ctx& x, int cc, uint8_t* slot)
+// (Q0 .. Q1 - 1: the copies issued by this call.)
+template <int Q0 = 0, int Q1 = 4>
+__device__ __forceinline__ void copy_b_chunk(const Ctx& x, int cc, int slot)
 {
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const uint8_t* base = x.b_row0 + (int64_t)cc * 64;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int r0 = (4 * q + wave) * 16;
-        const int r = r0 + (lane >> 2);
-        const int p = (lane & 3) ^ swz4(r);
-        copy16(x.b_codes + (x.n0 + r) * x.rowb + (int64_t)cc * 64 + 16 * p,
-               __builtin_amdgcn_readfirstlane(lds_off(slot + r0 * 64)));
-    }
+    for (int q = Q0; q < Q1; ++q)
+        copy16(base, x.vb[q], x.lds_raw + slot * kRawBytes + (4 * q + x.wave) * 16 * 64);
 }
 
 // Half `hf` of scale chunk e (hf 0: the A rows, 1: the B rows): 8
 // instructions of 32 rows x 32 bytes, two per wave.
-__device__ __forceinline__ void copy_scales(const Ctx& x, int e, int hf, uint8_t* slot)
+template <int Q0 = 0, int Q1 = 2>
+__device__ __forceinline__ void copy_scales(const Ctx& x, int e, int hf, int slot)
 {
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    const uint8_t* src = hf ? x.b_scales : x.a_scales;
-    const int64_t row0 = hf ? x.n0 : x.m0;
+    const uint8_t* base = (hf ? x.bs_row0 : x.as_row0) + (int64_t)e * 32;
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-        const int r0 = (2 * wave + q) * 32;
-        const int r = r0 + (lane >> 1);
-        copy16(src + (row0 + r) * x.gpr + (int64_t)e * 32 + 16 * (lane & 1),
-               __builtin_amdgcn_readfirstlane(lds_off(slot + hf * kSclB + r0 * 32)));
-    }
+    for (int q = Q0; q < Q1; ++q)
+        copy16(base, x.vs[q], x.lds_scl + slot * kSclBytes + hf * kSclB + (2 * x.wave + q) * 32 * 32);
 }
 
 // A codes of chunk cc for this lane: rows arow0 + 32 i, bytes 32 h .. 32 h + 31.
-__device__ __forceinline__ void load_a_chunk(const Ctx& x, int64_t arow0, int h, int cc, u32x4 (&a)[2][2])
+__device__ __forceinline__ void load_a_chunk(const Ctx& x, int cc, u32x4 (&a)[2][2])
 {
+    const uint8_t* base = x.a_row0 + (int64_t)cc * 64;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-        const uint8_t* p = x.a_codes + (arow0 + 32 * i) * x.rowb + (int64_t)cc * 64 + 32 * h;
-        a[i][0] = load16(p);
-        a[i][1] = load16(p + 16);
+        a[i][0] = load16<0>(base, x.va[i]);
+        a[i][1] = load16<16>(base, x.va[i]);
     }
 }
 
@@ -1072,27 +1083,51 @@ __device__ __forceinline__ void read_a_scales(const Ctx& x, int c, int arow_loca
 }
 
 // B codes and scale bytes that step s decodes (B of step s + 2) -- chunk
-// (s + 2) / 2, step j = s % 2 of it -- for row t.
+// (s + 2) / 2, step j = s % 2 of it -- for row t: the LDS reads
+// (read_b_raw_issue) and, a few slots later, the unpacking into the state
+// (read_b_raw_finish), so that no wait for these reads falls right behind
+// them.
+template <int SPG> struct RawRead {
+    u32x4 lo, hi;
+    typename std::conditional<SPG == 2, u32x4, uint2>::type v;
+};
+
 template <int SPG>
-__device__ __forceinline__ void read_b_raw(const Ctx& x, int sd, StateT<SPG>& st)
+__device__ __forceinline__ void read_b_raw_issue(const Ctx& x, int sd, RawRead<SPG>& r)
 {
     const int t = threadIdx.x;
     const int c = sd >> 1, j = sd & 1;
     const uint8_t* rs = x.raw + (c & 1) * kRawBytes + t * 64;
     const int sw = swz4(t);
-    const u32x4 lo = *reinterpret_cast<const u32x4*>(rs + 16 * (j ^ sw));
-    const u32x4 hi = *reinterpret_cast<const u32x4*>(rs + 16 * ((2 + j) ^ sw));
-    st.bw[0] = lo.x; st.bw[1] = lo.y; st.bw[2] = lo.z; st.bw[3] = lo.w;
-    st.bw[4] = hi.x; st.bw[5] = hi.y; st.bw[6] = hi.z; st.bw[7] = hi.w;
+    r.lo = *reinterpret_cast<const u32x4*>(rs + 16 * (j ^ sw));
+    r.hi = *reinterpret_cast<const u32x4*>(rs + 16 * ((2 + j) ^ sw));
+    if constexpr (SPG == 1)
+        r.v = *reinterpret_cast<const uint2*>(x.scl + ((c >> 2) & 1) * kSclBytes + kSclB + t * 32 + 8 * (c & 3));
+    else
+        r.v = *reinterpret_cast<const u32x4*>(x.scl + ((c >> 1) & 1) * kSclBytes + kSclB + t * 32 + 16 * (c & 1));
+}
+
+template <int SPG>
+__device__ __forceinline__ void read_b_raw_finish(int sd, const RawRead<SPG>& r, StateT<SPG>& st)
+{
+    const int j = sd & 1;
+    st.bw[0] = r.lo.x; st.bw[1] = r.lo.y; st.bw[2] = r.lo.z; st.bw[3] = r.lo.w;
+    st.bw[4] = r.hi.x; st.bw[5] = r.hi.y; st.bw[6] = r.hi.z; st.bw[7] = r.hi.w;
     if constexpr (SPG == 1) {
-        const uint2 v = *reinterpret_cast<const uint2*>(x.scl + ((c >> 2) & 1) * kSclBytes + kSclB + t * 32 + 8 * (c & 3));
-        st.bs = __builtin_amdgcn_perm(v.y, v.x, j ? 0x07060302u : 0x05040100u);
+        st.bs = __builtin_amdgcn_perm(r.v.y, r.v.x, j ? 0x07060302u : 0x05040100u);
     } else {
         // 16 bytes of chunk c: groups 2j, 2j + 1 at bytes 4j .. 4j + 3 and
         // groups 4 + 2j, 5 + 2j at bytes 8 + 4j .. 8 + 4j + 3
-        const u32x4 v = *reinterpret_cast<const u32x4*>(x.scl + ((c >> 1) & 1) * kSclBytes + kSclB + t * 32 + 16 * (c & 1));
-        st.bs = j ? ((uint64_t)v.y | ((uint64_t)v.w << 32)) : ((uint64_t)v.x | ((uint64_t)v.z << 32));
+        st.bs = j ? ((uint64_t)r.v.y | ((uint64_t)r.v.w << 32)) : ((uint64_t)r.v.x | ((uint64_t)r.v.z << 32));
     }
+}
+
+template <int SPG>
+__device__ __forceinline__ void read_b_raw(const Ctx& x, int sd, StateT<SPG>& st)
+{
+    RawRead<SPG> r;
+    read_b_raw_issue<SPG>(x, sd, r);
+    read_b_raw_finish<SPG>(sd, r, st);
 }
 
 // Decode B group G (0..3, decode order) of row t into stage `stg`: halves
@@ -1186,23 +1221,24 @@ __device__ __forceinline__ void step(const Ctx& x, StateT<kSpg<FMT>>& st, int s,
     const int h = lane >> 5;
     const int c = s >> 1;
     const int swb = swz8(t);
-    if constexpr (j == 1) {
-        copy_b_chunk(x, min(c + 3, x.nch - 1), x.raw + (CS ^ 1) * kRawBytes);
-        if constexpr (SPG == 1 && Q == 1) {
-            // scale chunk e = (u + 3) / 2, half (u + 1) % 2, for u = s / 4
-            const int u = s >> 2;
-            const int e = (u + 3) >> 1;
-            copy_scales(x, min(e, x.nsc - 1), (u + 1) & 1, x.scl + (e & 1) * kSclBytes);
-        } else if constexpr (SPG == 2) {
-            // 4-step scale chunks: e = u + 2, its A half at Q = 1, its B half at Q = 3
-            const int e = (s >> 2) + 2;
-            copy_scales(x, min(e, x.nsc - 1), Q >> 1, x.scl + (e & 1) * kSclBytes);
-        }
-    } else {
-        read_a_scales<SPG>(x, min(c + 1, x.nch - 1), arow_local, h, st.as[CS ^ 1]);
+    // Odd steps copy B codes of chunk c + 3 (slots 4-7 of slice 0) and, where
+    // due, half of a scale chunk (slots 10, 11); even steps read the A scale
+    // bytes of chunk c + 1 (slot 4).
+    const int cb = min(c + 3, x.nch - 1);
+    constexpr bool SCOPY = (SPG == 1 && Q == 1) || (SPG == 2 && j == 1);
+    int se = 0, shf = 0;
+    if constexpr (SPG == 1 && Q == 1) {
+        // scale chunk e = (u + 3) / 2, half (u + 1) % 2, for u = s / 4
+        const int u = s >> 2;
+        se = (u + 3) >> 1;
+        shf = (u + 1) & 1;
+    } else if constexpr (SPG == 2 && j == 1) {
+        // 4-step scale chunks: e = u + 2, its A half at Q = 1, its B half at Q = 3
+        se = (s >> 2) + 2;
+        shf = Q >> 1;
     }
-    __builtin_amdgcn_sched_barrier(0);
-    KC bkc;
+    const int sec = min(se, x.nsc - 1);
+    RawRead<SPG> rr;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
         const int f = kk & 1, gg = kk >> 1, par = kk & 1;
@@ -1215,12 +1251,10 @@ __device__ __forceinline__ void step(const Ctx& x, StateT<kSpg<FMT>>& st, int s,
 #define IFQ_SLOT_END() __builtin_amdgcn_sched_barrier(0)
         IFQ_MFMA(0);
         read_bfrag2(nstg, nkk, lane, st.bf[f ^ 1], 0);
-        if constexpr (SPG == 1) {
-            if (kk == 0) bkc = pair_kc<FMT>(st.bs & 0xFFFFu);
-            if (kk == 2) bkc = pair_kc<FMT>(st.bs >> 16);
-        } else {
-            bkc = pair_kc<FMT>((uint32_t)(st.bs >> (16 * kk)) & 0xFFFFu);   // group kk's two bytes
-        }
+        // constants of this slice's B group (computed in an earlier slot:
+        // for block size 16 from the pair of groups 2 (kk / 2), 2 (kk / 2) + 1,
+        // for block size 8 from group kk's two bytes)
+        const KC bkc = st.bkc;
         // word 0 and word 1 of the group: the same half of bkc, or (block size
         // 8) halves 0 and 1
         const TypeSel bts = (SPG == 1 && (kk & 1)) ? type_sel<FMT, 1>(bkc) : type_sel<FMT, 0>(bkc);
@@ -1239,16 +1273,24 @@ __device__ __forceinline__ void step(const Ctx& x, StateT<kSpg<FMT>>& st, int s,
         wd_s3<FMT, true>(b0);
         IFQ_SLOT_END();
         IFQ_MFMA(4);
+        if (kk == 0) {
+            if constexpr (j == 1) copy_b_chunk<0, 1>(x, cb, CS ^ 1);
+            else read_a_scales<SPG>(x, min(c + 1, x.nch - 1), arow_local, h, st.as[CS ^ 1]);
+        }
+        if (kk == 3) read_b_raw_issue<SPG>(x, s + 3, rr);
         uint32_t v0[4], v1[4];
         if (SPG == 1 && (kk & 1)) wd_s4<FMT, 1, true>(b0, bkc, v0); else wd_s4<FMT, 0, true>(b0, bkc, v0);
         IFQ_SLOT_END();
         IFQ_MFMA(5);
+        if constexpr (j == 1) if (kk == 0) copy_b_chunk<1, 2>(x, cb, CS ^ 1);
         wd_s1<FMT, true>(st.bw[2 * kk + 1], bts1, b1);
         IFQ_SLOT_END();
         IFQ_MFMA(6);
+        if constexpr (j == 1) if (kk == 0) copy_b_chunk<2, 3>(x, cb, CS ^ 1);
         wd_s2<FMT, true>(st.bw[2 * kk + 1], bts1, b1);
         IFQ_SLOT_END();
         IFQ_MFMA(7);
+        if constexpr (j == 1) if (kk == 0) copy_b_chunk<3, 4>(x, cb, CS ^ 1);
         wd_s3<FMT, true>(b1);
         IFQ_SLOT_END();
         IFQ_MFMA(8);
@@ -1281,47 +1323,69 @@ __device__ __forceinline__ void step(const Ctx& x, StateT<kSpg<FMT>>& st, int s,
                 if (kk == 2) {
                     vm_wait<(SPG == 2 || Q == 1) ? 6 : 4>(st.a[CS ^ 1][0][0], st.a[CS ^ 1][0][1],
                                                            st.a[CS ^ 1][1][0], st.a[CS ^ 1][1][1]);
-                    load_a_chunk(x, arow0, h, min(c + 2, x.nch - 1), st.a[CS]);
-                }
-                if constexpr (SPG == 1) {
-                    st.akc[kk - 2] = pair_kc<FMT>(st.as[CS ^ 1][kk - 2] & 0xFFFFu);
-                } else {
-                    akc = pair_kc<FMT>((uint32_t)st.as[CS ^ 1][kk - 2] & 0xFFFFu);
-                    st.akc[kk - 2] = pair_kc<FMT>((uint32_t)(st.as[CS ^ 1][kk - 2] >> 16) & 0xFFFFu);
+                    load_a_chunk(x, min(c + 2, x.nch - 1), st.a[CS]);
                 }
                 aw0 = st.a[CS ^ 1][kk - 2][0][0];
                 aw1 = st.a[CS ^ 1][kk - 2][0][1];
             } else {
-                if constexpr (SPG == 1) {
-                    st.akc[kk - 2] = pair_kc<FMT>(st.as[CS][kk - 2] >> 16);
-                } else {
-                    akc = pair_kc<FMT>((uint32_t)(st.as[CS][kk - 2] >> 32) & 0xFFFFu);
-                    st.akc[kk - 2] = pair_kc<FMT>((uint32_t)(st.as[CS][kk - 2] >> 48));
-                }
                 aw0 = st.a[CS][kk - 2][1][0];
                 aw1 = st.a[CS][kk - 2][1][1];
             }
-            if constexpr (SPG == 1) akc = st.akc[kk - 2];
+            // constants computed in slot 13 of the previous slice
+            akc = SPG == 1 ? st.akc[kk - 2] : st.akf;
         }
         const TypeSel ats = (SPG == 1 && kk < 2) ? type_sel<FMT, 1>(akc) : type_sel<FMT, 0>(akc);
         const TypeSel ats1 = (SPG == 1 && kk >= 2) ? type_sel<FMT, 0>(akc) : type_sel<FMT, 1>(akc);
         wd_s1<FMT, true>(aw0, ats, a0);
         IFQ_SLOT_END();
         IFQ_MFMA(10);
+        if constexpr (SCOPY) if (kk == 0) copy_scales<0, 1>(x, sec, shf, se & 1);
         wd_s2<FMT, true>(aw0, ats, a0);
         IFQ_SLOT_END();
         IFQ_MFMA(11);
+        if constexpr (SCOPY) if (kk == 0) copy_scales<1, 2>(x, sec, shf, se & 1);
         wd_s3<FMT, true>(a0);
         IFQ_SLOT_END();
         IFQ_MFMA(12);
+        if constexpr (SPG == 1) {
+            if (kk == 1) st.bkc = pair_kc<FMT>(st.bs >> 16);
+        } else {
+            if (kk < 3) st.bkc = pair_kc<FMT>((uint32_t)(st.bs >> (16 * (kk + 1))) & 0xFFFFu);
+        }
         uint32_t o0[4], o1[4];
         if (SPG == 1 && kk < 2) wd_s4<FMT, 1, true>(a0, akc, o0); else wd_s4<FMT, 0, true>(a0, akc, o0);
         wd_s1<FMT, true>(aw1, ats1, a1);
         IFQ_SLOT_END();
         IFQ_MFMA(13);
+        if (kk == 1 || kk == 2) {
+            // constants of the first A group of the next step (row block kk - 1),
+            // decoded in slice kk + 1 (its slot is free: slice kk decodes row
+            // block kk % 2 with akc[kk % 2], block size 8 with its own copy)
+            const int rb = kk - 1;
+            if constexpr (j == 1) {
+                if constexpr (SPG == 1) {
+                    st.akc[rb] = pair_kc<FMT>(st.as[CS ^ 1][rb] & 0xFFFFu);
+                } else {
+                    st.akf = pair_kc<FMT>((uint32_t)st.as[CS ^ 1][rb] & 0xFFFFu);
+                    st.akc[rb] = pair_kc<FMT>((uint32_t)(st.as[CS ^ 1][rb] >> 16) & 0xFFFFu);
+                }
+            } else {
+                if constexpr (SPG == 1) {
+                    st.akc[rb] = pair_kc<FMT>(st.as[CS][rb] >> 16);
+                } else {
+                    st.akf = pair_kc<FMT>((uint32_t)(st.as[CS][rb] >> 32) & 0xFFFFu);
+                    st.akc[rb] = pair_kc<FMT>((uint32_t)(st.as[CS][rb] >> 48));
+                }
+            }
+        }
         wd_s2<FMT, true>(aw1, ats1, a1);
         IFQ_SLOT_END();
         IFQ_MFMA(14);
+        if (kk == 3) {
+            // B codes, scales and constants of the next step's first group
+            read_b_raw_finish<SPG>(s + 3, rr, st);
+            st.bkc = pair_kc<FMT>((uint32_t)st.bs & 0xFFFFu);
+        }
         wd_s3<FMT, true>(a1);
         IFQ_SLOT_END();
         IFQ_MFMA(15);
@@ -1332,7 +1396,7 @@ __device__ __forceinline__ void step(const Ctx& x, StateT<kSpg<FMT>>& st, int s,
             st.af[kk < 2 ? 1 : 0][kk & 1][0] = f0;
             st.af[kk < 2 ? 1 : 0][kk & 1][1] = f1;
         }
-        if (kk == 3) read_b_raw<SPG>(x, s + 3, st);
+
         IFQ_SLOT_END();
 #undef IFQ_MFMA
 #undef IFQ_SLOT_END
@@ -1356,8 +1420,37 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
     const int arow_local = 64 * wave + (lane & 31);
     const int64_t arow0 = m0 + arow_local;
     constexpr int SPG = kSpg<FMT>;
-    Ctx x{a_codes, a_scales, b_codes, b_scales, K / 2, SPG * (K / kGroup), (int)(K / 128),
-          (int)(K / (512 / SPG)), m0, n0, dec, raw, scl};
+    Ctx x;
+    x.a_codes = a_codes;
+    x.a_scales = a_scales;
+    x.b_codes = b_codes;
+    x.b_scales = b_scales;
+    x.rowb = K / 2;
+    x.gpr = SPG * (K / kGroup);
+    x.nch = (int)(K / 128);
+    x.nsc = (int)(K / (512 / SPG));
+    x.m0 = m0;
+    x.n0 = n0;
+    x.dec = dec;
+    x.raw = raw;
+    x.scl = scl;
+    x.a_row0 = a_codes + m0 * x.rowb;
+    x.b_row0 = b_codes + n0 * x.rowb;
+    x.as_row0 = a_scales + m0 * x.gpr;
+    x.bs_row0 = b_scales + n0 * x.gpr;
+    x.wave = __builtin_amdgcn_readfirstlane(wave);
+    x.lds_raw = __builtin_amdgcn_readfirstlane(lds_off(raw));
+    x.lds_scl = __builtin_amdgcn_readfirstlane(lds_off(scl));
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int r = (4 * q + wave) * 16 + (lane >> 2);
+        x.vb[q] = (uint32_t)(r * x.rowb) + 16u * (uint32_t)((lane & 3) ^ swz4(r));
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+        x.vs[q] = (uint32_t)(((2 * wave + q) * 32 + (lane >> 1)) * x.gpr) + 16u * (uint32_t)(lane & 1);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) x.va[i] = (uint32_t)((arow_local + 32 * i) * x.rowb) + 32u * (uint32_t)h;
     const int nsteps = (int)(K / kBK);
 
     floatx16 acc[2][8];
@@ -1371,13 +1464,13 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
     StateT<SPG> st;
     // prologue: B codes of chunks 0, 1; scale chunk 0 and the A half of
     // chunk 1 (block size 8: scale chunks 0 and 1 whole); A codes of chunk 0
-    copy_b_chunk(x, 0, raw);
-    copy_b_chunk(x, min(1, x.nch - 1), raw + kRawBytes);
-    copy_scales(x, 0, 0, scl);
-    copy_scales(x, 0, 1, scl);
-    copy_scales(x, min(1, x.nsc - 1), 0, scl + kSclBytes);
-    if constexpr (SPG == 2) copy_scales(x, min(1, x.nsc - 1), 1, scl + kSclBytes);
-    load_a_chunk(x, arow0, h, 0, st.a[0]);
+    copy_b_chunk(x, 0, 0);
+    copy_b_chunk(x, min(1, x.nch - 1), 1);
+    copy_scales(x, 0, 0, 0);
+    copy_scales(x, 0, 1, 0);
+    copy_scales(x, min(1, x.nsc - 1), 0, 1);
+    if constexpr (SPG == 2) copy_scales(x, min(1, x.nsc - 1), 1, 1);
+    load_a_chunk(x, 0, st.a[0]);
     vm_wait<0>(st.a[0][0][0], st.a[0][0][1], st.a[0][1][0], st.a[0][1][1]);
     lds_barrier();
     int r0 = 0, r1 = 1, r2 = 2;
@@ -1386,6 +1479,7 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
     read_b_raw<SPG>(x, 1, st);
     decode_b_all<FMT>(st, dec + r1 * kStageBytes);
     read_b_raw<SPG>(x, 2, st);
+    st.bkc = pair_kc<FMT>((uint32_t)st.bs & 0xFFFFu);
     read_a_scales<SPG>(x, 0, arow_local, h, st.as[0]);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -1400,8 +1494,8 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
     }
     lds_barrier();
     // the odd step before step 0: B codes of chunk 2 into slot 0, A codes of chunk 1
-    copy_b_chunk(x, min(2, x.nch - 1), raw);
-    load_a_chunk(x, arow0, h, min(1, x.nch - 1), st.a[1]);
+    copy_b_chunk(x, min(2, x.nch - 1), 0);
+    load_a_chunk(x, min(1, x.nch - 1), st.a[1]);
     read_bfrags_fast(dec + r0 * kStageBytes, 0, lane, st.bf[0]);
 
     for (int s = 0; s < nsteps; s += 4) {
@@ -1502,7 +1596,10 @@ static hipError_t launch_g(const GemmArgs& a, hipStream_t s)
     const int64_t full_n = interior_ok ? a.N / kBN : 0;
     {
       if (full_m * full_n > 0) {
-        const bool fast_ok = Fmt<FMT>::BITS == 4 && (a.K % 512) == 0 && ((uintptr_t)a.a_codes % 16) == 0 &&
+        // (K <= 2^24 keeps the fast kernel's 32-bit per-lane offsets, below
+        // 256 code rows of K / 2 bytes, in range)
+        const bool fast_ok = Fmt<FMT>::BITS == 4 && (a.K % 512) == 0 && a.K <= ((int64_t)1 << 24) &&
+                             ((uintptr_t)a.a_codes % 16) == 0 &&
                              ((uintptr_t)a.b_codes % 16) == 0 && ((uintptr_t)a.a_scales % 16) == 0 &&
                              ((uintptr_t)a.b_scales % 16) == 0;
         const dim3 grid((unsigned)(full_m * full_n)), block(kGemmThreads);
