@@ -78,6 +78,9 @@ template <> struct Fold<IFQ_FMT_IF4_BS8> : Fold<IFQ_FMT_IF4> {};
 template <> struct Fold<IFQ_FMT_IF3_BS8> : Fold<IFQ_FMT_IF3> {};
 template <> struct Fold<IFQ_FMT_NVFP4_BS8> : Fold<IFQ_FMT_NVFP4> {};
 
+typedef float float2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ uint32_t h2_as_u32(half2v h) { return __builtin_bit_cast(uint32_t, h); }
 __device__ __forceinline__ half2v u32_as_h2(uint32_t u) { return __builtin_bit_cast(half2v, u); }
 
@@ -792,14 +795,22 @@ __device__ __forceinline__ void store_tile(const floatx16 (&acc)[2][8], const fl
         for (int j = 0; j < 8; ++j) {
             const int64_t n = n0 + j * 32 + (lane & 31);
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
+            for (int e = 0; e < 16; e += 2) {
+                // elements e and e + 1 are rows m and m + 1 of column n
                 const int64_t m = m0 + 64 * wave + i * 32 + (e >> 2) * 8 + h * 4 + (e & 3);
-                if (!EDGE || (m < M && n < N)) {
-                    const float v = acc[i][j][e] * sc;
-                    if constexpr (OUT_BF16)
-                        static_cast<uint16_t*>(C)[m * ldc + n] = f32_to_bf16_rne(v);
-                    else
-                        static_cast<float*>(C)[m * ldc + n] = v;
+                const float v0 = acc[i][j][e] * sc, v1 = acc[i][j][e + 1] * sc;
+                if constexpr (OUT_BF16) {
+                    // both rounded to nearest even by one v_cvt_pk_bf16_f32; the
+                    // second row is stored from the high half
+                    const float2v v = {v0, v1};
+                    const uint32_t u = __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2v));
+                    uint16_t* c = static_cast<uint16_t*>(C);
+                    if (!EDGE || (m < M && n < N)) c[m * ldc + n] = (uint16_t)u;
+                    if (!EDGE || (m + 1 < M && n < N)) c[(m + 1) * ldc + n] = (uint16_t)(u >> 16);
+                } else {
+                    float* c = static_cast<float*>(C);
+                    if (!EDGE || (m < M && n < N)) c[m * ldc + n] = v0;
+                    if (!EDGE || (m + 1 < M && n < N)) c[(m + 1) * ldc + n] = v1;
                 }
             }
         }
