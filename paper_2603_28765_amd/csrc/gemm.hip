@@ -281,7 +281,12 @@ template <int FMT>
 __device__ __forceinline__ KC pair_kc(uint32_t sw)
 {
     KC r;
-    if constexpr (Fmt<FMT>::KIND == kKindInt) {
+    if constexpr (Fmt<FMT>::BITS == 3) {
+        // IF3: K = Delta (the folds 3 and 4 live in the code tables), C = the
+        // signed Delta, negative exactly for INT groups (only its sign is used)
+        r.K = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw & 0x7F7Fu, 1.0f, false);
+        r.C = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw, 1.0f, false);
+    } else if constexpr (Fmt<FMT>::KIND == kKindInt) {
         const half2v d = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw & 0x7F7Fu, 1.0f, false);
         const half2v ki = {(_Float16)128.0f, (_Float16)128.0f}, cn = {(_Float16)-2.0f, (_Float16)-2.0f};
         r.K = d * ki;
@@ -362,12 +367,33 @@ template <bool ON> __device__ __forceinline__ void pin4(uint32_t (&a)[4])
 struct WordDec {
     uint32_t d0, d1;
     uint32_t x[4];
+    uint32_t w, tlo, thi;   // IF3: the word and its code tables
 };
+
+// IF3 words: 8 three-bit codes, code i at bits 3i (24 bits; what lies above
+// bit 23 is ignored).  The selector bytes of four codes (one code per byte)
+// index a v_perm table of the E4M3 bytes of their folded values: 3 x E2M0
+// (sign-magnitude) for FP groups, 4 x INT3 (two's complement) for INT
+// groups -- small integers, exact in E4M3 and after the FP8 conversion in
+// FP16; one FP16 multiply by Delta then gives the operand (at most 6
+// significant bits, exact).
+// bytes 0..7 = code 0..7: FP {0, 3, 6, 12, -0, -3, -6, -12}; INT {0, 4, 8, 12, -16, -12, -8, -4}
+constexpr uint32_t kIf3FpLo = 0x544C4400u, kIf3FpHi = 0xD4CCC480u;
+constexpr uint32_t kIf3IntLo = 0x54504800u, kIf3IntHi = 0xC8D0D4D8u;
+
+__device__ __forceinline__ uint32_t if3_sel(uint32_t t)
+{
+    return (t & 7u) | ((t << 5) & 0x700u) | ((t << 10) & 0x70000u) | ((t << 15) & 0x7000000u);
+}
 
 template <int FMT, bool PIN>
 __device__ __forceinline__ void wd_s1(uint32_t w, const TypeSel& ts, WordDec& s)
 {
-    if constexpr (Fmt<FMT>::KIND == kKindInt) {
+    if constexpr (Fmt<FMT>::BITS == 3) {
+        s.w = w;
+        s.d0 = if3_sel(w);
+        pin<PIN>(s.d0);
+    } else if constexpr (Fmt<FMT>::KIND == kKindInt) {
         s.d0 = (w & 0x0F0F0F0Fu) ^ 0x08080808u;
         pin<PIN>(s.d0);
     } else if constexpr (Fmt<FMT>::ADAPTIVE) {
@@ -385,7 +411,15 @@ __device__ __forceinline__ void wd_s1(uint32_t w, const TypeSel& ts, WordDec& s)
 template <int FMT, bool PIN>
 __device__ __forceinline__ void wd_s2(uint32_t w, const TypeSel& ts, WordDec& s)
 {
-    if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
+    if constexpr (Fmt<FMT>::BITS == 3) {
+        // the group's table (M: all ones for an INT group), codes 0-3
+        s.tlo = kIf3FpLo ^ ((kIf3FpLo ^ kIf3IntLo) & ts.M);
+        s.thi = kIf3FpHi ^ ((kIf3FpHi ^ kIf3IntHi) & ts.M);
+        const uint32_t e = __builtin_amdgcn_perm(s.thi, s.tlo, s.d0);
+        s.x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(e, 1.0f, false));
+        s.x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(e, 1.0f, true));
+        if constexpr (PIN) asm volatile("" : "+v"(s.x[0]), "+v"(s.x[1]), "+v"(s.tlo), "+v"(s.thi));
+    } else if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
         const uint32_t w4 = w >> 4;
         if constexpr (Fmt<FMT>::KIND == kKindInt) s.d1 = (w4 & 0x0F0F0F0Fu) ^ 0x08080808u;
         else s.d1 = if4_bytes(w4, ts);
@@ -396,7 +430,10 @@ __device__ __forceinline__ void wd_s2(uint32_t w, const TypeSel& ts, WordDec& s)
 template <int FMT, bool PIN>
 __device__ __forceinline__ void wd_s3(WordDec& s)
 {
-    if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
+    if constexpr (Fmt<FMT>::BITS == 3) {
+        s.d1 = if3_sel(s.w >> 12);   // codes 4-7
+        pin<PIN>(s.d1);
+    } else if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
         s.x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d0, 1.0f, false));
         s.x[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d0, 1.0f, true));
         s.x[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d1, 1.0f, false));
@@ -409,9 +446,19 @@ template <int FMT, int HS, bool PIN>
 __device__ __forceinline__ void wd_s4(const WordDec& s, const KC& kc, uint32_t (&out)[4])
 {
     const half2v K2 = {kc.K[HS], kc.K[HS]};
-    const half2v C2 = {kc.C[HS], kc.C[HS]};
+    if constexpr (Fmt<FMT>::BITS == 3) {
+        const uint32_t e = __builtin_amdgcn_perm(s.thi, s.tlo, s.d1);
+        const half2v x2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(e, 1.0f, false);
+        const half2v x3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(e, 1.0f, true);
+        out[0] = h2_as_u32(u32_as_h2(s.x[0]) * K2);
+        out[1] = h2_as_u32(u32_as_h2(s.x[1]) * K2);
+        out[2] = h2_as_u32(x2 * K2);
+        out[3] = h2_as_u32(x3 * K2);
+    } else {
+        const half2v C2 = {kc.C[HS], kc.C[HS]};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) out[i] = h2_as_u32(__builtin_elementwise_fma(u32_as_h2(s.x[i]), K2, C2));
+        for (int i = 0; i < 4; ++i) out[i] = h2_as_u32(__builtin_elementwise_fma(u32_as_h2(s.x[i]), K2, C2));
+    }
     pin4<PIN>(out);
 }
 
@@ -940,10 +987,16 @@ using namespace dec;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kStageBytes = kBN * kBK * 2;       // decoded B stage, 32 KiB
 constexpr int kRawBytes = kBN * 64;              // B codes of one chunk, 16 KiB
+// Code bytes of a row per 2-step chunk and of a B chunk: 64 and 16 KiB for
+// 4-bit codes, 48 and 12 KiB for IF3.
+template <int BITS> constexpr int kChunkB = BITS == 3 ? 48 : 64;
+template <int BITS> constexpr int kRawBytesF = kBN * kChunkB<BITS>;
 constexpr int kSclBytes = (kBM + kBN) * 32;      // scales of one 8-step chunk, 16 KiB
 constexpr int kSclB = kBM * 32;                  // offset of the B rows in a scale chunk
 
 __device__ __forceinline__ int swz8(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+// IF3 raw rows (32 bytes of pieces 0 and 1): piece p at position p ^ swz2(row)
+__device__ __forceinline__ int swz2(int row) { return (row >> 3) & 1; }
 __device__ __forceinline__ int swz4(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
 
 __device__ __forceinline__ uint32_t lds_off(const void* p)
@@ -968,6 +1021,16 @@ template <int OFS> __device__ __forceinline__ u32x4 load16(const uint8_t* base, 
     return v;
 }
 
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// 8 bytes per lane from base + voff + OFS into registers.
+template <int OFS> __device__ __forceinline__ u32x2 load8(const uint8_t* base, uint32_t voff)
+{
+    u32x2 v;
+    asm volatile("global_load_dwordx2 %0, %1, %2 offset:%3" : "=v"(v) : "v"(voff), "s"(base), "n"(OFS) : "memory");
+    return v;
+}
+
 template <int N> __device__ __forceinline__ void vm_wait()
 {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
@@ -975,6 +1038,12 @@ template <int N> __device__ __forceinline__ void vm_wait()
 
 // Wait as above and mark the four registers of an A chunk as produced here.
 template <int N> __device__ __forceinline__ void vm_wait(u32x4& a, u32x4& b, u32x4& c, u32x4& d)
+{
+    asm volatile("s_waitcnt vmcnt(%4)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : "n"(N) : "memory");
+}
+
+// The same for IF3's A chunk (16 + 8 bytes per row block).
+template <int N> __device__ __forceinline__ void vm_wait(u32x4& a, u32x2& b, u32x4& c, u32x2& d)
 {
     asm volatile("s_waitcnt vmcnt(%4)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : "n"(N) : "memory");
 }
@@ -989,6 +1058,15 @@ __device__ __forceinline__ void vm_drain(u32x4 (&a)[2][2][2])
     asm volatile("s_waitcnt vmcnt(0)"
                  : "+v"(a[0][0][0]), "+v"(a[0][0][1]), "+v"(a[0][1][0]), "+v"(a[0][1][1]),
                    "+v"(a[1][0][0]), "+v"(a[1][0][1]), "+v"(a[1][1][0]), "+v"(a[1][1][1])
+                 :
+                 : "memory");
+}
+
+__device__ __forceinline__ void vm_drain(u32x4 (&a)[2][2][2], u32x2 (&a3)[2][2])
+{
+    asm volatile("s_waitcnt vmcnt(0)"
+                 : "+v"(a[0][0][0]), "+v"(a3[0][0]), "+v"(a[0][1][0]), "+v"(a3[0][1]),
+                   "+v"(a[1][0][0]), "+v"(a3[1][0]), "+v"(a[1][1][0]), "+v"(a3[1][1])
                  :
                  : "memory");
 }
@@ -1015,8 +1093,10 @@ struct Ctx {
     const uint8_t* as_row0;
     const uint8_t* bs_row0;
     uint32_t vb[4];      // B code copy q: row (4 q + wave) 16 + lane / 4, piece (lane % 4) ^ swz4(row)
+                         // (IF3: q < 2 row 64 wave + 32 q + lane / 2, piece (lane % 2) ^ swz2(row);
+                         // q = 2 row 64 wave + lane, piece 2)
     uint32_t vs[2];      // scale copy q: row (2 wave + q) 32 + lane / 2, half lane % 2
-    uint32_t va[2];      // A code loads: row arow_local + 32 i, bytes 32 h ..
+    uint32_t va[2];      // A code loads: row arow_local + 32 i, bytes 32 h .. (IF3: 24 h ..)
     uint32_t lds_raw;    // LDS byte address of raw slot 0 (wave-uniform)
     uint32_t lds_scl;    // LDS byte address of scale slot 0 (wave-uniform)
     int wave;            // wave-uniform wavefront index
@@ -1026,8 +1106,9 @@ struct Ctx {
 template <int FMT> constexpr int kSpg = Fmt<FMT>::G == 8 ? 2 : 1;
 template <int SPG> using SclWord = typename std::conditional<SPG == 2, uint64_t, uint32_t>::type;
 
-template <int SPG> struct StateT {
-    u32x4 a[2][2][2];        // A codes [chunk slot][row block][16-byte half]
+template <int SPG, int BITS = 4> struct StateT {
+    u32x4 a[2][2][2];        // A codes [chunk slot][row block][16-byte half] (IF3: first 16 bytes)
+    typename std::conditional<BITS == 3, u32x2[2][2], char>::type a3;  // IF3: the last 8 bytes
     SclWord<SPG> as[2][2];   // A scale bytes [chunk slot][row block] (4 groups)
     uint32_t bw[8];          // B codes of the next decode (4 groups, decode order)
     SclWord<SPG> bs;         // their scale bytes
@@ -1039,18 +1120,43 @@ template <int SPG> struct StateT {
     half8 af[2][2][2];       // A fragments [group gg][row block][slice parity]
     half8 bf[2][8];          // B fragments, double buffered over slices
 };
+template <int FMT> using StateF = StateT<kSpg<FMT>, Fmt<FMT>::BITS>;
+
+// The two words (8 codes each) of IF3 group g of a run of 48-bit groups in
+// dwords D: group g starts at bit 48 g; word 0 holds codes 0-7 (bits 0-23 of
+// the group), word 1 codes 8-15 (bits above 23 are ignored by the decode).
+__device__ __forceinline__ void group_words3(const uint32_t* D, int g, uint32_t& w0, uint32_t& w1)
+{
+    const int m = 3 * (g >> 1);
+    if (g & 1) {
+        w0 = __builtin_amdgcn_alignbit(D[m + 2], D[m + 1], 16);
+        w1 = D[m + 2] >> 8;
+    } else {
+        w0 = D[m];
+        w1 = __builtin_amdgcn_alignbit(D[m + 1], D[m], 24);
+    }
+}
 
 // B codes of chunk cc (rows n0 .. n0 + 255, 64 bytes each) into raw slot:
 // instruction q of wave w covers rows 16 (4 q + w) .. + 15, four lanes per
 // row; piece p of a row is stored at position p ^ swz4(row).
 // (Q0 .. Q1 - 1: the copies issued by this call.)
-template <int Q0 = 0, int Q1 = 4>
+// IF3 chunks (48 bytes a row) take three instructions per wave: q = 0, 1
+// copy pieces 0 and 1 of rows 64 wave + 32 q .. + 31 (two lanes per row)
+// into the slot's first 8 KiB (32 bytes a row), q = 2 piece 2 of rows
+// 64 wave .. + 63 (one lane per row) into its last 4 KiB.
+template <int BITS = 4, int Q0 = 0, int Q1 = (BITS == 3 ? 3 : 4)>
 __device__ __forceinline__ void copy_b_chunk(const Ctx& x, int cc, int slot)
 {
-    const uint8_t* base = x.b_row0 + (int64_t)cc * 64;
+    const uint8_t* base = x.b_row0 + (int64_t)cc * kChunkB<BITS>;
 #pragma unroll
-    for (int q = Q0; q < Q1; ++q)
-        copy16(base, x.vb[q], x.lds_raw + slot * kRawBytes + (4 * q + x.wave) * 16 * 64);
+    for (int q = Q0; q < Q1; ++q) {
+        if constexpr (BITS == 3)
+            copy16(base, x.vb[q], x.lds_raw + slot * kRawBytesF<3> +
+                                      (q < 2 ? (64 * x.wave + 32 * q) * 32 : kBN * 32 + 64 * x.wave * 16));
+        else
+            copy16(base, x.vb[q], x.lds_raw + slot * kRawBytes + (4 * q + x.wave) * 16 * 64);
+    }
 }
 
 // Half `hf` of scale chunk e (hf 0: the A rows, 1: the B rows): 8
@@ -1073,6 +1179,51 @@ __device__ __forceinline__ void load_a_chunk(const Ctx& x, int cc, u32x4 (&a)[2]
         a[i][0] = load16<0>(base, x.va[i]);
         a[i][1] = load16<16>(base, x.va[i]);
     }
+}
+
+// IF3: 24 bytes a lane and row block (groups 4 h .. 4 h + 3 of the chunk).
+__device__ __forceinline__ void load_a_chunk(const Ctx& x, int cc, u32x4 (&a)[2][2], u32x2 (&a3)[2])
+{
+    const uint8_t* base = x.a_row0 + (int64_t)cc * 48;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        a[i][0] = load16<0>(base, x.va[i]);
+        a3[i] = load8<16>(base, x.va[i]);
+    }
+}
+
+template <int FMT>
+__device__ __forceinline__ void load_a_any(const Ctx& x, int cc, StateF<FMT>& st, int slot)
+{
+    if constexpr (Fmt<FMT>::BITS == 3)
+        load_a_chunk(x, cc, st.a[slot], st.a3[slot]);
+    else
+        load_a_chunk(x, cc, st.a[slot]);
+}
+
+// The two words of local group G (0..3) of the lane's A chunk in (slot, row block).
+template <int FMT, int G>
+__device__ __forceinline__ void a_words(const StateF<FMT>& st, int slot, int rb, uint32_t& w0, uint32_t& w1)
+{
+    if constexpr (Fmt<FMT>::BITS == 3) {
+        const u32x4 v = st.a[slot][rb][0];
+        const u32x2 u = st.a3[slot][rb];
+        const uint32_t D[6] = {v.x, v.y, v.z, v.w, u.x, u.y};
+        group_words3(D, G, w0, w1);
+    } else {
+        w0 = st.a[slot][rb][G >> 1][2 * (G & 1)];
+        w1 = st.a[slot][rb][G >> 1][2 * (G & 1) + 1];
+    }
+}
+
+// Wait for the A chunk in `slot` (N loads may stay outstanding).
+template <int FMT, int N>
+__device__ __forceinline__ void vm_wait_a(StateF<FMT>& st, int slot)
+{
+    if constexpr (Fmt<FMT>::BITS == 3)
+        vm_wait<N>(st.a[slot][0][0], st.a3[slot][0], st.a[slot][1][0], st.a3[slot][1]);
+    else
+        vm_wait<N>(st.a[slot][0][0], st.a[slot][0][1], st.a[slot][1][0], st.a[slot][1][1]);
 }
 
 // Scale bytes of A chunk c for this lane (4 groups per row block; two
@@ -1099,31 +1250,49 @@ __device__ __forceinline__ void read_a_scales(const Ctx& x, int c, int arow_loca
 // (read_b_raw_finish), so that no wait for these reads falls right behind
 // them.
 template <int SPG> struct RawRead {
-    u32x4 lo, hi;
+    u32x4 lo, hi, mid;   // (mid: IF3 only)
     typename std::conditional<SPG == 2, u32x4, uint2>::type v;
 };
 
-template <int SPG>
+// IF3 reads the whole 48-byte row of the chunk (pieces 0, 1, 2).
+template <int SPG, int BITS = 4>
 __device__ __forceinline__ void read_b_raw_issue(const Ctx& x, int sd, RawRead<SPG>& r)
 {
     const int t = threadIdx.x;
     const int c = sd >> 1, j = sd & 1;
-    const uint8_t* rs = x.raw + (c & 1) * kRawBytes + t * 64;
-    const int sw = swz4(t);
-    r.lo = *reinterpret_cast<const u32x4*>(rs + 16 * (j ^ sw));
-    r.hi = *reinterpret_cast<const u32x4*>(rs + 16 * ((2 + j) ^ sw));
+    if constexpr (BITS == 3) {
+        const uint8_t* rs = x.raw + (c & 1) * kRawBytesF<3>;
+        const int sw = swz2(t);
+        r.lo = *reinterpret_cast<const u32x4*>(rs + t * 32 + 16 * sw);
+        r.mid = *reinterpret_cast<const u32x4*>(rs + t * 32 + 16 * (1 ^ sw));
+        r.hi = *reinterpret_cast<const u32x4*>(rs + kBN * 32 + t * 16);
+    } else {
+        const uint8_t* rs = x.raw + (c & 1) * kRawBytes + t * 64;
+        const int sw = swz4(t);
+        r.lo = *reinterpret_cast<const u32x4*>(rs + 16 * (j ^ sw));
+        r.hi = *reinterpret_cast<const u32x4*>(rs + 16 * ((2 + j) ^ sw));
+    }
     if constexpr (SPG == 1)
         r.v = *reinterpret_cast<const uint2*>(x.scl + ((c >> 2) & 1) * kSclBytes + kSclB + t * 32 + 8 * (c & 3));
     else
         r.v = *reinterpret_cast<const u32x4*>(x.scl + ((c >> 1) & 1) * kSclBytes + kSclB + t * 32 + 16 * (c & 1));
 }
 
-template <int SPG>
-__device__ __forceinline__ void read_b_raw_finish(int sd, const RawRead<SPG>& r, StateT<SPG>& st)
+// J: the step of the chunk (sd % 2).  IF3: the words of groups 2 J, 2 J + 1,
+// 4 + 2 J, 5 + 2 J of the row.
+template <int SPG, int BITS, int J>
+__device__ __forceinline__ void read_b_raw_finish(const RawRead<SPG>& r, StateT<SPG, BITS>& st)
 {
-    const int j = sd & 1;
-    st.bw[0] = r.lo.x; st.bw[1] = r.lo.y; st.bw[2] = r.lo.z; st.bw[3] = r.lo.w;
-    st.bw[4] = r.hi.x; st.bw[5] = r.hi.y; st.bw[6] = r.hi.z; st.bw[7] = r.hi.w;
+    constexpr int j = J;
+    if constexpr (BITS == 3) {
+        const uint32_t D[12] = {r.lo.x, r.lo.y, r.lo.z, r.lo.w, r.mid.x, r.mid.y,
+                                r.mid.z, r.mid.w, r.hi.x, r.hi.y, r.hi.z, r.hi.w};
+#pragma unroll
+        for (int G = 0; G < 4; ++G) group_words3(D, (G < 2 ? 0 : 4) + 2 * j + (G & 1), st.bw[2 * G], st.bw[2 * G + 1]);
+    } else {
+        st.bw[0] = r.lo.x; st.bw[1] = r.lo.y; st.bw[2] = r.lo.z; st.bw[3] = r.lo.w;
+        st.bw[4] = r.hi.x; st.bw[5] = r.hi.y; st.bw[6] = r.hi.z; st.bw[7] = r.hi.w;
+    }
     if constexpr (SPG == 1) {
         st.bs = __builtin_amdgcn_perm(r.v.y, r.v.x, j ? 0x07060302u : 0x05040100u);
     } else {
@@ -1133,19 +1302,19 @@ __device__ __forceinline__ void read_b_raw_finish(int sd, const RawRead<SPG>& r,
     }
 }
 
-template <int SPG>
-__device__ __forceinline__ void read_b_raw(const Ctx& x, int sd, StateT<SPG>& st)
+template <int SPG, int BITS, int J>
+__device__ __forceinline__ void read_b_raw(const Ctx& x, int sd, StateT<SPG, BITS>& st)
 {
     RawRead<SPG> r;
-    read_b_raw_issue<SPG>(x, sd, r);
-    read_b_raw_finish<SPG>(sd, r, st);
+    read_b_raw_issue<SPG, BITS>(x, sd, r);
+    read_b_raw_finish<SPG, BITS, J>(r, st);
 }
 
 // Decode B group G (0..3, decode order) of row t into stage `stg`: halves
 // 16 G .. 16 G + 15, i.e. pieces 2 G and 2 G + 1 (swizzled); kc holds the
 // constants of groups 2 (G / 2) and 2 (G / 2) + 1.
 template <int FMT, int G>
-__device__ __forceinline__ void decode_b_fast(const StateT<kSpg<FMT>>& st, const KC& kc, uint8_t* stg)
+__device__ __forceinline__ void decode_b_fast(const StateF<FMT>& st, const KC& kc, uint8_t* stg)
 {
     const int t = threadIdx.x;
     uint32_t v[8];
@@ -1160,7 +1329,7 @@ __device__ __forceinline__ void decode_b_fast(const StateT<kSpg<FMT>>& st, const
 }
 
 template <int FMT>
-__device__ __forceinline__ void decode_b_all(const StateT<kSpg<FMT>>& st, uint8_t* stg)
+__device__ __forceinline__ void decode_b_all(const StateF<FMT>& st, uint8_t* stg)
 {
     if constexpr (kSpg<FMT> == 2) {
         decode_b_fast<FMT, 0>(st, pair_kc<FMT>((uint32_t)st.bs & 0xFFFFu), stg);
@@ -1179,10 +1348,11 @@ __device__ __forceinline__ void decode_b_all(const StateT<kSpg<FMT>>& st, uint8_
 // Decode local group G (0..3) of the lane's A chunk (one row block) with the
 // constants kc of its pair.
 template <int FMT, int G>
-__device__ __forceinline__ void decode_a_fast(const u32x4 (&a)[2], const KC& kc, half8& f0, half8& f1)
+__device__ __forceinline__ void decode_a_fast(const StateF<FMT>& st, int slot, int rb, const KC& kc, half8& f0,
+                                              half8& f1)
 {
-    const uint32_t w[2] = {G < 2 ? a[0][2 * (G & 1)] : a[1][2 * (G & 1)],
-                           G < 2 ? a[0][2 * (G & 1) + 1] : a[1][2 * (G & 1) + 1]};
+    uint32_t w[2];
+    a_words<FMT, G>(st, slot, rb, w[0], w[1]);
     uint32_t v[8];
     if constexpr (kSpg<FMT> == 2)
         decode_words_kc2<FMT>(w, kc, v);   // kc: this group's two scale bytes
@@ -1222,11 +1392,12 @@ __device__ __forceinline__ void read_bfrag2(const uint8_t* stg, int kk, int lane
 //                first group at kk = 2, 3)
 // Every MFMA operand was produced at least one slice earlier.
 template <int FMT, int Q>
-__device__ __forceinline__ void step(const Ctx& x, StateT<kSpg<FMT>>& st, int s, int64_t arow0, int arow_local,
+__device__ __forceinline__ void step(const Ctx& x, StateF<FMT>& st, int s, int64_t arow0, int arow_local,
                                      uint8_t* Bs, uint8_t* Bn, uint8_t* Bd, floatx16 (&acc)[2][8])
 {
     constexpr int j = Q & 1, CS = Q >> 1;
     constexpr int SPG = kSpg<FMT>;
+    constexpr int BITS = Fmt<FMT>::BITS;
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int h = lane >> 5;
@@ -1285,23 +1456,23 @@ __device__ __forceinline__ void step(const Ctx& x, StateT<kSpg<FMT>>& st, int s,
         IFQ_SLOT_END();
         IFQ_MFMA(4);
         if (kk == 0) {
-            if constexpr (j == 1) copy_b_chunk<0, 1>(x, cb, CS ^ 1);
+            if constexpr (j == 1) copy_b_chunk<BITS, 0, 1>(x, cb, CS ^ 1);
             else read_a_scales<SPG>(x, min(c + 1, x.nch - 1), arow_local, h, st.as[CS ^ 1]);
         }
-        if (kk == 3) read_b_raw_issue<SPG>(x, s + 3, rr);
+        if (kk == 3) read_b_raw_issue<SPG, BITS>(x, s + 3, rr);
         uint32_t v0[4], v1[4];
         if (SPG == 1 && (kk & 1)) wd_s4<FMT, 1, true>(b0, bkc, v0); else wd_s4<FMT, 0, true>(b0, bkc, v0);
         IFQ_SLOT_END();
         IFQ_MFMA(5);
-        if constexpr (j == 1) if (kk == 0) copy_b_chunk<1, 2>(x, cb, CS ^ 1);
+        if constexpr (j == 1) if (kk == 0) copy_b_chunk<BITS, 1, 2>(x, cb, CS ^ 1);
         wd_s1<FMT, true>(st.bw[2 * kk + 1], bts1, b1);
         IFQ_SLOT_END();
         IFQ_MFMA(6);
-        if constexpr (j == 1) if (kk == 0) copy_b_chunk<2, 3>(x, cb, CS ^ 1);
+        if constexpr (j == 1) if (kk == 0) copy_b_chunk<BITS, 2, 3>(x, cb, CS ^ 1);
         wd_s2<FMT, true>(st.bw[2 * kk + 1], bts1, b1);
         IFQ_SLOT_END();
         IFQ_MFMA(7);
-        if constexpr (j == 1) if (kk == 0) copy_b_chunk<3, 4>(x, cb, CS ^ 1);
+        if constexpr (j == 1 && BITS == 4) if (kk == 0) copy_b_chunk<BITS, 3, 4>(x, cb, CS ^ 1);
         wd_s3<FMT, true>(b1);
         IFQ_SLOT_END();
         IFQ_MFMA(8);
@@ -1326,21 +1497,20 @@ __device__ __forceinline__ void step(const Ctx& x, StateT<kSpg<FMT>>& st, int s,
         uint32_t aw0, aw1;
         KC akc;
         if (kk < 2) {
-            aw0 = st.a[CS][kk][j][2];
-            aw1 = st.a[CS][kk][j][3];
+            a_words<FMT, 2 * j + 1>(st, CS, kk, aw0, aw1);
             akc = st.akc[kk];
         } else {
             if constexpr (j == 1) {
                 if (kk == 2) {
-                    vm_wait<(SPG == 2 || Q == 1) ? 6 : 4>(st.a[CS ^ 1][0][0], st.a[CS ^ 1][0][1],
-                                                           st.a[CS ^ 1][1][0], st.a[CS ^ 1][1][1]);
-                    load_a_chunk(x, min(c + 2, x.nch - 1), st.a[CS]);
+                    // outstanding after the wait: this step's B code copies (4, IF3: 3)
+                    // and, where issued, 2 scale copies
+                    constexpr int NB = BITS == 3 ? 3 : 4;
+                    vm_wait_a<FMT, (SPG == 2 || Q == 1) ? NB + 2 : NB>(st, CS ^ 1);
+                    load_a_any<FMT>(x, min(c + 2, x.nch - 1), st, CS);
                 }
-                aw0 = st.a[CS ^ 1][kk - 2][0][0];
-                aw1 = st.a[CS ^ 1][kk - 2][0][1];
+                a_words<FMT, 0>(st, CS ^ 1, kk - 2, aw0, aw1);
             } else {
-                aw0 = st.a[CS][kk - 2][1][0];
-                aw1 = st.a[CS][kk - 2][1][1];
+                a_words<FMT, 2>(st, CS, kk - 2, aw0, aw1);
             }
             // constants computed in slot 13 of the previous slice
             akc = SPG == 1 ? st.akc[kk - 2] : st.akf;
@@ -1394,7 +1564,7 @@ __device__ __forceinline__ void step(const Ctx& x, StateT<kSpg<FMT>>& st, int s,
         IFQ_MFMA(14);
         if (kk == 3) {
             // B codes, scales and constants of the next step's first group
-            read_b_raw_finish<SPG>(s + 3, rr, st);
+            read_b_raw_finish<SPG, BITS, (Q + 1) & 1>(rr, st);
             st.bkc = pair_kc<FMT>((uint32_t)st.bs & 0xFFFFu);
         }
         wd_s3<FMT, true>(a1);
@@ -1431,12 +1601,13 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
     const int arow_local = 64 * wave + (lane & 31);
     const int64_t arow0 = m0 + arow_local;
     constexpr int SPG = kSpg<FMT>;
+    constexpr int BITS = Fmt<FMT>::BITS;
     Ctx x;
     x.a_codes = a_codes;
     x.a_scales = a_scales;
     x.b_codes = b_codes;
     x.b_scales = b_scales;
-    x.rowb = K / 2;
+    x.rowb = K * BITS / 8;
     x.gpr = SPG * (K / kGroup);
     x.nch = (int)(K / 128);
     x.nsc = (int)(K / (512 / SPG));
@@ -1452,16 +1623,27 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
     x.wave = __builtin_amdgcn_readfirstlane(wave);
     x.lds_raw = __builtin_amdgcn_readfirstlane(lds_off(raw));
     x.lds_scl = __builtin_amdgcn_readfirstlane(lds_off(scl));
+    if constexpr (BITS == 3) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int r = (4 * q + wave) * 16 + (lane >> 2);
-        x.vb[q] = (uint32_t)(r * x.rowb) + 16u * (uint32_t)((lane & 3) ^ swz4(r));
+        for (int q = 0; q < 2; ++q) {
+            const int r = 64 * wave + 32 * q + (lane >> 1);
+            x.vb[q] = (uint32_t)(r * x.rowb) + 16u * (uint32_t)((lane & 1) ^ swz2(r));
+        }
+        x.vb[2] = (uint32_t)((64 * wave + lane) * x.rowb) + 32u;
+        x.vb[3] = 0;
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int r = (4 * q + wave) * 16 + (lane >> 2);
+            x.vb[q] = (uint32_t)(r * x.rowb) + 16u * (uint32_t)((lane & 3) ^ swz4(r));
+        }
     }
 #pragma unroll
     for (int q = 0; q < 2; ++q)
         x.vs[q] = (uint32_t)(((2 * wave + q) * 32 + (lane >> 1)) * x.gpr) + 16u * (uint32_t)(lane & 1);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) x.va[i] = (uint32_t)((arow_local + 32 * i) * x.rowb) + 32u * (uint32_t)h;
+    for (int i = 0; i < 2; ++i)
+        x.va[i] = (uint32_t)((arow_local + 32 * i) * x.rowb) + (BITS == 3 ? 24u : 32u) * (uint32_t)h;
     const int nsteps = (int)(K / kBK);
 
     floatx16 acc[2][8];
@@ -1472,41 +1654,41 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][jb][e] = 0.0f;
 
-    StateT<SPG> st;
+    StateF<FMT> st;
     // prologue: B codes of chunks 0, 1; scale chunk 0 and the A half of
     // chunk 1 (block size 8: scale chunks 0 and 1 whole); A codes of chunk 0
-    copy_b_chunk(x, 0, 0);
-    copy_b_chunk(x, min(1, x.nch - 1), 1);
+    copy_b_chunk<BITS>(x, 0, 0);
+    copy_b_chunk<BITS>(x, min(1, x.nch - 1), 1);
     copy_scales(x, 0, 0, 0);
     copy_scales(x, 0, 1, 0);
     copy_scales(x, min(1, x.nsc - 1), 0, 1);
     if constexpr (SPG == 2) copy_scales(x, min(1, x.nsc - 1), 1, 1);
-    load_a_chunk(x, 0, st.a[0]);
-    vm_wait<0>(st.a[0][0][0], st.a[0][0][1], st.a[0][1][0], st.a[0][1][1]);
+    load_a_any<FMT>(x, 0, st, 0);
+    vm_wait_a<FMT, 0>(st, 0);
     lds_barrier();
     int r0 = 0, r1 = 1, r2 = 2;
-    read_b_raw<SPG>(x, 0, st);
+    read_b_raw<SPG, BITS, 0>(x, 0, st);
     decode_b_all<FMT>(st, dec + r0 * kStageBytes);
-    read_b_raw<SPG>(x, 1, st);
+    read_b_raw<SPG, BITS, 1>(x, 1, st);
     decode_b_all<FMT>(st, dec + r1 * kStageBytes);
-    read_b_raw<SPG>(x, 2, st);
+    read_b_raw<SPG, BITS, 0>(x, 2, st);
     st.bkc = pair_kc<FMT>((uint32_t)st.bs & 0xFFFFu);
     read_a_scales<SPG>(x, 0, arow_local, h, st.as[0]);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         if constexpr (SPG == 1) {
             st.akc[i] = pair_kc<FMT>(st.as[0][i] & 0xFFFFu);
-            decode_a_fast<FMT, 0>(st.a[0][i], st.akc[i], st.af[0][i][0], st.af[0][i][1]);
+            decode_a_fast<FMT, 0>(st, 0, i, st.akc[i], st.af[0][i][0], st.af[0][i][1]);
         } else {
             st.akc[i] = pair_kc<FMT>((uint32_t)(st.as[0][i] >> 16) & 0xFFFFu);
-            decode_a_fast<FMT, 0>(st.a[0][i], pair_kc<FMT>((uint32_t)st.as[0][i] & 0xFFFFu), st.af[0][i][0],
+            decode_a_fast<FMT, 0>(st, 0, i, pair_kc<FMT>((uint32_t)st.as[0][i] & 0xFFFFu), st.af[0][i][0],
                                   st.af[0][i][1]);
         }
     }
     lds_barrier();
     // the odd step before step 0: B codes of chunk 2 into slot 0, A codes of chunk 1
-    copy_b_chunk(x, min(2, x.nch - 1), 0);
-    load_a_chunk(x, min(1, x.nch - 1), st.a[1]);
+    copy_b_chunk<BITS>(x, min(2, x.nch - 1), 0);
+    load_a_any<FMT>(x, min(1, x.nch - 1), st, 1);
     read_bfrags_fast(dec + r0 * kStageBytes, 0, lane, st.bf[0]);
 
     for (int s = 0; s < nsteps; s += 4) {
@@ -1524,7 +1706,10 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
         r2 = r0;
         r0 = t0;
     }
-    vm_drain(st.a);
+    if constexpr (BITS == 3)
+        vm_drain(st.a, st.a3);
+    else
+        vm_drain(st.a);
     store_tile<FMT, OUT_BF16, false>(acc, a_ts, b_ts, M, N, C, ldc, m0, n0);
 }
 
@@ -1541,7 +1726,7 @@ void gemm_tn_fast(const uint8_t* __restrict__ a_codes, const uint8_t* __restrict
                   int tiles_m, int tiles_n)
 {
     __shared__ __attribute__((aligned(16))) uint8_t dec[3 * fast::kStageBytes];
-    __shared__ __attribute__((aligned(16))) uint8_t raw[2 * fast::kRawBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t raw[2 * fast::kRawBytesF<Fmt<FMT>::BITS>];
     __shared__ __attribute__((aligned(16))) uint8_t scl[2 * fast::kSclBytes];
     int tm, tn;
     tile_coords(tiles_m, tiles_n, tm, tn);
@@ -1608,8 +1793,9 @@ static hipError_t launch_g(const GemmArgs& a, hipStream_t s)
     {
       if (full_m * full_n > 0) {
         // (K <= 2^24 keeps the fast kernel's 32-bit per-lane offsets, below
-        // 256 code rows of K / 2 bytes, in range)
-        const bool fast_ok = Fmt<FMT>::BITS == 4 && (a.K % 512) == 0 && a.K <= ((int64_t)1 << 24) &&
+        // 256 code rows of K * bits / 8 bytes, in range)
+        const bool fast_ok = (Fmt<FMT>::BITS == 4 || Fmt<FMT>::BITS == 3) && (a.K % 512) == 0 &&
+                             a.K <= ((int64_t)1 << 24) &&
                              ((uintptr_t)a.a_codes % 16) == 0 &&
                              ((uintptr_t)a.b_codes % 16) == 0 && ((uintptr_t)a.a_scales % 16) == 0 &&
                              ((uintptr_t)a.b_scales % 16) == 0;
@@ -1617,7 +1803,10 @@ static hipError_t launch_g(const GemmArgs& a, hipStream_t s)
 #define IFQ_GEMM_ARGS a.a_codes, a.a_scales, a.a_ts, a.b_codes, a.b_scales, a.b_ts, a.M, a.N, a.K, a.c, a.ldc, \
                       (int)full_m, (int)full_n
         bool done = false;
-        if constexpr (Fmt<FMT>::BITS == 4) {  // fast path: 4-bit codes, one scale per 16 or per 8 values
+        // fast path: 4-bit codes with one scale per 16 or per 8 values, IF3 with
+        // one per 16 (IF3 with block size 8 spills there and runs the general
+        // kernel)
+        if constexpr (Fmt<FMT>::BITS == 4 || (Fmt<FMT>::BITS == 3 && Fmt<FMT>::G == 16)) {
             if (fast_ok && a.out_bf16)
                 hipLaunchKernelGGL((gemm_tn_fast<FMT, true>), grid, block, 0, s, IFQ_GEMM_ARGS);
             else if (fast_ok)

@@ -97,11 +97,13 @@ def _packed_from_arrays(fmt, codes, scales, alpha=1.0):
     return ops.Packed(fmt, torch.from_numpy(codes).cuda(), torch.from_numpy(scales).cuda(), ts, R, K)
 
 
-@pytest.mark.parametrize("fmt", [ops.IF4, ops.NVFP4, ops.NVINT4, ops.IF4_BS8, ops.NVFP4_BS8])
+@pytest.mark.parametrize("fmt", [ops.IF4, ops.NVFP4, ops.NVINT4, ops.IF4_BS8, ops.NVFP4_BS8, ops.IF3,
+                                 ops.IF3_BS8])
 def test_every_code_and_scale_byte(fmt):
-    """Packed operands written directly: every 4-bit code, every finite E4M3
-    scale byte and, for IF4, both values of the indicator bit (both group
-    types), at shapes whose interior tiles take the fast kernel.  Case 1:
+    """Packed operands written directly: every 4-bit (or 3-bit) code, every
+    finite E4M3 scale byte and, for the adaptive formats, both values of the
+    indicator bit (both group types), at shapes whose interior tiles take the
+    fast kernel (IF3-BS8: the general kernel's interior tiles).  Case 1:
     each row has one scale byte for all its groups (rows cycle through the
     bytes), so every output is a sum of terms of one magnitude and a wrong
     decode at any scale, down to the E4M3 subnormals, shows against the
@@ -110,12 +112,13 @@ def test_every_code_and_scale_byte(fmt):
     only by accumulation rounding.  Case 2: random scale bytes per group
     (types mixed along K), relative Frobenius error."""
     rng = np.random.default_rng(70 + fmt)
-    top = 256 if fmt in (ops.IF4, ops.IF4_BS8) else 128
+    top = 256 if fmt in (ops.IF4, ops.IF4_BS8, ops.IF3, ops.IF3_BS8) else 128
     byte_vals = np.array([b for b in range(top) if (b & 0x7F) != 0x7F], dtype=np.uint8)
     G = ops.GSIZE[fmt]
+    nb = ops.BITS[fmt]
     for (M, N, K) in [(256, 256, 512), (512, 288, 1024)]:
-        ca = rng.integers(0, 256, (M, K // 2), dtype=np.uint8)
-        cb = rng.integers(0, 256, (N, K // 2), dtype=np.uint8)
+        ca = rng.integers(0, 256, (M, K * nb // 8), dtype=np.uint8)
+        cb = rng.integers(0, 256, (N, K * nb // 8), dtype=np.uint8)
         sa = np.repeat(byte_vals[np.arange(M) % len(byte_vals)][:, None], K // G, axis=1)
         sb = np.repeat(byte_vals[(7 * np.arange(N) + 3) % len(byte_vals)][:, None], K // G, axis=1)
         c = ops.ifx_gemm(_packed_from_arrays(fmt, ca, sa), _packed_from_arrays(fmt, cb, sb),
