@@ -1370,13 +1370,12 @@ __device__ __forceinline__ void read_bfrags_fast(const uint8_t* stg, int kk, int
     for (int j = 0; j < 8; ++j) bf[j] = *reinterpret_cast<const half8*>(base + j * 32 * 128);
 }
 
-// B fragments j0, j0 + 1 of slice kk of a decoded stage.
-__device__ __forceinline__ void read_bfrag2(const uint8_t* stg, int kk, int lane, half8 (&bf)[8], int j0)
+// B fragment j0 of slice kk of a decoded stage.
+__device__ __forceinline__ void read_bfrag1(const uint8_t* stg, int kk, int lane, half8 (&bf)[8], int j0)
 {
     const int h = lane >> 5;
     const uint8_t* base = stg + (lane & 31) * 128 + 16 * ((4 * h + kk) ^ swz8(lane & 31));
     bf[j0] = *reinterpret_cast<const half8*>(base + j0 * 32 * 128);
-    bf[j0 + 1] = *reinterpret_cast<const half8*>(base + (j0 + 1) * 32 * 128);
 }
 
 // One K step s = 4 u + Q of the four-step loop body.  c = s / 2 is the A
@@ -1384,7 +1383,7 @@ __device__ __forceinline__ void read_bfrag2(const uint8_t* stg, int kk, int lane
 // Each slice kk issues its 16 MFMAs one per slot and places, after each,
 // one piece of the slice's other work, fenced with sched_barrier so that
 // the matrix core never waits behind a long run of VALU work:
-//   slots 0..3 : the next slice's B fragments (two LDS reads per slot)
+//   slots 0..7 : the next slice's B fragments (one LDS read per slot)
 //   slots 1..8 : decode of one B group (stages of its two words), stored
 //                to the stage of step s + 2 at slot 8
 //   slots 9..15: decode of one A group into the fragments of a later slice
@@ -1432,7 +1431,7 @@ __device__ __forceinline__ void step(const Ctx& x, StateF<FMT>& st, int s, int64
                                                                       acc[(m) >> 3][(m) & 7], 0, 0, 0)
 #define IFQ_SLOT_END() __builtin_amdgcn_sched_barrier(0)
         IFQ_MFMA(0);
-        read_bfrag2(nstg, nkk, lane, st.bf[f ^ 1], 0);
+        read_bfrag1(nstg, nkk, lane, st.bf[f ^ 1], 0);
         // constants of this slice's B group (computed in an earlier slot:
         // for block size 16 from the pair of groups 2 (kk / 2), 2 (kk / 2) + 1,
         // for block size 8 from group kk's two bytes)
@@ -1443,18 +1442,19 @@ __device__ __forceinline__ void step(const Ctx& x, StateF<FMT>& st, int s, int64
         const TypeSel bts1 = (SPG == 1 && !(kk & 1)) ? type_sel<FMT, 0>(bkc) : type_sel<FMT, 1>(bkc);
         IFQ_SLOT_END();
         IFQ_MFMA(1);
-        read_bfrag2(nstg, nkk, lane, st.bf[f ^ 1], 2);
+        read_bfrag1(nstg, nkk, lane, st.bf[f ^ 1], 1);
         wd_s1<FMT, true>(st.bw[2 * kk], bts, b0);
         IFQ_SLOT_END();
         IFQ_MFMA(2);
-        read_bfrag2(nstg, nkk, lane, st.bf[f ^ 1], 4);
+        read_bfrag1(nstg, nkk, lane, st.bf[f ^ 1], 2);
         wd_s2<FMT, true>(st.bw[2 * kk], bts, b0);
         IFQ_SLOT_END();
         IFQ_MFMA(3);
-        read_bfrag2(nstg, nkk, lane, st.bf[f ^ 1], 6);
+        read_bfrag1(nstg, nkk, lane, st.bf[f ^ 1], 3);
         wd_s3<FMT, true>(b0);
         IFQ_SLOT_END();
         IFQ_MFMA(4);
+        read_bfrag1(nstg, nkk, lane, st.bf[f ^ 1], 4);
         if (kk == 0) {
             if constexpr (j == 1) copy_b_chunk<BITS, 0, 1>(x, cb, CS ^ 1);
             else read_a_scales<SPG>(x, min(c + 1, x.nch - 1), arow_local, h, st.as[CS ^ 1]);
@@ -1464,14 +1464,17 @@ __device__ __forceinline__ void step(const Ctx& x, StateF<FMT>& st, int s, int64
         if (SPG == 1 && (kk & 1)) wd_s4<FMT, 1, true>(b0, bkc, v0); else wd_s4<FMT, 0, true>(b0, bkc, v0);
         IFQ_SLOT_END();
         IFQ_MFMA(5);
+        read_bfrag1(nstg, nkk, lane, st.bf[f ^ 1], 5);
         if constexpr (j == 1) if (kk == 0) copy_b_chunk<BITS, 1, 2>(x, cb, CS ^ 1);
         wd_s1<FMT, true>(st.bw[2 * kk + 1], bts1, b1);
         IFQ_SLOT_END();
         IFQ_MFMA(6);
+        read_bfrag1(nstg, nkk, lane, st.bf[f ^ 1], 6);
         if constexpr (j == 1) if (kk == 0) copy_b_chunk<BITS, 2, 3>(x, cb, CS ^ 1);
         wd_s2<FMT, true>(st.bw[2 * kk + 1], bts1, b1);
         IFQ_SLOT_END();
         IFQ_MFMA(7);
+        read_bfrag1(nstg, nkk, lane, st.bf[f ^ 1], 7);
         if constexpr (j == 1 && BITS == 4) if (kk == 0) copy_b_chunk<BITS, 3, 4>(x, cb, CS ^ 1);
         wd_s3<FMT, true>(b1);
         IFQ_SLOT_END();
