@@ -196,15 +196,29 @@ __device__ __forceinline__ void decode_if3_group(uint64_t bitsv, bool is_int0, u
 // FP16 operand pairs: Fold::FP * q (FP, sign-magnitude ExMy) or Fold::INT * q
 // (INT6 two's complement), times Delta, rounded once to FP16.  FP codes go
 // through the gfx950 FP6 converter (E2M3: fp6, E3M2: bf6; 32 codes per
-// instruction, the upper 16 unused) to exact FP16 values; INT codes are
-// sign-extended and turned into FP16 exactly through the bits of 1536 + q;
-// one FP16 multiply by the exact fold constant (Fold * Delta has at most 9
-// significant bits) rounds the product once, as the FP32 product rounded to
-// FP16 would.
+// instruction, the upper 16 unused) to exact FP16 values; INT codes become
+// FP16 exactly through the bits of 1056 + q (int6_pair); one FP16 multiply by
+// the exact fold constant (Fold * Delta has at most 9 significant bits)
+// rounds the product once, as the FP32 product rounded to FP16 would.
 typedef int v6i32 __attribute__((ext_vector_type(6)));
 typedef _Float16 v32f16 __attribute__((ext_vector_type(32)));
 
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// Codes 2i and 2i + 1 of an INT6 group as an exact FP16 pair (q, q'): the
+// pair's 12 bits lie in half HI of x, code 2i at bit S0 and code 2i + 1 at
+// bit S1 of that half.  One packed shift moves each code to bit 0 of its
+// lane; the mask keeps its six bits, and the exclusive or flips its sign bit
+// (n ^ 32 = q + 32 in [0, 63]) and sets the exponent of 1024, whose ulp is 1:
+// the lane reads 1056 + q, and one subtraction leaves q.
+template <int HI, int S0, int S1>
+__device__ __forceinline__ half2v int6_pair(uint32_t x)
+{
+    const unsigned short s = HI ? (unsigned short)(x >> 16) : (unsigned short)x;
+    const u16x2 v = u16x2{s, s} >> u16x2{(unsigned short)S0, (unsigned short)S1};
+    const uint32_t b = (__builtin_bit_cast(uint32_t, v) & 0x003F003Fu) ^ 0x64206420u;
+    return __builtin_bit_cast(half2v, b) - half2v{(_Float16)1056.0f, (_Float16)1056.0f};
+}
 
 template <int FMT>
 __device__ __forceinline__ void decode_if6_group(const uint32_t* w, bool is_int, uint32_t k2, uint32_t (&out)[8])
@@ -221,41 +235,26 @@ __device__ __forceinline__ void decode_if6_group(const uint32_t* w, bool is_int,
         f = __builtin_amdgcn_cvt_scalef32_pk32_f16_fp6(src, 1.0f);
     else
         f = __builtin_amdgcn_cvt_scalef32_pk32_f16_bf6(src, 1.0f);
-    // code j at bits 6j: codes 5 (bits 30-35) and 10 (bits 60-65) straddle words
-    const uint32_t x5 = __builtin_amdgcn_alignbit(w[1], w[0], 30);
-    const uint32_t x10 = __builtin_amdgcn_alignbit(w[2], w[1], 28);
-    const u16x2 bias = {0x6600, 0x6600};          // 1536 in FP16: ulp 1 on [1024, 2048)
-    const half2v off = {(_Float16)1536.0f, (_Float16)1536.0f};
-    int q[16];
+    // pair i = codes 2i, 2i + 1 at bits 12 i .. 12 i + 11: pairs 0, 3, 4 and
+    // 7 lie in one half of a word; xa = bits 8-39 holds pairs 1 and 2, xb =
+    // bits 56-87 pairs 5 and 6
+    const uint32_t xa = __builtin_amdgcn_alignbit(w[1], w[0], 8);
+    const uint32_t xb = __builtin_amdgcn_alignbit(w[2], w[1], 24);
+    half2v hv[8];
+    hv[0] = int6_pair<0, 0, 6>(w[0]);
+    hv[1] = int6_pair<0, 4, 10>(xa);
+    hv[2] = int6_pair<1, 0, 6>(xa);
+    hv[3] = int6_pair<0, 4, 10>(w[1]);
+    hv[4] = int6_pair<1, 0, 6>(w[1]);
+    hv[5] = int6_pair<0, 4, 10>(xb);
+    hv[6] = int6_pair<1, 0, 6>(xb);
+    hv[7] = int6_pair<1, 4, 10>(w[2]);
+    // the group's own pair and constant, then one rounding of their product
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-        if (j < 5) q[j] = __builtin_amdgcn_sbfe((int)w[0], 6 * j, 6);
-        else if (j == 5) q[j] = __builtin_amdgcn_sbfe((int)x5, 0, 6);
-        else if (j < 10) q[j] = __builtin_amdgcn_sbfe((int)w[1], 6 * j - 32, 6);
-        else if (j == 10) q[j] = __builtin_amdgcn_sbfe((int)x10, 0, 6);
-        else q[j] = __builtin_amdgcn_sbfe((int)w[2], 6 * j - 64, 6);
-    }
-    // the INT6 pairs as FP16: bits of 1536 + q (exact), minus 1536; two
-    // pairs side by side, so that no packed operation waits on the one
-    // before it
-#pragma unroll
-    for (int i = 0; i < 8; i += 2) {
-        half2v hv[2], fv[2];
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            const u16x2 qq = __builtin_bit_cast(
-                u16x2, __builtin_amdgcn_perm((uint32_t)q[2 * (i + e) + 1], (uint32_t)q[2 * (i + e)], 0x05040100u));
-            hv[e] = __builtin_bit_cast(half2v, qq + bias);
-            fv[e] = half2v{f[2 * (i + e)], f[2 * (i + e) + 1]};
-        }
-#pragma unroll
-        for (int e = 0; e < 2; ++e) hv[e] = hv[e] - off;
-        // the group's own pair and constant, then one rounding of their product
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            const uint32_t x = (h2_as_u32(hv[e]) & im) | (h2_as_u32(fv[e]) & ~im);
-            out[i + e] = h2_as_u32(u32_as_h2(x) * KS);
-        }
+    for (int i = 0; i < 8; ++i) {
+        const half2v fv = {f[2 * i], f[2 * i + 1]};
+        const uint32_t x = (h2_as_u32(hv[i]) & im) | (h2_as_u32(fv) & ~im);
+        out[i] = h2_as_u32(u32_as_h2(x) * KS);
     }
 }
 
