@@ -166,6 +166,21 @@ __device__ __forceinline__ void decode_word(uint32_t w, bool is_int, uint32_t k2
     for (int i = 0; i < 4; ++i) out[i] = h2_as_u32(__builtin_elementwise_fma(u32_as_h2(x[i]), K, C));
 }
 
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// The four three-bit codes in bits 0-11 of t, one per byte (code k in bits
+// 0-2 of byte k, the other bits zero), as v_perm selectors; bits of t above
+// 11 are ignored.  One packed shift makes the 16-bit lanes bits 0-15 and
+// 6-15 of t (codes 0 and 2 at bit 0 of their lane, codes 1 and 3 at bit 3);
+// a shift of the word by 5 moves codes 1 and 3 to bytes 1 and 3, and the
+// masks keep each code's three bits.
+__device__ __forceinline__ uint32_t spread3x4(uint32_t t)
+{
+    const unsigned short s = (unsigned short)t;
+    const uint32_t y = __builtin_bit_cast(uint32_t, u16x2{s, s} >> u16x2{0, 6});
+    return (y & 0x00070007u) | ((y << 5) & 0x07000700u);
+}
+
 // Sixteen three-bit IF3 codes (48 bits) -> 8 FP16 operand pairs: 3 q (FP) or
 // 4 q (INT), times Delta (at most 6 significant bits, exact).  Codes 0-7 use
 // (is_int0, k20), codes 8-15 (is_int1, k21): the same for block size 16.
@@ -184,8 +199,7 @@ __device__ __forceinline__ void decode_if3_group(uint64_t bitsv, bool is_int0, u
     for (int q = 0; q < 4; ++q) {
         const bool is_int = q < 2 ? is_int0 : is_int1;
         const half2v K = u32_as_h2(q < 2 ? k20 : k21);
-        const uint32_t t = (uint32_t)(bitsv >> (12 * q)) & 0xFFFu;
-        const uint32_t sel = (t & 7u) | ((t << 5) & 0x700u) | ((t << 10) & 0x70000u) | ((t << 15) & 0x7000000u);
+        const uint32_t sel = spread3x4((uint32_t)(bitsv >> (12 * q)));
         const uint32_t e = __builtin_amdgcn_perm(is_int ? kIntHi : kFpHi, is_int ? kIntLo : kFpLo, sel);
         out[2 * q] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(e, 1.0f, false) * K);
         out[2 * q + 1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(e, 1.0f, true) * K);
@@ -202,8 +216,6 @@ __device__ __forceinline__ void decode_if3_group(uint64_t bitsv, bool is_int0, u
 // rounds the product once, as the FP32 product rounded to FP16 would.
 typedef int v6i32 __attribute__((ext_vector_type(6)));
 typedef _Float16 v32f16 __attribute__((ext_vector_type(32)));
-
-typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 
 // Codes 2i and 2i + 1 of an INT6 group as an exact FP16 pair (q, q'): the
 // pair's 12 bits lie in half HI of x, code 2i at bit S0 and code 2i + 1 at
@@ -380,17 +392,12 @@ struct WordDec {
 constexpr uint32_t kIf3FpLo = 0x544C4400u, kIf3FpHi = 0xD4CCC480u;
 constexpr uint32_t kIf3IntLo = 0x54504800u, kIf3IntHi = 0xC8D0D4D8u;
 
-__device__ __forceinline__ uint32_t if3_sel(uint32_t t)
-{
-    return (t & 7u) | ((t << 5) & 0x700u) | ((t << 10) & 0x70000u) | ((t << 15) & 0x7000000u);
-}
-
 template <int FMT, bool PIN>
 __device__ __forceinline__ void wd_s1(uint32_t w, const TypeSel& ts, WordDec& s)
 {
     if constexpr (Fmt<FMT>::BITS == 3) {
         s.w = w;
-        s.d0 = if3_sel(w);
+        s.d0 = spread3x4(w);
         pin<PIN>(s.d0);
     } else if constexpr (Fmt<FMT>::KIND == kKindInt) {
         s.d0 = (w & 0x0F0F0F0Fu) ^ 0x08080808u;
@@ -430,7 +437,7 @@ template <int FMT, bool PIN>
 __device__ __forceinline__ void wd_s3(WordDec& s)
 {
     if constexpr (Fmt<FMT>::BITS == 3) {
-        s.d1 = if3_sel(s.w >> 12);   // codes 4-7
+        s.d1 = spread3x4(s.w >> 12);   // codes 4-7
         pin<PIN>(s.d1);
     } else if constexpr (Fmt<FMT>::KIND == kKindInt || Fmt<FMT>::ADAPTIVE) {
         s.x[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp8(s.d0, 1.0f, false));
