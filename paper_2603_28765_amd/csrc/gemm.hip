@@ -818,10 +818,14 @@ __device__ __forceinline__ void gemm_step(int s, int nsteps, const uint8_t* __re
 #pragma unroll
             for (int j = 0; j < 8; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(st.af[gg][i][par], st.bf[f][j], acc[i][j], 0, 0, 0);
+        // VALU operations placed after each MFMA: the slice's decode spread
+        // over its 16 MFMAs (IF6 and IF3 with block size 8 decode about 7 per
+        // MFMA, the other formats of this kernel at most 6)
+        constexpr int kValu = (Fmt<FMT>::BITS == 6 || (Fmt<FMT>::BITS == 3 && Fmt<FMT>::G == 8)) ? 8 : 6;
 #pragma unroll
         for (int m = 0; m < 16; ++m) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, kValu, 0);
             if (m < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             if (m == 3 || m == 7) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
         }
