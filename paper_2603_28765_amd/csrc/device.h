@@ -584,6 +584,74 @@ __device__ __forceinline__ uint32_t quantize_group_e2m1(const float (&v)[kGroup]
     return dcode | (use_int ? 0x80u : 0u);
 }
 
+// Block size 8 (IF4-BS8, NVFP4-BS8) with round-to-nearest: the arithmetic
+// of quantize_group over one block of 8 values with the candidates of
+// quantize_group_e2m1 (FP from the E2M1 converter, INT by the biased
+// rounding); returns the scale byte and the block's 8 codes in one word
+// (code j in nibble j).
+template <bool ADAPTIVE>
+__device__ __forceinline__ uint32_t quantize_block8_e2m1(const float (&v)[8], float alpha, const Div& denom,
+                                                         uint32_t& word)
+{
+    constexpr float C_UP = 7.0f / 6.0f, K_DN = 6.0f / 7.0f;
+    float amax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(v[j]));
+    float delta;
+    const uint32_t dcode = group_scale<false>(amax, denom, delta);
+    const float s = alpha * delta;
+    if (!(s >= 1.17549435e-38f)) {
+        word = 0;
+        return 0;
+    }
+    const float inv = recip_scale<false>(s, denom);
+    float xb[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) xb[j] = v[j] * inv;
+    uint32_t f = 0;
+    f = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f, xb[0], xb[1], 1.0f, 0);
+    f = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f, xb[2], xb[3], 1.0f, 1);
+    f = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f, xb[4], xb[5], 1.0f, 2);
+    f = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f, xb[6], xb[7], 1.0f, 3);
+    if constexpr (!ADAPTIVE) {
+        word = f;
+        return dcode;
+    }
+    float q[8];
+    {
+        typedef float f2 __attribute__((ext_vector_type(2)));
+        f2 t;
+        t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(f, 1.0f, 0); q[0] = t[0]; q[1] = t[1];
+        t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(f, 1.0f, 1); q[2] = t[0]; q[3] = t[1];
+        t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(f, 1.0f, 2); q[4] = t[0]; q[5] = t[1];
+        t = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(f, 1.0f, 3); q[6] = t[0]; q[7] = t[1];
+    }
+    float ef = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float d = q[j] - xb[j];
+        ef = __builtin_fmaf(d, d, ef);
+    }
+    float ei = 0.0f;
+    uint32_t tb[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float xc = __builtin_amdgcn_fmed3f(xb[j], -6.0f, 6.0f);
+        const float t = __builtin_fmaf(xc, C_UP, 12582912.0f);
+        tb[j] = __float_as_uint(t);
+        const float d = __builtin_fmaf(t - 12582912.0f, K_DN, -xb[j]);
+        ei = __builtin_fmaf(d, d, ei);
+    }
+    const uint32_t e = __builtin_amdgcn_perm(tb[2], tb[0], 0x0C0C0400u) |
+                       __builtin_amdgcn_perm(tb[6], tb[4], 0x04000C0Cu);
+    const uint32_t o = __builtin_amdgcn_perm(tb[3], tb[1], 0x0C0C0400u) |
+                       __builtin_amdgcn_perm(tb[7], tb[5], 0x04000C0Cu);
+    const uint32_t ic = (e & 0x0F0F0F0Fu) | ((o << 4) & 0xF0F0F0F0u);
+    const bool use_int = ei < ef;
+    word = use_int ? ic : f;
+    return dcode | (use_int ? 0x80u : 0u);
+}
+
 // ------------------------------------------------------------ NVINT4
 // INT4 elements scaled straight to 7 (Sec. 2, Table 1): Delta =
 // E4M3(max|X_g| / (alpha * 7)), q = the nearest integer to x-bar clamped to
@@ -966,7 +1034,18 @@ __device__ __forceinline__ uint32_t quantize_any(const float (&v)[kGroup], float
     using F = Fmt<FMT>;
     constexpr int BITS = F::BITS;
     const bool rtn_type = (qflags & kQSrRtnType) != 0;
-    if constexpr (F::G == 8) {
+    if constexpr (F::G == 8 && BITS == 4 && !SR) {
+        // two blocks of 8; returns both scale bytes, low byte first
+        float v0[8], v1[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            v0[j] = v[j];
+            v1[j] = v[8 + j];
+        }
+        const uint32_t b0 = quantize_block8_e2m1<F::ADAPTIVE>(v0, alpha, denom, out.w[0]);
+        const uint32_t b1 = quantize_block8_e2m1<F::ADAPTIVE>(v1, alpha, denom, out.w[1]);
+        return b0 | (b1 << 8);
+    } else if constexpr (F::G == 8) {
         // two groups of 8 (scale bytes 2 gi and 2 gi + 1, which are also their
         // SR counters); returns both scale bytes, low byte first
         constexpr int B = Base<FMT>::F;
