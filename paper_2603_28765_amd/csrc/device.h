@@ -652,6 +652,54 @@ __device__ __forceinline__ uint32_t quantize_block8_e2m1(const float (&v)[8], fl
     return dcode | (use_int ? 0x80u : 0u);
 }
 
+// IF3 (and IF3-BS8 per block of 8) with round-to-nearest: the arithmetic of
+// quantize_group with fewer steps.  The E2M0 candidate comes straight from
+// the three midpoint comparisons as its value q in {0, 1, 2, 4} (ties to the
+// even code: 0.5 -> 0, 1.5 -> 2, 3 -> 2), its code index is the frexp
+// exponent of q (0, 1, 2, 3), and its error uses q - |x-bar| (the signed
+// difference negated exactly); the INT3 code is the low three bits of the
+// biased float of the rounded value.  Codes come out one per element.
+template <int N>
+__device__ __forceinline__ uint32_t quantize_group_e2m0(const float (&v)[N], float alpha, const Div& denom,
+                                                        uint32_t (&code)[N])
+{
+    constexpr float C_UP = 3.0f / 4.0f, K_DN = 4.0f / 3.0f;
+    float amax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < N; ++j) amax = fmaxf(amax, fabsf(v[j]));
+    float delta;
+    const uint32_t dcode = group_scale<false>(amax, denom, delta);
+    const float s = alpha * delta;
+    if (!(s >= 1.17549435e-38f)) {
+#pragma unroll
+        for (int j = 0; j < N; ++j) code[j] = 0;
+        return 0;
+    }
+    const float inv = recip_scale<false>(s, denom);
+    float ef = 0.0f, ei = 0.0f;
+    uint32_t cf[N], ci[N];
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+        const float xb = v[j] * inv;
+        const float m = fabsf(xb);
+        float q = m > 0.5f ? 1.0f : 0.0f;
+        q = m >= 1.5f ? 2.0f : q;
+        q = m > 3.0f ? 4.0f : q;
+        cf[j] = ((__float_as_uint(xb) >> 29) & 4u) | (uint32_t)__builtin_amdgcn_frexp_expf(q);
+        const float d = q - m;
+        ef = __builtin_fmaf(d, d, ef);
+        const float xc = __builtin_amdgcn_fmed3f(xb, -4.0f, 4.0f);
+        const float t = __builtin_fmaf(xc, C_UP, 12582912.0f);  // rint(xc * 3/4) + 1.5 * 2^23
+        ci[j] = __float_as_uint(t) & 7u;
+        const float di = __builtin_fmaf(t - 12582912.0f, K_DN, -xb);
+        ei = __builtin_fmaf(di, di, ei);
+    }
+    const bool use_int = ei < ef;
+#pragma unroll
+    for (int j = 0; j < N; ++j) code[j] = use_int ? ci[j] : cf[j];
+    return dcode | (use_int ? 0x80u : 0u);
+}
+
 // ------------------------------------------------------------ NVINT4
 // INT4 elements scaled straight to 7 (Sec. 2, Table 1): Delta =
 // E4M3(max|X_g| / (alpha * 7)), q = the nearest integer to x-bar clamped to
@@ -801,6 +849,17 @@ template <> struct Packed<3> { uint32_t w[2]; };  // 48 bits: w[0] full, w[1] lo
 template <int BITS> __device__ __forceinline__ Packed<BITS> pack16(const uint32_t (&c)[kGroup])
 {
     Packed<BITS> p;
+    if constexpr (BITS == 3) {
+        // 32-bit shifts only (code 10 straddles the words)
+        uint32_t w0 = c[0], w1 = c[10] >> 2;
+#pragma unroll
+        for (int j = 1; j < 11; ++j) w0 |= c[j] << (3 * j);
+#pragma unroll
+        for (int j = 11; j < kGroup; ++j) w1 |= c[j] << (3 * j - 32);
+        p.w[0] = w0;
+        p.w[1] = w1;
+        return p;
+    }
     uint64_t lo = 0, hi = 0;
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) {
@@ -1045,6 +1104,23 @@ __device__ __forceinline__ uint32_t quantize_any(const float (&v)[kGroup], float
         const uint32_t b0 = quantize_block8_e2m1<F::ADAPTIVE>(v0, alpha, denom, out.w[0]);
         const uint32_t b1 = quantize_block8_e2m1<F::ADAPTIVE>(v1, alpha, denom, out.w[1]);
         return b0 | (b1 << 8);
+    } else if constexpr (F::G == 8 && BITS == 3 && !SR) {
+        float v0[8], v1[8];
+        uint32_t c0[8], c1[8], c[kGroup];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            v0[j] = v[j];
+            v1[j] = v[8 + j];
+        }
+        const uint32_t b0 = quantize_group_e2m0<8>(v0, alpha, denom, c0);
+        const uint32_t b1 = quantize_group_e2m0<8>(v1, alpha, denom, c1);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            c[j] = c0[j];
+            c[8 + j] = c1[j];
+        }
+        out = pack16<3>(c);
+        return b0 | (b1 << 8);
     } else if constexpr (F::G == 8) {
         // two groups of 8 (scale bytes 2 gi and 2 gi + 1, which are also their
         // SR counters); returns both scale bytes, low byte first
@@ -1106,6 +1182,11 @@ __device__ __forceinline__ uint32_t quantize_any(const float (&v)[kGroup], float
         return sb;
     } else if constexpr (BITS == 6 && !SR) {
         return quantize_group_fp6<FMT>(v, alpha, denom, out);
+    } else if constexpr (BITS == 3 && !SR) {
+        uint32_t c[kGroup];
+        const uint32_t sb = quantize_group_e2m0<kGroup>(v, alpha, denom, c);
+        out = pack16<3>(c);
+        return sb;
     } else {
         uint32_t c[kGroup];
         const uint32_t sb = (SR && rtn_type) ? quantize_group<FMT, SR, true>(v, alpha, denom, w, c)
