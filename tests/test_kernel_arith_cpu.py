@@ -12,7 +12,10 @@ straightforward forms, checked on the CPU in binary32
   taken from one 16-bit half of a word or of an aligned copy, shifted per
   lane, masked, its sign bit flipped under the exponent of 1024 and 1056
   subtracted, against the codes read by their definition (code j at bits
-  6j .. 6j + 5 of the group's 96 bits), for every 12-bit pair value.
+  6j .. 6j + 5 of the group's 96 bits), for every 12-bit pair value;
+- the GEMM's IF3 selector spread: four 3-bit codes to one byte each by a
+  packed 16-bit shift, a word shift and two masks, against the codes read
+  by their definition, for every 16-bit input under random upper bits.
 
 The sampled strides keep this to a few seconds; stride 1 (every value) was
 run too and found no difference."""
@@ -104,3 +107,13 @@ def test_int6_pair_decode():
         assert not np.signbit(a[code(2 * i) == 0]).any()
         checked += int((pos == i).sum())
     assert checked == n
+
+
+def test_if3_selector_spread():
+    rng = np.random.default_rng(11)
+    t = np.arange(1 << 16, dtype=np.uint64) | (rng.integers(0, 1 << 16, 1 << 16, dtype=np.uint64) << np.uint64(16))
+    s = t & np.uint64(0xFFFF)
+    y = s | ((s >> np.uint64(6)) << np.uint64(16))           # lanes: s >> 0, s >> 6
+    got = (y & np.uint64(0x00070007)) | (((y << np.uint64(5)) & np.uint64(0xFFFFFFFF)) & np.uint64(0x07000700))
+    want = sum(((t >> np.uint64(3 * k)) & np.uint64(7)) << np.uint64(8 * k) for k in range(4))
+    assert np.array_equal(got, want)
