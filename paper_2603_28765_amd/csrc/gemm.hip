@@ -33,6 +33,7 @@
 // two K steps ahead.  LDS rows hold 64 halves padded to 144 bytes, so the 16
 // lanes of a 128-bit access phase touch disjoint banks and every address is a
 // per-lane base plus an immediate.
+#include <atomic>
 #include <type_traits>
 
 #include "device.h"
@@ -840,12 +841,32 @@ __device__ __forceinline__ void gemm_step(int s, int nsteps, const uint8_t* __re
 template <int FMT, bool OUT_BF16, bool EDGE>
 __device__ __forceinline__ void store_tile(const floatx16 (&acc)[2][8], const float* __restrict__ a_ts,
                                            const float* __restrict__ b_ts, int64_t M, int64_t N,
-                                           void* __restrict__ C, int64_t ldc, int64_t m0, int64_t n0)
+                                           void* __restrict__ C, int64_t ldc, int64_t m0, int64_t n0,
+                                           bool add = false)
 {
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     const int h = lane >> 5;
     const float sc = (*a_ts * *b_ts) * Fold<FMT>::EPI;
+    if constexpr (!OUT_BF16 && !EDGE) {
+        if (add) {
+            // one K half of a split tile: its share of the product, added into
+            // the zeroed output by the hardware atomic
+            float* c = static_cast<float*>(C);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int64_t n = n0 + j * 32 + (lane & 31);
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const int64_t m = m0 + 64 * wave + i * 32 + (e >> 2) * 8 + h * 4 + (e & 3);
+                        unsafeAtomicAdd(c + m * ldc + n, acc[i][j][e] * sc);
+                    }
+                }
+            return;
+        }
+    }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
 #pragma unroll
@@ -946,11 +967,8 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ a_codes,
 // ids, and tile ids are ordered in bands of 4 tile rows (column-major inside
 // a band), so the 32 workgroups resident on one XCD form a 4 x 8 block of
 // tiles that share A and B rows in its L2.
-__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn)
+__device__ __forceinline__ void band_tile(int tile, int tiles_m, int tiles_n, int& tm, int& tn)
 {
-    const int nwg = gridDim.x;
-    const int bid = blockIdx.x;
-    const int tile = (nwg % 8 == 0) ? (bid % 8) * (nwg / 8) + bid / 8 : bid;
     constexpr int GM = 4;
     const int band = tile / (GM * tiles_n);
     const int first_m = band * GM;
@@ -958,6 +976,39 @@ __device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, i
     const int in_band = tile - band * GM * tiles_n;
     tm = first_m + in_band % gm;
     tn = in_band / gm;
+}
+
+__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn)
+{
+    const int nwg = gridDim.x;
+    const int bid = blockIdx.x;
+    const int tile = (nwg % 8 == 0) ? (bid % 8) * (nwg / 8) + bid / 8 : bid;
+    band_tile(tile, tiles_m, tiles_n, tm, tn);
+}
+
+// Split tail (fast path, fp32 output): tiles [0, t_full) run whole, tiles
+// [t_full, t_full + t_split) as two halves of K each, whose products are
+// added into the zeroed output.  With t_full % 8 == 0 and t_split % 4 == 0,
+// every XCD takes t_full / 8 whole tiles (a contiguous range, first) and
+// t_split / 4 halves, so the halves fill the last round on every XCD;
+// otherwise blocks take whole tiles, then halves, in order.  Returns the
+// tile; half = -1 for a whole tile, else the K half.
+__device__ __forceinline__ int split_tile(int t_full, int t_split, int& half)
+{
+    const int nwg = gridDim.x, bid = blockIdx.x;
+    half = -1;
+    if (t_split == 0) return (nwg % 8 == 0) ? (bid % 8) * (nwg / 8) + bid / 8 : bid;
+    int j;
+    if (t_full % 8 == 0 && t_split % 4 == 0) {
+        const int x = bid % 8, p = bid / 8, fpx = t_full / 8;
+        if (p < fpx) return x * fpx + p;
+        j = x * (t_split / 4) + (p - fpx);
+    } else {
+        if (bid < t_full) return bid;
+        j = bid - t_full;
+    }
+    half = j & 1;
+    return t_full + (j >> 1);
 }
 
 // ------------------------------------------------------- fast interior path
@@ -1606,8 +1657,11 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
                                      const float* __restrict__ a_ts, const uint8_t* __restrict__ b_codes,
                                      const uint8_t* __restrict__ b_scales, const float* __restrict__ b_ts,
                                      int64_t M, int64_t N, int64_t K, void* __restrict__ C, int64_t ldc,
-                                     int64_t m0, int64_t n0, uint8_t* dec, uint8_t* raw, uint8_t* scl)
+                                     int64_t m0, int64_t n0, uint8_t* dec, uint8_t* raw, uint8_t* scl,
+                                     int64_t k0, int64_t klen, bool add)
 {
+    // K values [k0, k0 + klen) of the rows (k0 and klen multiples of 512);
+    // the row pitches come from the whole K
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     const int h = lane >> 5;
@@ -1622,17 +1676,17 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
     x.b_scales = b_scales;
     x.rowb = K * BITS / 8;
     x.gpr = SPG * (K / kGroup);
-    x.nch = (int)(K / 128);
-    x.nsc = (int)(K / (512 / SPG));
+    x.nch = (int)(klen / 128);
+    x.nsc = (int)(klen / (512 / SPG));
     x.m0 = m0;
     x.n0 = n0;
     x.dec = dec;
     x.raw = raw;
     x.scl = scl;
-    x.a_row0 = a_codes + m0 * x.rowb;
-    x.b_row0 = b_codes + n0 * x.rowb;
-    x.as_row0 = a_scales + m0 * x.gpr;
-    x.bs_row0 = b_scales + n0 * x.gpr;
+    x.a_row0 = a_codes + m0 * x.rowb + k0 * BITS / 8;
+    x.b_row0 = b_codes + n0 * x.rowb + k0 * BITS / 8;
+    x.as_row0 = a_scales + m0 * x.gpr + SPG * (k0 / kGroup);
+    x.bs_row0 = b_scales + n0 * x.gpr + SPG * (k0 / kGroup);
     x.wave = __builtin_amdgcn_readfirstlane(wave);
     x.lds_raw = __builtin_amdgcn_readfirstlane(lds_off(raw));
     x.lds_scl = __builtin_amdgcn_readfirstlane(lds_off(scl));
@@ -1657,7 +1711,7 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
 #pragma unroll
     for (int i = 0; i < 2; ++i)
         x.va[i] = (uint32_t)((arow_local + 32 * i) * x.rowb) + (BITS == 3 ? 24u : 32u) * (uint32_t)h;
-    const int nsteps = (int)(K / kBK);
+    const int nsteps = (int)(klen / kBK);
 
     floatx16 acc[2][8];
 #pragma unroll
@@ -1723,7 +1777,7 @@ __device__ __forceinline__ void tile(const uint8_t* __restrict__ a_codes, const 
         vm_drain(st.a, st.a3);
     else
         vm_drain(st.a);
-    store_tile<FMT, OUT_BF16, false>(acc, a_ts, b_ts, M, N, C, ldc, m0, n0);
+    store_tile<FMT, OUT_BF16, false>(acc, a_ts, b_ts, M, N, C, ldc, m0, n0, add);
 }
 
 }  // namespace fast
@@ -1736,15 +1790,33 @@ void gemm_tn_fast(const uint8_t* __restrict__ a_codes, const uint8_t* __restrict
                   const float* __restrict__ a_ts, const uint8_t* __restrict__ b_codes,
                   const uint8_t* __restrict__ b_scales, const float* __restrict__ b_ts,
                   int64_t M, int64_t N, int64_t K, void* __restrict__ C, int64_t ldc,
-                  int tiles_m, int tiles_n)
+                  int tiles_m, int tiles_n, int t_full, int t_split)
 {
     __shared__ __attribute__((aligned(16))) uint8_t dec[3 * fast::kStageBytes];
     __shared__ __attribute__((aligned(16))) uint8_t raw[2 * fast::kRawBytesF<Fmt<FMT>::BITS>];
     __shared__ __attribute__((aligned(16))) uint8_t scl[2 * fast::kSclBytes];
+    int half;
+    const int tile = split_tile(t_full, OUT_BF16 ? 0 : t_split, half);
     int tm, tn;
-    tile_coords(tiles_m, tiles_n, tm, tn);
+    band_tile(tile, tiles_m, tiles_n, tm, tn);
+    const int64_t klen = half < 0 ? K : K / 2;
     fast::tile<FMT, OUT_BF16>(a_codes, a_scales, a_ts, b_codes, b_scales, b_ts, M, N, K, C, ldc,
-                              (int64_t)tm * kBM, (int64_t)tn * kBN, dec, raw, scl);
+                              (int64_t)tm * kBM, (int64_t)tn * kBN, dec, raw, scl,
+                              half > 0 ? klen : 0, klen, half >= 0);
+}
+
+// Zeroes the output tiles [t_full, t_full + gridDim.x) of the band order
+// (fp32, ldc % 4 == 0, 16-byte aligned C), ahead of the split halves' atomic
+// additions.
+__global__ __launch_bounds__(256) void zero_split_tiles(float* __restrict__ C, int64_t ldc, int t_full,
+                                                        int tiles_m, int tiles_n)
+{
+    int tm, tn;
+    band_tile(t_full + (int)blockIdx.x, tiles_m, tiles_n, tm, tn);
+    float* base = C + (int64_t)tm * kBM * ldc + (int64_t)tn * kBN;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const float4 z = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int r = wave; r < kBM; r += 4) reinterpret_cast<float4*>(base + (int64_t)r * ldc)[lane] = z;
 }
 
 // Interior tiles: every row, column and K group in range (K % 128 == 0,
@@ -1790,6 +1862,21 @@ void gemm_tn_edge(const uint8_t* __restrict__ a_codes, const uint8_t* __restrict
                                    ldc, (int64_t)tm * kBM, (int64_t)tn * kBN, lds);
 }
 
+// Compute units of the current device, cached per device (a racing first
+// query repeats the same answer); 0 when it cannot be read.
+static int device_cus()
+{
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+        cache[dev].store(v, std::memory_order_relaxed);
+    }
+    return v;
+}
+
 template <int FMT>
 static hipError_t launch_g(const GemmArgs& a, hipStream_t s)
 {
@@ -1820,10 +1907,31 @@ static hipError_t launch_g(const GemmArgs& a, hipStream_t s)
         // one per 16 (IF3 with block size 8 spills there and runs the general
         // kernel)
         if constexpr (Fmt<FMT>::BITS == 4 || (Fmt<FMT>::BITS == 3 && Fmt<FMT>::G == 16)) {
+            // fp32 output: when the last round of tiles would leave at least
+            // half of the compute units idle, those tiles run as two K halves
+            // each (K % 1024 == 0), added into their zeroed output
+            int t_full = (int)(full_m * full_n), t_split = 0;
+            if (fast_ok && !a.out_bf16 && (a.K % 1024) == 0 && (a.ldc % 4) == 0 &&
+                ((uintptr_t)a.c % 16) == 0) {
+                const int64_t cus = device_cus();
+                const int64_t tail = cus > 0 ? (full_m * full_n) % cus : 0;
+                if (tail > 0 && 2 * tail <= cus) {
+                    t_split = (int)tail;
+                    t_full -= t_split;
+                }
+            }
+            if (t_split > 0) {
+                hipLaunchKernelGGL(zero_split_tiles, dim3((unsigned)t_split), dim3(256), 0, s,
+                                   static_cast<float*>(a.c), a.ldc, t_full, (int)full_m, (int)full_n);
+                hipError_t e = hipGetLastError();
+                if (e != hipSuccess) return e;
+            }
+            const dim3 fgrid((unsigned)(t_full + 2 * t_split));
             if (fast_ok && a.out_bf16)
-                hipLaunchKernelGGL((gemm_tn_fast<FMT, true>), grid, block, 0, s, IFQ_GEMM_ARGS);
+                hipLaunchKernelGGL((gemm_tn_fast<FMT, true>), fgrid, block, 0, s, IFQ_GEMM_ARGS, t_full, 0);
             else if (fast_ok)
-                hipLaunchKernelGGL((gemm_tn_fast<FMT, false>), grid, block, 0, s, IFQ_GEMM_ARGS);
+                hipLaunchKernelGGL((gemm_tn_fast<FMT, false>), fgrid, block, 0, s, IFQ_GEMM_ARGS, t_full,
+                                   t_split);
             done = fast_ok;
         }
         if (!done && a.out_bf16)

@@ -74,6 +74,16 @@ def test_checker_finds_the_pattern():
     assert vmem_violations(fixed, 1, 3) == []
 
 
+def _loop_bounds(body):
+    """(header, back edge) of the K loop: the line of the label marked
+    "Inner Loop Header" and the last conditional branch back to it."""
+    header = next(i for i, ln in enumerate(body) if "Inner Loop Header" in ln)
+    label = body[header].split(":")[0].strip()
+    back = max(i for i, ln in enumerate(body)
+               if ln.strip().startswith("s_cbranch_") and ln.split()[-1] == label and i > header)
+    return header, back
+
+
 @pytest.fixture(scope="module")
 def gemm_asm(tmp_path_factory):
     hipcc = _build.hipcc()
@@ -95,9 +105,7 @@ def test_fast_gemm_kernels_have_no_pending_load_hazards(gemm_asm):
     for name in names:
         start = gemm_asm.index(name + ":")
         body = gemm_asm[start: gemm_asm.index(".Lfunc_end", start)].split("\n")
-        header = next(i for i, ln in enumerate(body) if "Inner Loop Header" in ln)
-        back = max(i for i, ln in enumerate(body)
-                   if ln.strip().startswith("s_cbranch_scc1") and i > header)
+        header, back = _loop_bounds(body)
         loads = sum(1 for ln in body if "global_load_dwordx4 v[" in ln or "global_load_dwordx2 v[" in ln)
         assert loads >= 16, (name, loads)
         bad = vmem_violations(body, header, back)
@@ -158,9 +166,7 @@ def test_fast_gemm_copies_are_drained_within_one_barrier_period(gemm_asm):
     for name in names:
         start = gemm_asm.index(name + ":")
         body = gemm_asm[start: gemm_asm.index(".Lfunc_end", start)].split("\n")
-        header = next(i for i, ln in enumerate(body) if "Inner Loop Header" in ln)
-        back = max(i for i, ln in enumerate(body)
-                   if ln.strip().startswith("s_cbranch_scc1") and i > header)
+        header, back = _loop_bounds(body)
         assert sum(1 for ln in body if "global_load_lds_dwordx4" in ln) >= 6, name
         assert sum(1 for ln in body if ln.strip() == "s_barrier") >= 4, name
         bad = lds_copy_violations(body, header, back)

@@ -91,6 +91,25 @@ def test_shapes_k_multiple_of_512(fmt, dtype):
         _check(fmt, pa, oa, pb, ob, dtype, tag=f"{fmt} {M}x{N}x{K}")
 
 
+@pytest.mark.parametrize("fmt", [ops.IF4, ops.NVFP4, ops.IF3])
+def test_split_k_tail(fmt):
+    """fp32 output with K % 1024 == 0 on the fast kernel: when the last round
+    of tiles would leave at least half of the compute units idle (256 on
+    MI355X), those tiles run as two K halves added into their zeroed output.
+    3584 x 4864 (266 tiles: 256 whole, 10 split, halves taken in block order)
+    and 4352 x 4096 (272 tiles: 256 whole, 16 split, whole tiles and halves
+    spread over the XCDs); the result is also the same on a second call."""
+    rng = np.random.default_rng(90 + fmt)
+    for (M, N, K) in [(3584, 4864, 1024), (4352, 4096, 1024)]:
+        a = workloads.to_bf16(rng.standard_t(3, (M, K)))
+        b = workloads.to_bf16(rng.standard_normal((N, K)) * 0.02)
+        pa, oa, pb, ob = _quantized_pair(fmt, a, b)
+        _check(fmt, pa, oa, pb, ob, ops.F32, tag=f"{fmt} {M}x{N}x{K}")
+        c1 = ops.ifx_gemm(pa, pb, ops.F32)
+        c2 = ops.ifx_gemm(pa, pb, ops.F32)
+        assert torch.equal(c1, c2)
+
+
 def _packed_from_arrays(fmt, codes, scales, alpha=1.0):
     R, K = codes.shape[0], scales.shape[1] * ops.GSIZE[fmt]
     ts = torch.tensor([alpha], dtype=torch.float32, device="cuda")
