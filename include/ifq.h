@@ -260,7 +260,14 @@ int ifx_dequantize(int format, const uint8_t* codes, const uint8_t* scales,
  *   a_tensor_scale, b_tensor_scale  (device) alpha of A and of B
  *   c                  (device) [M, ldc] fp32 or bf16 (out_dtype); ldc >= N
  *   code pointers 16-byte aligned; K % 16 == 0.
- * The result is deterministic for a given shape (no split-K atomics).
+ * fp32 output with K % 1024 == 0, c 16-byte aligned and ldc % 4 == 0: when
+ * the last round of 256 x 256 tiles would leave at least half of the
+ * device's compute units idle, those tiles are computed as two K halves
+ * whose shares are added by atomics into their output, zeroed first in the
+ * same stream.  A sum of two terms into zero does not depend on their order,
+ * so the result is deterministic for a given shape and device (it differs
+ * from the whole-K accumulation by one rounding); other work must not touch
+ * c while the call runs.
  */
 int if4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_tensor_scale,
              const uint8_t* b_codes, const uint8_t* b_scales, const float* b_tensor_scale,
