@@ -287,6 +287,18 @@ __device__ __forceinline__ float sr_ceil(float t, float u)
     return __builtin_ceilf(t - u);
 }
 
+// The 16-bit draw h of element j as a float (exact), and sr_ceil with u =
+// h * 2^-16 taken inside one fma: h * 2^-16 is exact, so the fma's single
+// rounding of t - h * 2^-16 is the rounding of t - u that sr_ceil takes.
+__device__ __forceinline__ float sr_draw(const uint32_t (&w)[8], int j)
+{
+    return (float)((w[j >> 1] >> (16 * (j & 1))) & 0xFFFFu);
+}
+__device__ __forceinline__ float sr_ceil_h(float t, float h)
+{
+    return __builtin_ceilf(__builtin_fmaf(h, -0x1p-16f, t));
+}
+
 // |m| with the sign of x (one bit-field insert)
 __device__ __forceinline__ float with_sign_of(float m, float x)
 {
@@ -955,18 +967,18 @@ __device__ __forceinline__ uint32_t quantize_group_e2m1_sr(const float (&v)[kGro
 #pragma unroll
     for (int j = 0; j < kGroup; ++j) {
         xb[j] = v[j] * inv;
-        const float u = sr_uniform(w, j);
+        const float h = sr_draw(w, j);
         const float m = fminf(fabsf(xb[j]), 6.0f);
         // 2^floor(log2 m) (0 for m below 2^-126), the step q and 1/q (powers of two)
         const float p2 = __uint_as_float(__float_as_uint(m) & 0x7F800000u);
         const float q = fmaxf(p2 * 0.5f, 0.5f);
         const float inv_q = __uint_as_float((254u << 23) - __float_as_uint(q));
-        qf[j] = with_sign_of(sr_ceil(m * inv_q, u) * q, xb[j]);
+        qf[j] = with_sign_of(sr_ceil_h(m * inv_q, h) * q, xb[j]);
         const float d = qf[j] - xb[j];
         ef = __builtin_fmaf(d, d, ef);
         if constexpr (ADAPTIVE) {
             const float y = xb[j] * C_UP;
-            const float r = with_sign_of(fminf(sr_ceil(fabsf(y), u), 7.0f), y);
+            const float r = with_sign_of(fminf(sr_ceil_h(fabsf(y), h), 7.0f), y);
             tb[j] = __float_as_uint(r + 12582912.0f);
             const float di = __builtin_fmaf(r, K_DN, -xb[j]);
             ei = __builtin_fmaf(di, di, ei);
